@@ -1,0 +1,186 @@
+/*
+ * scd.h -- C ABI of libscd: asynchronous stochastic coordinate descent/ascent (SCD) for
+ * generalized linear models on one AMD Instinct MI355X (gfx950).
+ *
+ * Method: Parnell, Duenner, Atasu, Sifalakis, Pozidis, "Large-Scale Stochastic Learning
+ * using GPUs" (arXiv 1702.07005).  One epoch visits every coordinate once, in a fresh
+ * random permutation (Sec. III-A, Alg. 1); many coordinates are processed concurrently,
+ * each by a group of GPU lanes that splits the coordinate's sparse inner product, reduces
+ * it, applies the closed-form coordinate step and scatters the shared-vector update with
+ * device atomics (Sec. III-C, Alg. 2, "TPA-SCD").
+ *
+ * Problem statement (Sec. II): A in R^{N x M} (N examples, M features), labels y in R^N,
+ * regularisation lambda > 0 -- the paper's lambda of eq. (primal_obj), i.e. the objectives
+ * carry the 1/N normalisation and the closed-form ridge minimiser is
+ * (A^T A + N lambda I)^{-1} A^T y.
+ *
+ * Formulations:
+ *   SCD_RIDGE_PRIMAL  coordinates = features; A given by columns (CSC); model beta in R^M;
+ *                     shared vector w = A beta in R^N.  Step: eq. (update_primal).
+ *   SCD_SVM_DUAL      coordinates = examples; A given by rows (CSR); y in {-1, +1};
+ *                     model alpha in [0,1]^N; shared vector w = sum_i alpha_i y_i x_i/(lambda N)
+ *                     in R^M.  Hinge-loss SVM, P(w) = (1/N) sum max(0, 1 - y_i x_i.w)
+ *                     + lambda/2 |w|^2, D(alpha) = (1/N) sum alpha_i - lambda/2 |w|^2; step
+ *                     alpha_i <- clip(alpha_i + lambda N (1 - y_i x_i.w)/|x_i|^2, 0, 1)
+ *                     (alpha_i <- 1 for an empty row).
+ *   SCD_RIDGE_DUAL    coordinates = examples; A given by rows (CSR); model alpha in R^N;
+ *                     shared vector wbar = A^T alpha in R^M.  Step: eq. (update_dual).
+ *
+ * Conventions shared by every call:
+ *   - Status: every call returns SCD_OK (0) or a negative scd_status_t and never aborts or
+ *     throws across the ABI; scd_last_error() gives a message for the calling thread.
+ *   - Memory: pointers named *_dev are device pointers on the handle's GPU; all others are
+ *     host pointers.  Arrays are dense and contiguous.
+ *   - Ownership: the handle BORROWS A (ptr/idx/val) and y: they must stay allocated and
+ *     unmodified until scd_destroy.  The handle owns its model, shared vector, norms and
+ *     scratch and frees them in scd_destroy.
+ *   - Streams: `stream` is a hipStream_t (NULL = the null stream).  Calls that only
+ *     enqueue work return immediately; calls that return values to the host synchronise
+ *     the stream.  A handle is not thread-safe; separate handles on separate streams are.
+ *   - Faults inside kernels surface as SCD_ERR_HIP at the next synchronising call.
+ */
+#ifndef SCD_H
+#define SCD_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef struct scd_solver *scd_handle_t;
+
+typedef enum {
+    SCD_RIDGE_PRIMAL = 0,
+    SCD_SVM_DUAL = 1,
+    SCD_RIDGE_DUAL = 2
+} scd_formulation_t;
+
+typedef enum {
+    SCD_CSC = 0, /* segments are columns: ptr has n_cols+1 entries, idx are row indices   */
+    SCD_CSR = 1  /* segments are rows:    ptr has n_rows+1 entries, idx are column indices */
+} scd_layout_t;
+
+typedef enum {
+    SCD_OK = 0,
+    SCD_ERR_INVALID = -1,     /* bad argument, inconsistent matrix, wrong layout for the formulation */
+    SCD_ERR_UNSUPPORTED = -2, /* valid request this build does not implement (e.g. unknown option)   */
+    SCD_ERR_OOM = -3,         /* device or pinned-host allocation failed                              */
+    SCD_ERR_HIP = -4,         /* a HIP runtime call failed (includes earlier kernel faults)           */
+    SCD_ERR_NUMERIC = -5      /* non-finite input values or a non-finite objective                    */
+} scd_status_t;
+
+/* A sparse matrix in compressed form, stored on the device.
+ *   ptr: int64[S+1], S = n_cols (CSC) or n_rows (CSR); ptr[0] = 0, non-decreasing, ptr[S] = nnz.
+ *   idx: int32[nnz], 0-based, in [0, n_rows) for CSC and [0, n_cols) for CSR.
+ *   val: float32[nnz], finite.
+ * Duplicate indices inside one segment are allowed (they act as a sum). */
+typedef struct {
+    int64_t n_rows;
+    int64_t n_cols;
+    int64_t nnz;
+    int32_t layout; /* scd_layout_t */
+    int32_t reserved;
+    const int64_t *ptr;
+    const int32_t *idx;
+    const float *val;
+} scd_matrix_t;
+
+/* Read-only facts about a handle. */
+typedef struct {
+    int32_t formulation;  /* scd_formulation_t                                        */
+    int32_t group_lanes;  /* lanes per coordinate of the epoch kernel (1024 = ordered) */
+    int64_t n_coords;     /* C: M for SCD_RIDGE_PRIMAL, N for the duals                */
+    int64_t shared_len;   /* length of the shared vector: N (ridge primal) or M         */
+    int64_t nnz;
+    int64_t epoch;        /* global epoch counter (epochs run so far)                  */
+    int64_t max_segment;  /* longest coordinate segment                                */
+    int64_t window;       /* coordinates in flight at most (persistent groups)         */
+    double lambda;
+} scd_info_t;
+
+/* Create a solver for min P / max D of the chosen formulation (Sec. II; Sec. III-C).
+ *   A:       device matrix; layout must be SCD_CSC for SCD_RIDGE_PRIMAL and SCD_CSR otherwise.
+ *   y_dev:   float32[n_rows] labels (device); for SCD_SVM_DUAL every label is -1 or +1.
+ *   lambda:  the paper's normalised lambda (> 0, finite).
+ *   stream:  hipStream_t used for the set-up work; the call synchronises it.
+ * Validates A and y on the device (one pass), computes |a_c|^2 for every coordinate and sets
+ * model = 0, shared vector = 0 (Alg. 1/2 initialisation), epoch = 0.
+ * Errors: SCD_ERR_INVALID (null/negative sizes, wrong layout, ptr not monotone, index out of
+ * range, labels not +-1 for the SVM, lambda <= 0), SCD_ERR_NUMERIC (non-finite values or labels),
+ * SCD_ERR_OOM, SCD_ERR_HIP.  On error *out is set to NULL. */
+int scd_create(const scd_matrix_t *A, const float *y_dev, double lambda, int32_t formulation,
+               void *stream, scd_handle_t *out);
+
+/* Free everything the handle owns (not A or y).  NULL-safe.  Synchronises the device. */
+int scd_destroy(scd_handle_t h);
+
+/* Run n_epochs >= 0 epochs (Alg. 1 epochs executed as in Alg. 2): epoch t (global counter,
+ * continued across calls) visits the coordinates in the order pi_{seed,t} of
+ * scd_permutation; each visit is the exact coordinate step of the formulation against the
+ * shared vector as it stands, followed by an atomic scatter of the change into the shared
+ * vector.  Up to `window` coordinates are in flight at once (option "window"); window = 1
+ * reproduces the sequential order of Alg. 1 exactly.  Enqueues only. */
+int scd_epochs(scd_handle_t h, uint64_t seed, int32_t n_epochs, void *stream);
+
+/* Primal and dual objective of the current state, in fp64 (synchronises):
+ *   SCD_RIDGE_PRIMAL: P(beta) of eq. (primal_obj) and D((y - w)/N) of eq. (dual_obj), with the
+ *                     maintained shared vector w standing in for A beta (Sec. II-C).
+ *   SCD_RIDGE_DUAL:   P(wbar/lambda) and D(alpha) (Sec. II-C), wbar = maintained A^T alpha.
+ *   SCD_SVM_DUAL:     P(w) and D(alpha) of the hinge SVM, w = maintained shared vector.
+ * Either output pointer may be NULL. */
+int scd_objective(scd_handle_t h, void *stream, double *primal, double *dual);
+
+/* Duality gap |P - D| of the current state (Sec. II-C: G_P for the ridge primal, G_D for the
+ * ridge dual; P - D >= 0 for the SVM).  Synchronises. */
+int scd_duality_gap(scd_handle_t h, void *stream, double *gap);
+
+/* Copy the state out (device buffers, may be NULL to skip):
+ *   model_dev:  float32[n_coords]   (beta, or alpha)
+ *   shared_dev: float32[shared_len] (w = A beta, or w(alpha), or wbar = A^T alpha)
+ *   epoch:      host int64 (may be NULL).  Enqueues only. */
+int scd_get_state(scd_handle_t h, float *model_dev, float *shared_dev, int64_t *epoch, void *stream);
+
+/* Overwrite the state (resume from a checkpoint).  model_dev/shared_dev as in scd_get_state
+ * (NULL leaves that part unchanged); epoch >= 0 sets the global epoch counter.
+ * The caller is responsible for shared = function of model (invariant of Sec. II-A/B).
+ * Enqueues only. */
+int scd_set_state(scd_handle_t h, const float *model_dev, const float *shared_dev, int64_t epoch,
+                  void *stream);
+
+/* Tuning and test options (host-side, take effect at the next scd_epochs):
+ *   "window"      coordinates in flight at most; 0 = as many as the GPU holds (default), 1 = ordered.
+ *   "group"       lanes per coordinate: 0 = by segment length (default), 4, 8, 16, 32, 64, or
+ *                 256 (one workgroup per coordinate).
+ *   "fresh_reads" 1 = gather the shared vector with device-scope loads (bypass non-coherent
+ *                 caches), 0 = plain loads.
+ * Errors: SCD_ERR_UNSUPPORTED for an unknown key, SCD_ERR_INVALID for a bad value. */
+int scd_set_option(scd_handle_t h, const char *key, int64_t value);
+int scd_get_option(scd_handle_t h, const char *key, int64_t *value);
+
+int scd_get_info(scd_handle_t h, scd_info_t *info);
+
+/* out_dev[c] = sum over coordinate c's segment of val * u_dev[idx]  (float32, c < n_coords):
+ * the sparse gather-dot of the epoch kernel (the inner product of eq. update_primal /
+ * update_dual) against a frozen vector u_dev[shared_len].  Enqueues only. */
+int scd_gather_dots(scd_handle_t h, const float *u_dev, float *out_dev, void *stream);
+
+/* out_dev[c] = |a_c|^2 (float32[n_coords]): the squared segment norms used by every step. */
+int scd_norms(scd_handle_t h, float *out_dev, void *stream);
+
+/* The visiting order of epoch `epoch`: out_dev[j] = pi_{seed,epoch}(j), j < n (int32[n]),
+ * 1 <= n < 2^31.  pi is a 4-round balanced Feistel network on 2h bits (h >= 1 smallest with
+ * 2^(2h) >= n), round function fmix32(R xor k_r) mod 2^h (MurmurHash3 finaliser), round keys
+ * k_r = low 32 bits of SplitMix64 output r+1 from state b, b = SplitMix64 output epoch+1 from
+ * state seed, values outside [0, n) re-encrypted until inside (cycle-walking).  The paper only
+ * asks for a fresh random permutation per epoch (Alg. 1, Alg. 2).  Enqueues only. */
+int scd_permutation(uint64_t seed, int64_t epoch, int64_t n, int32_t *out_dev, void *stream);
+
+/* Message describing the last error on the calling thread ("" if none). */
+const char *scd_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* SCD_H */

@@ -1,0 +1,495 @@
+// scd_api.cpp -- the C ABI of include/scd.h: handle lifecycle, validation, launch planning,
+// objectives and state.  All compute runs in the HIP kernels of scd_kernels.hip.
+#include <hip/hip_runtime.h>
+
+#include <cmath>
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+#include <new>
+#include <string>
+
+#include "scd.h"
+#include "scd_kernels.h"
+
+using namespace scd;
+
+namespace {
+
+thread_local std::string g_err;
+
+int fail(int code, const char* fmt, ...) {
+    char buf[512];
+    va_list ap;
+    va_start(ap, fmt);
+    vsnprintf(buf, sizeof buf, fmt, ap);
+    va_end(ap);
+    g_err = buf;
+    return code;
+}
+
+#define HIP_TRY(expr)                                                                            \
+    do {                                                                                         \
+        hipError_t e_ = (expr);                                                                  \
+        if (e_ != hipSuccess)                                                                    \
+            return fail(e_ == hipErrorOutOfMemory ? SCD_ERR_OOM : SCD_ERR_HIP, "%s: %s (%s:%d)", \
+                        #expr, hipGetErrorString(e_), __FILE__, __LINE__);                       \
+    } while (0)
+
+// SplitMix64 (Steele, Lea, Flood 2014): output n (n >= 1) of the generator started at state s.
+uint64_t splitmix64(uint64_t s, uint64_t n) {
+    uint64_t z = s + 0x9E3779B97F4A7C15ULL * n;
+    z = (z ^ (z >> 30)) * 0xBF58476D1CE4E5B9ULL;
+    z = (z ^ (z >> 27)) * 0x94D049BB133111EBULL;
+    return z ^ (z >> 31);
+}
+
+PermKeys make_perm(uint64_t seed, uint64_t epoch, uint32_t n) {
+    PermKeys p{};
+    const uint64_t base = splitmix64(seed, epoch + 1);
+    for (int r = 0; r < 4; ++r) p.k[r] = (uint32_t)splitmix64(base, (uint64_t)r + 1);
+    uint32_t h = 1;
+    while (h < 16 && ((uint64_t)1 << (2 * h)) < (uint64_t)n) ++h;
+    p.h = h;
+    p.mask = (1u << h) - 1u;
+    p.n = n;
+    return p;
+}
+
+// Register-cache depth of the group kernels (elements per lane kept between gather and scatter).
+int cached_per_lane(int G) { return G <= 4 ? 4 : G <= 16 ? 6 : G == 32 ? 5 : 4; }
+
+constexpr int kBlockThreads = 256;
+constexpr int kBlocksPerCU = 8;
+constexpr int kObjBlocksMax = 2048;
+
+}  // namespace
+
+struct scd_solver {
+    int form = 0;
+    int64_t n_rows = 0, n_cols = 0, nnz = 0, C = 0, L = 0;
+    const int64_t* ptr = nullptr;
+    const int32_t* idx = nullptr;
+    const float* val = nullptr;
+    const float* y = nullptr;
+    double lambda = 0.0;
+    float* model = nullptr;
+    float* u = nullptr;
+    float* norms = nullptr;
+    int* flags = nullptr;
+    double* partials = nullptr;
+    double* sums = nullptr;
+    double* host_sums = nullptr;  // pinned
+    int64_t epoch = 0;
+    int device = 0;
+    int cus = 0;
+    size_t max_lds = 0;
+    int64_t max_seg = 0;
+    // options
+    int64_t window = 0;
+    int64_t group = 0;
+    int64_t fresh = 0;
+};
+
+namespace {
+
+int auto_group(const scd_solver* h) {
+    const double mean = h->C > 0 ? (double)h->nnz / (double)h->C : 0.0;
+    const int widths[5] = {4, 8, 16, 32, 64};
+    for (int G : widths)
+        if (mean <= (double)(G * cached_per_lane(G))) return G;
+    return kBlockThreads;  // one workgroup per coordinate
+}
+
+int plan_epoch(const scd_solver* h, LaunchPlan* lp, uint32_t* n_groups) {
+    memset(lp, 0, sizeof *lp);
+    lp->fresh = (int)h->fresh;
+    const int G = h->group ? (int)h->group : auto_group(h);
+    if (h->window == 1) {
+        const size_t need = ((size_t)((h->L + 63) & ~int64_t(63)) + 2 * 16) * sizeof(float);
+        if (need <= h->max_lds) {
+            lp->kind = PLAN_ORDERED_LDS;
+            lp->L = (uint32_t)h->L;
+            lp->lds_bytes = need;
+            lp->blocks = 1;
+            *n_groups = 1;
+            return SCD_OK;
+        }
+        lp->kind = PLAN_BLOCK;
+        lp->ordered = 1;
+        lp->fresh = 1;
+        lp->blocks = 1;
+        *n_groups = 1;
+        return SCD_OK;
+    }
+    const int64_t cap_blocks = (int64_t)h->cus * kBlocksPerCU;
+    if (G == kBlockThreads) {
+        int64_t groups = cap_blocks;
+        if (h->window > 0 && h->window < groups) groups = h->window;
+        if (groups > h->C) groups = h->C;
+        if (groups < 1) groups = 1;
+        lp->kind = PLAN_BLOCK;
+        lp->blocks = (int)groups;
+        *n_groups = (uint32_t)groups;
+        return SCD_OK;
+    }
+    const int64_t per_block = kBlockThreads / G;
+    int64_t groups = cap_blocks * per_block;
+    if (h->window > 0 && h->window < groups) groups = h->window;
+    if (groups > h->C) groups = h->C;
+    if (groups < 1) groups = 1;
+    lp->kind = PLAN_GROUP;
+    lp->group = G;
+    lp->blocks = (int)((groups + per_block - 1) / per_block);
+    *n_groups = (uint32_t)groups;
+    return SCD_OK;
+}
+
+int obj_group(const scd_solver* h) {
+    const int G = h->group ? (int)h->group : auto_group(h);
+    return G > 64 ? 64 : G;
+}
+
+int obj_blocks(const scd_solver* h, int G) {
+    int64_t b = (h->C * G + kBlockThreads - 1) / kBlockThreads;
+    if (b > kObjBlocksMax) b = kObjBlocksMax;
+    if (b < 1) b = 1;
+    return (int)b;
+}
+
+int check_handle(scd_handle_t h) {
+    if (!h) return fail(SCD_ERR_INVALID, "null handle");
+    return SCD_OK;
+}
+
+int set_device(const scd_solver* h) {
+    int cur = -1;
+    HIP_TRY(hipGetDevice(&cur));
+    if (cur != h->device) HIP_TRY(hipSetDevice(h->device));
+    return SCD_OK;
+}
+
+void release(scd_solver* h) {
+    if (!h) return;
+    (void)hipFree(h->model);
+    (void)hipFree(h->u);
+    (void)hipFree(h->norms);
+    (void)hipFree(h->flags);
+    (void)hipFree(h->partials);
+    (void)hipFree(h->sums);
+    if (h->host_sums) (void)hipHostFree(h->host_sums);
+    delete h;
+}
+
+// Compute the five reduction sums of the current state into h->host_sums (synchronises).
+int reduce_state(scd_solver* h, hipStream_t s) {
+    ObjArgs o{};
+    o.ptr = h->ptr;
+    o.idx = h->idx;
+    o.val = h->val;
+    o.u = h->u;
+    o.model = h->model;
+    o.y = h->form == FORM_RIDGE_PRIMAL ? nullptr : h->y;
+    o.yv = h->form == FORM_RIDGE_PRIMAL ? h->y : nullptr;
+    o.C = (uint32_t)h->C;
+    o.L = h->L;
+    o.lam = h->lambda;
+    const int G = obj_group(h);
+    const int blocks = obj_blocks(h, G);
+    HIP_TRY(launch_objective(h->form, o, G, blocks, h->partials, h->sums, s));
+    HIP_TRY(hipMemcpyAsync(h->host_sums, h->sums, 5 * sizeof(double), hipMemcpyDeviceToHost, s));
+    HIP_TRY(hipStreamSynchronize(s));
+    return SCD_OK;
+}
+
+void objectives_from_sums(const scd_solver* h, double* P, double* D) {
+    const double* t = h->host_sums;
+    const double N = (double)h->n_rows, lam = h->lambda;
+    if (h->form == FORM_RIDGE_PRIMAL) {
+        // t0 = sum_m <a_m, r>^2, t1 = |beta|^2, t3 = |r|^2, t4 = <r, y>,  r = y - A beta.
+        *P = t[3] / (2.0 * N) + 0.5 * lam * t[1];
+        *D = -t[3] / (2.0 * N) - t[0] / (2.0 * lam * N * N) + t[4] / N;
+    } else if (h->form == FORM_SVM_DUAL) {
+        // t0 = sum hinge, t1 = sum alpha, t3 = |w|^2.
+        *P = t[0] / N + 0.5 * lam * t[3];
+        *D = t[1] / N - 0.5 * lam * t[3];
+    } else {
+        // t0 = |A wbar / lambda - y|^2, t1 = |alpha|^2, t2 = <alpha, y>, t3 = |wbar|^2.
+        *P = t[0] / (2.0 * N) + 0.5 * t[3] / lam;
+        *D = -0.5 * N * t[1] - t[3] / (2.0 * lam) + t[2];
+    }
+}
+
+}  // namespace
+
+extern "C" {
+
+const char* scd_last_error(void) { return g_err.c_str(); }
+
+int scd_create(const scd_matrix_t* A, const float* y, double lambda, int32_t formulation, void* stream,
+               scd_handle_t* out) {
+    g_err.clear();
+    if (!out) return fail(SCD_ERR_INVALID, "out is null");
+    *out = nullptr;
+    if (!A) return fail(SCD_ERR_INVALID, "matrix is null");
+    if (formulation < SCD_RIDGE_PRIMAL || formulation > SCD_RIDGE_DUAL)
+        return fail(SCD_ERR_INVALID, "unknown formulation %d", (int)formulation);
+    const int want = formulation == SCD_RIDGE_PRIMAL ? SCD_CSC : SCD_CSR;
+    if (A->layout != want)
+        return fail(SCD_ERR_INVALID, "formulation %d needs layout %s", (int)formulation,
+                    want == SCD_CSC ? "CSC (columns = coordinates)" : "CSR (rows = coordinates)");
+    if (A->n_rows < 1 || A->n_cols < 1 || A->nnz < 0)
+        return fail(SCD_ERR_INVALID, "bad sizes n_rows=%lld n_cols=%lld nnz=%lld", (long long)A->n_rows,
+                    (long long)A->n_cols, (long long)A->nnz);
+    if (A->n_rows > 2147483647LL || A->n_cols > 2147483647LL)
+        return fail(SCD_ERR_INVALID, "dimensions must be below 2^31");
+    if (!A->ptr || (A->nnz > 0 && (!A->idx || !A->val)) || !y)
+        return fail(SCD_ERR_INVALID, "null device pointer");
+    if (!(lambda > 0.0) || !std::isfinite(lambda)) return fail(SCD_ERR_INVALID, "lambda must be finite and > 0");
+
+    scd_solver* h = new (std::nothrow) scd_solver;
+    if (!h) return fail(SCD_ERR_OOM, "host allocation failed");
+    h->form = formulation;
+    h->n_rows = A->n_rows;
+    h->n_cols = A->n_cols;
+    h->nnz = A->nnz;
+    h->C = formulation == SCD_RIDGE_PRIMAL ? A->n_cols : A->n_rows;
+    h->L = formulation == SCD_RIDGE_PRIMAL ? A->n_rows : A->n_cols;
+    h->ptr = A->ptr;
+    h->idx = A->idx;
+    h->val = A->val;
+    h->y = y;
+    h->lambda = lambda;
+    hipStream_t s = (hipStream_t)stream;
+
+    int rc = SCD_OK;
+    auto step = [&](int r) { if (rc == SCD_OK) rc = r; return rc == SCD_OK; };
+    auto hip = [&](hipError_t e, const char* what) {
+        if (rc != SCD_OK) return false;
+        if (e != hipSuccess) rc = fail(e == hipErrorOutOfMemory ? SCD_ERR_OOM : SCD_ERR_HIP, "%s: %s", what,
+                                       hipGetErrorString(e));
+        return rc == SCD_OK;
+    };
+    hip(hipGetDevice(&h->device), "hipGetDevice");
+    if (rc == SCD_OK) {
+        hipDeviceProp_t prop;
+        if (hip(hipGetDeviceProperties(&prop, h->device), "hipGetDeviceProperties")) {
+            h->cus = prop.multiProcessorCount > 0 ? prop.multiProcessorCount : 1;
+            h->max_lds = prop.sharedMemPerBlock;
+            int v = 0;
+            if (hipDeviceGetAttribute(&v, hipDeviceAttributeMaxSharedMemoryPerBlock, h->device) == hipSuccess &&
+                (size_t)v > h->max_lds)
+                h->max_lds = (size_t)v;
+        }
+    }
+    hip(hipMalloc(&h->model, sizeof(float) * (size_t)h->C), "hipMalloc(model)");
+    hip(hipMalloc(&h->u, sizeof(float) * (size_t)h->L), "hipMalloc(shared)");
+    hip(hipMalloc(&h->norms, sizeof(float) * (size_t)h->C), "hipMalloc(norms)");
+    hip(hipMalloc(&h->flags, 2 * sizeof(int64_t)), "hipMalloc(flags)");
+    hip(hipMalloc(&h->partials, sizeof(double) * (size_t)kObjBlocksMax * 5), "hipMalloc(partials)");
+    hip(hipMalloc(&h->sums, sizeof(double) * 8), "hipMalloc(sums)");
+    hip(hipHostMalloc(&h->host_sums, sizeof(double) * 8, hipHostMallocDefault), "hipHostMalloc");
+
+    // Validation pass over ptr, idx, val and y.
+    int64_t fl[2] = {0, 0};  // validation bits, longest segment
+    hip(hipMemsetAsync(h->flags, 0, 2 * sizeof(int64_t), s), "hipMemsetAsync(flags)");
+    hip(launch_validate(h->ptr, (uint32_t)h->C, h->idx, h->val, h->nnz, h->L, h->y, h->n_rows,
+                        formulation == SCD_SVM_DUAL, h->flags, s),
+        "validate");
+    hip(hipMemcpyAsync(fl, h->flags, 2 * sizeof(int64_t), hipMemcpyDeviceToHost, s), "copy flags");
+    hip(hipStreamSynchronize(s), "synchronize");
+    const int flags = (int)(fl[0] & 0xFFFFFFFF);
+    h->max_seg = fl[1];
+    if (rc == SCD_OK && flags) {
+        if (flags & 1) step(fail(SCD_ERR_INVALID, "ptr must start at 0, end at nnz and be non-decreasing"));
+        else if (flags & 2) step(fail(SCD_ERR_INVALID, "an index is outside [0, %lld)", (long long)h->L));
+        else if (flags & 16) step(fail(SCD_ERR_INVALID, "SVM labels must be -1 or +1"));
+        else step(fail(SCD_ERR_NUMERIC, "non-finite matrix value or label"));
+    }
+    if (rc == SCD_OK) {
+        const int G = obj_group(h);
+        hip(launch_norms(h->ptr, h->val, (uint32_t)h->C, G, obj_blocks(h, G), h->norms, s), "norms");
+        hip(hipMemsetAsync(h->model, 0, sizeof(float) * (size_t)h->C, s), "zero model");
+        if (formulation == SCD_RIDGE_PRIMAL)  // beta = 0: w = 0, residual r = y
+            hip(hipMemcpyAsync(h->u, h->y, sizeof(float) * (size_t)h->L, hipMemcpyDeviceToDevice, s), "r = y");
+        else
+            hip(hipMemsetAsync(h->u, 0, sizeof(float) * (size_t)h->L, s), "zero shared");
+        hip(hipStreamSynchronize(s), "synchronize");
+    }
+    if (rc != SCD_OK) {
+        release(h);
+        return rc;
+    }
+    *out = h;
+    return SCD_OK;
+}
+
+int scd_destroy(scd_handle_t h) {
+    if (!h) return SCD_OK;
+    const int dev = h->device;
+    int cur = -1;
+    (void)hipGetDevice(&cur);
+    if (cur != dev) (void)hipSetDevice(dev);
+    hipError_t e = hipDeviceSynchronize();
+    release(h);
+    if (cur >= 0 && cur != dev) (void)hipSetDevice(cur);
+    if (e != hipSuccess) return fail(SCD_ERR_HIP, "hipDeviceSynchronize: %s", hipGetErrorString(e));
+    return SCD_OK;
+}
+
+int scd_epochs(scd_handle_t h, uint64_t seed, int32_t n_epochs, void* stream) {
+    if (int r = check_handle(h)) return r;
+    if (n_epochs < 0) return fail(SCD_ERR_INVALID, "n_epochs must be >= 0");
+    if (int r = set_device(h)) return r;
+    LaunchPlan lp;
+    uint32_t n_groups = 1;
+    if (int r = plan_epoch(h, &lp, &n_groups)) return r;
+    if (lp.kind == PLAN_ORDERED_LDS) HIP_TRY(ordered_lds_prepare(h->form, lp.lds_bytes));
+    EpochArgs a{};
+    a.ptr = h->ptr;
+    a.idx = h->idx;
+    a.val = h->val;
+    a.y = h->y;
+    a.model = h->model;
+    a.u = h->u;
+    a.norms = h->norms;
+    const double lamN = h->lambda * (double)h->n_rows;
+    a.k.lamN = (float)lamN;
+    a.k.inv_lamN = (float)(1.0 / lamN);
+    a.k.lam = (float)h->lambda;
+    a.n_groups = n_groups;
+    hipStream_t s = (hipStream_t)stream;
+    for (int32_t e = 0; e < n_epochs; ++e) {
+        a.perm = make_perm(seed, (uint64_t)h->epoch, (uint32_t)h->C);
+        HIP_TRY(launch_epoch(h->form, a, lp, s));
+        ++h->epoch;
+    }
+    return SCD_OK;
+}
+
+int scd_objective(scd_handle_t h, void* stream, double* primal, double* dual) {
+    if (int r = check_handle(h)) return r;
+    if (int r = set_device(h)) return r;
+    if (int r = reduce_state(h, (hipStream_t)stream)) return r;
+    double P, D;
+    objectives_from_sums(h, &P, &D);
+    if (!std::isfinite(P) || !std::isfinite(D)) return fail(SCD_ERR_NUMERIC, "non-finite objective (P=%g, D=%g)", P, D);
+    if (primal) *primal = P;
+    if (dual) *dual = D;
+    return SCD_OK;
+}
+
+int scd_duality_gap(scd_handle_t h, void* stream, double* gap) {
+    if (!gap) return fail(SCD_ERR_INVALID, "gap is null");
+    double P = 0, D = 0;
+    if (int r = scd_objective(h, stream, &P, &D)) return r;
+    *gap = h->form == FORM_SVM_DUAL ? P - D : std::fabs(P - D);
+    return SCD_OK;
+}
+
+int scd_get_state(scd_handle_t h, float* model, float* shared, int64_t* epoch, void* stream) {
+    if (int r = check_handle(h)) return r;
+    if (int r = set_device(h)) return r;
+    hipStream_t s = (hipStream_t)stream;
+    if (model) HIP_TRY(hipMemcpyAsync(model, h->model, sizeof(float) * (size_t)h->C, hipMemcpyDeviceToDevice, s));
+    if (shared) {
+        if (h->form == FORM_RIDGE_PRIMAL)
+            HIP_TRY(launch_sub(h->y, h->u, h->L, shared, s));  // w = y - r
+        else
+            HIP_TRY(hipMemcpyAsync(shared, h->u, sizeof(float) * (size_t)h->L, hipMemcpyDeviceToDevice, s));
+    }
+    if (epoch) *epoch = h->epoch;
+    return SCD_OK;
+}
+
+int scd_set_state(scd_handle_t h, const float* model, const float* shared, int64_t epoch, void* stream) {
+    if (int r = check_handle(h)) return r;
+    if (epoch < 0) return fail(SCD_ERR_INVALID, "epoch must be >= 0");
+    if (int r = set_device(h)) return r;
+    hipStream_t s = (hipStream_t)stream;
+    if (model) HIP_TRY(hipMemcpyAsync(h->model, model, sizeof(float) * (size_t)h->C, hipMemcpyDeviceToDevice, s));
+    if (shared) {
+        if (h->form == FORM_RIDGE_PRIMAL)
+            HIP_TRY(launch_sub(h->y, shared, h->L, h->u, s));  // r = y - w
+        else
+            HIP_TRY(hipMemcpyAsync(h->u, shared, sizeof(float) * (size_t)h->L, hipMemcpyDeviceToDevice, s));
+    }
+    h->epoch = epoch;
+    return SCD_OK;
+}
+
+int scd_set_option(scd_handle_t h, const char* key, int64_t value) {
+    if (int r = check_handle(h)) return r;
+    if (!key) return fail(SCD_ERR_INVALID, "key is null");
+    if (!strcmp(key, "window")) {
+        if (value < 0 || value > 2147483647LL) return fail(SCD_ERR_INVALID, "window must be in [0, 2^31)");
+        h->window = value;
+    } else if (!strcmp(key, "group")) {
+        if (!(value == 0 || value == 4 || value == 8 || value == 16 || value == 32 || value == 64 ||
+              value == kBlockThreads))
+            return fail(SCD_ERR_INVALID, "group must be 0, 4, 8, 16, 32, 64 or 256");
+        h->group = value;
+    } else if (!strcmp(key, "fresh_reads")) {
+        if (value != 0 && value != 1) return fail(SCD_ERR_INVALID, "fresh_reads must be 0 or 1");
+        h->fresh = value;
+    } else {
+        return fail(SCD_ERR_UNSUPPORTED, "unknown option '%s'", key);
+    }
+    return SCD_OK;
+}
+
+int scd_get_option(scd_handle_t h, const char* key, int64_t* value) {
+    if (int r = check_handle(h)) return r;
+    if (!key || !value) return fail(SCD_ERR_INVALID, "null argument");
+    if (!strcmp(key, "window")) *value = h->window;
+    else if (!strcmp(key, "group")) *value = h->group;
+    else if (!strcmp(key, "fresh_reads")) *value = h->fresh;
+    else return fail(SCD_ERR_UNSUPPORTED, "unknown option '%s'", key);
+    return SCD_OK;
+}
+
+int scd_get_info(scd_handle_t h, scd_info_t* info) {
+    if (int r = check_handle(h)) return r;
+    if (!info) return fail(SCD_ERR_INVALID, "info is null");
+    LaunchPlan lp;
+    uint32_t n_groups = 1;
+    plan_epoch(h, &lp, &n_groups);
+    info->formulation = h->form;
+    info->group_lanes = lp.kind == PLAN_GROUP ? lp.group : lp.kind == PLAN_BLOCK && !lp.ordered ? kBlockThreads : 1024;
+    info->n_coords = h->C;
+    info->shared_len = h->L;
+    info->nnz = h->nnz;
+    info->epoch = h->epoch;
+    info->max_segment = h->max_seg;
+    info->window = n_groups;
+    info->lambda = h->lambda;
+    return SCD_OK;
+}
+
+int scd_gather_dots(scd_handle_t h, const float* u, float* out, void* stream) {
+    if (int r = check_handle(h)) return r;
+    if (!u || !out) return fail(SCD_ERR_INVALID, "null device pointer");
+    if (int r = set_device(h)) return r;
+    const int G = obj_group(h);
+    HIP_TRY(launch_gather_dots(h->ptr, h->idx, h->val, u, (uint32_t)h->C, G, obj_blocks(h, G), out,
+                               (hipStream_t)stream));
+    return SCD_OK;
+}
+
+int scd_norms(scd_handle_t h, float* out, void* stream) {
+    if (int r = check_handle(h)) return r;
+    if (!out) return fail(SCD_ERR_INVALID, "null device pointer");
+    if (int r = set_device(h)) return r;
+    HIP_TRY(hipMemcpyAsync(out, h->norms, sizeof(float) * (size_t)h->C, hipMemcpyDeviceToDevice, (hipStream_t)stream));
+    return SCD_OK;
+}
+
+int scd_permutation(uint64_t seed, int64_t epoch, int64_t n, int32_t* out, void* stream) {
+    if (n < 1 || n > 2147483647LL) return fail(SCD_ERR_INVALID, "n must be in [1, 2^31)");
+    if (epoch < 0) return fail(SCD_ERR_INVALID, "epoch must be >= 0");
+    if (!out) return fail(SCD_ERR_INVALID, "null device pointer");
+    HIP_TRY(launch_perm_fill(make_perm(seed, (uint64_t)epoch, (uint32_t)n), out, (hipStream_t)stream));
+    return SCD_OK;
+}
+
+}  // extern "C"

@@ -1,0 +1,80 @@
+// scd_kernels.h -- argument structures and launchers shared by the C ABI and the kernels.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace scd {
+
+enum { FORM_RIDGE_PRIMAL = 0, FORM_SVM_DUAL = 1, FORM_RIDGE_DUAL = 2 };
+
+// Keys of one epoch's permutation of [0, n): 4 Feistel round keys on 2h bits.
+struct PermKeys {
+    uint32_t k[4];
+    uint32_t h;
+    uint32_t mask;
+    uint32_t n;
+    uint32_t pad_;
+};
+
+// Constants of the closed-form steps (lambda is the paper's normalised lambda).
+struct StepConsts {
+    float lamN;      // lambda * N
+    float inv_lamN;  // 1 / (lambda * N)
+    float lam;       // lambda
+    float pad_;
+};
+
+struct EpochArgs {
+    const int64_t* ptr;
+    const int32_t* idx;
+    const float* val;
+    const float* y;      // per-coordinate labels (duals); unused by the ridge primal
+    float* model;        // [C]
+    float* u;            // shared vector [L] (residual y - A beta for the ridge primal)
+    const float* norms;  // [C]
+    StepConsts k;
+    PermKeys perm;       // perm.n = C
+    uint32_t n_groups;   // persistent groups (coordinates in flight at most)
+    uint32_t pad_;
+};
+
+enum { PLAN_GROUP = 0, PLAN_BLOCK = 1, PLAN_ORDERED_LDS = 2 };
+
+struct LaunchPlan {
+    int kind;        // PLAN_*
+    int group;       // lanes per coordinate (PLAN_GROUP)
+    int blocks;      // workgroups launched
+    int fresh;       // device-scope gathers
+    int ordered;     // PLAN_BLOCK with a single workgroup, fenced between coordinates
+    uint32_t L;      // shared-vector length (PLAN_ORDERED_LDS)
+    size_t lds_bytes;
+};
+
+struct ObjArgs {
+    const int64_t* ptr;
+    const int32_t* idx;
+    const float* val;
+    const float* u;      // shared vector as maintained
+    const float* model;
+    const float* y;      // per-coordinate labels (duals)
+    const float* yv;     // per-shared-entry labels (ridge primal: y over rows)
+    uint32_t C;
+    int64_t L;
+    double lam;
+};
+
+hipError_t launch_epoch(int form, const EpochArgs& a, const LaunchPlan& lp, hipStream_t s);
+hipError_t ordered_lds_prepare(int form, size_t lds_bytes);
+hipError_t launch_perm_fill(const PermKeys& p, int32_t* out, hipStream_t s);
+hipError_t launch_gather_dots(const int64_t* ptr, const int32_t* idx, const float* val, const float* u, uint32_t C,
+                              int G, int blocks, float* out, hipStream_t s);
+hipError_t launch_norms(const int64_t* ptr, const float* val, uint32_t C, int G, int blocks, float* out,
+                        hipStream_t s);
+hipError_t launch_validate(const int64_t* ptr, uint32_t S, const int32_t* idx, const float* val, int64_t nnz,
+                           int64_t bound, const float* y, int64_t ny, int pm1, int* flags, hipStream_t s);
+hipError_t launch_sub(const float* a, const float* b, int64_t n, float* out, hipStream_t s);
+hipError_t launch_objective(int form, const ObjArgs& o, int G, int blocks, double* partials, double* sums,
+                            hipStream_t s);
+
+}  // namespace scd

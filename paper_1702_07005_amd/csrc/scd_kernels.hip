@@ -1,0 +1,592 @@
+// scd_kernels.hip -- HIP kernels for gfx950 (CDNA4, wave64) of asynchronous stochastic
+// coordinate descent/ascent (arXiv 1702.07005, Sec. III-C "TPA-SCD", Alg. 2).
+//
+// Every coordinate c owns one segment [ptr[c], ptr[c+1]) of (idx, val): a column of A for
+// the ridge primal (CSC), a row for the duals (CSR).  One epoch = one persistent launch in
+// which groups of lanes take permutation positions j = g, g + P, g + 2P, ... (P groups in
+// flight: the "window"), and for the coordinate m = pi(j):
+//   1. gather  g = <a_m, u>   over the segment (u = the shared vector, see below),
+//   2. reduce the lane partials inside the group (DPP / swizzle, LDS across waves),
+//   3. step    closed form of the formulation -> model[m], scatter coefficient,
+//   4. scatter u[idx] += coef * val  with device-scope fp32 atomics (no return).
+//
+// Shared vector kept on the device, per formulation:
+//   ridge primal : the residual r = y - A beta (the paper's w = A beta is y - r); the step
+//                  needs <y - w, a_m> (eq. update_primal) = <r, a_m>, one gather instead of
+//                  two, and r carries the small quantity itself near the optimum.
+//   SVM dual     : w = sum_i alpha_i y_i x_i / (lambda N).
+//   ridge dual   : wbar = A^T alpha (eq. update_dual).
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "scd_kernels.h"
+
+namespace scd {
+
+// ----------------------------------------------------------------------------------------
+// Permutation: 4-round balanced Feistel network on 2h bits + cycle-walking.
+// ----------------------------------------------------------------------------------------
+__device__ __forceinline__ uint32_t murmur_fmix32(uint32_t x) {
+    x ^= x >> 16;
+    x *= 0x85EBCA6BU;
+    x ^= x >> 13;
+    x *= 0xC2B2AE35U;
+    x ^= x >> 16;
+    return x;
+}
+
+__device__ __forceinline__ uint32_t feistel4(uint32_t x, const PermKeys& p) {
+    uint32_t l = x >> p.h, r = x & p.mask, t;
+    t = l ^ (murmur_fmix32(r ^ p.k[0]) & p.mask); l = r; r = t;
+    t = l ^ (murmur_fmix32(r ^ p.k[1]) & p.mask); l = r; r = t;
+    t = l ^ (murmur_fmix32(r ^ p.k[2]) & p.mask); l = r; r = t;
+    t = l ^ (murmur_fmix32(r ^ p.k[3]) & p.mask); l = r; r = t;
+    return (l << p.h) | r;
+}
+
+__device__ __forceinline__ uint32_t perm_at(uint32_t j, const PermKeys& p) {
+    uint32_t x = feistel4(j, p);
+    while (x >= p.n) x = feistel4(x, p);
+    return x;
+}
+
+__global__ void k_perm_fill(PermKeys p, int32_t* __restrict__ out) {
+    uint32_t j = blockIdx.x * blockDim.x + threadIdx.x;
+    if (j < p.n) out[j] = (int32_t)perm_at(j, p);
+}
+
+// ----------------------------------------------------------------------------------------
+// Group reductions.  The butterfly makes every lane of the group hold the bitwise-identical
+// sum (fp add is commutative), so all lanes take the same step without a broadcast.
+// ----------------------------------------------------------------------------------------
+template <int CTRL>
+__device__ __forceinline__ float dpp_f(float x) {
+    return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(x), CTRL, 0xF, 0xF, false));
+}
+
+template <int G>
+__device__ __forceinline__ float group_sum(float x) {
+    static_assert(G == 1 || G == 2 || G == 4 || G == 8 || G == 16 || G == 32 || G == 64, "group width");
+    if constexpr (G >= 2) x += dpp_f<0xB1>(x);   // quad_perm [1,0,3,2]  (lane ^ 1)
+    if constexpr (G >= 4) x += dpp_f<0x4E>(x);   // quad_perm [2,3,0,1]  (lane ^ 2)
+    if constexpr (G >= 8) x += dpp_f<0x141>(x);  // row_half_mirror      (other quad of 8)
+    if constexpr (G >= 16) x += dpp_f<0x140>(x); // row_mirror           (other half of 16)
+    if constexpr (G >= 32) x += __int_as_float(__builtin_amdgcn_ds_swizzle(__float_as_int(x), 0x401F));  // lane ^ 16
+    if constexpr (G >= 64) {
+        float a = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(x), 0));
+        float b = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(x), 32));
+        x = a + b;
+    }
+    return x;
+}
+
+template <int G>
+__device__ __forceinline__ double group_sum_f64(double x) {
+#pragma unroll
+    for (int o = 1; o < G; o <<= 1) x += __shfl_xor(x, o, G);
+    return x;
+}
+
+// ----------------------------------------------------------------------------------------
+// Shared-vector access.
+// ----------------------------------------------------------------------------------------
+template <bool FRESH>
+__device__ __forceinline__ float ld_u(const float* p) {
+    if constexpr (FRESH)
+        return __hip_atomic_load(const_cast<float*>(p), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    else
+        return *p;
+}
+
+__device__ __forceinline__ void atomic_add_u(float* p, float v) {
+    __hip_atomic_fetch_add(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+// ----------------------------------------------------------------------------------------
+// Closed-form coordinate steps.  g = <a_m, u>, s = |a_m|^2, m_old = model[m].
+// Returns the new model value; *coef is the factor of val in the scatter u += coef * a_m.
+// ----------------------------------------------------------------------------------------
+template <int FORM>
+__device__ __forceinline__ float coord_step(float g, float s, float m_old, float ylab, const StepConsts& k,
+                                            float* coef) {
+    if constexpr (FORM == FORM_RIDGE_PRIMAL) {
+        // eq. (update_primal): d = (<y - w, a_m> - lambda N beta_m) / (|a_m|^2 + lambda N);
+        // r = y - w moves by -d a_m.
+        float d = (g - k.lamN * m_old) / (s + k.lamN);
+        *coef = -d;
+        return m_old + d;
+    } else if constexpr (FORM == FORM_SVM_DUAL) {
+        // exact maximisation of the hinge dual along alpha_i, projected on [0, 1].
+        float a = 1.0f;
+        if (s > 0.0f) a = fminf(fmaxf(m_old + k.lamN * (1.0f - ylab * g) / s, 0.0f), 1.0f);
+        *coef = (a - m_old) * ylab * k.inv_lamN;
+        return a;
+    } else {
+        // eq. (update_dual): d = (lambda y_n - <wbar, abar_n> - lambda N alpha_n) / (lambda N + |abar_n|^2).
+        float d = (k.lam * ylab - g - k.lamN * m_old) / (k.lamN + s);
+        *coef = d;
+        return m_old + d;
+    }
+}
+
+// ----------------------------------------------------------------------------------------
+// Epoch kernel, sub-wave / wave groups: G lanes per coordinate, 256-thread workgroups,
+// persistent over permutation positions.  The first R*G elements of a segment stay in
+// registers between the gather and the scatter (A is read once); longer segments stream
+// their tail twice.
+// ----------------------------------------------------------------------------------------
+template <int FORM, int G, int R, bool FRESH>
+__global__ __launch_bounds__(256) void k_epoch_group(EpochArgs a) {
+    const int lane = threadIdx.x & (G - 1);
+    const uint32_t gid = (blockIdx.x * 256u + threadIdx.x) / G;
+    if (gid >= a.n_groups) return;
+    for (uint32_t j = gid; j < a.perm.n; j += a.n_groups) {
+        const uint32_t m = perm_at(j, a.perm);
+        const int64_t s0 = a.ptr[m], s1 = a.ptr[m + 1];
+        const float m_old = a.model[m];
+        const float sn = a.norms[m];
+        const float ylab = (FORM == FORM_RIDGE_PRIMAL) ? 0.0f : a.y[m];
+        int ci[R];
+        float cv[R];
+#pragma unroll
+        for (int r = 0; r < R; ++r) {
+            const int64_t k = s0 + lane + (int64_t)r * G;
+            if (k < s1) { ci[r] = a.idx[k]; cv[r] = a.val[k]; }
+            else { ci[r] = -1; cv[r] = 0.0f; }
+        }
+        float acc = 0.0f;
+#pragma unroll
+        for (int r = 0; r < R; ++r)
+            if (ci[r] >= 0) acc = fmaf(cv[r], ld_u<FRESH>(a.u + ci[r]), acc);
+        for (int64_t k = s0 + lane + (int64_t)R * G; k < s1; k += G)
+            acc = fmaf(a.val[k], ld_u<FRESH>(a.u + a.idx[k]), acc);
+        const float g = group_sum<G>(acc);
+        float coef;
+        const float m_new = coord_step<FORM>(g, sn, m_old, ylab, a.k, &coef);
+        if (lane == 0) a.model[m] = m_new;
+        if (coef != 0.0f) {
+#pragma unroll
+            for (int r = 0; r < R; ++r)
+                if (ci[r] >= 0) atomic_add_u(a.u + ci[r], coef * cv[r]);
+            for (int64_t k = s0 + lane + (int64_t)R * G; k < s1; k += G)
+                atomic_add_u(a.u + a.idx[k], coef * a.val[k]);
+        }
+    }
+}
+
+// ----------------------------------------------------------------------------------------
+// Epoch kernel, one workgroup of BS threads per coordinate (long segments): wave sums by
+// DPP, then the BS/64 wave sums through a double-buffered LDS array (one barrier per
+// coordinate).  ORDERED adds a device-scope fence and a barrier after the scatter so that
+// with a single workgroup the next coordinate sees every update (sequential Alg. 1).
+// ----------------------------------------------------------------------------------------
+template <int FORM, int BS, int R, bool FRESH, bool ORDERED>
+__global__ __launch_bounds__(BS) void k_epoch_block(EpochArgs a) {
+    constexpr int NW = BS / 64;
+    __shared__ float part[2][NW];
+    const int tid = threadIdx.x, wave = tid >> 6;
+    int buf = 0;
+    if (blockIdx.x >= a.n_groups) return;
+    for (uint32_t j = blockIdx.x; j < a.perm.n; j += a.n_groups) {
+        const uint32_t m = perm_at(j, a.perm);
+        const int64_t s0 = a.ptr[m], s1 = a.ptr[m + 1];
+        const float m_old = a.model[m];
+        const float sn = a.norms[m];
+        const float ylab = (FORM == FORM_RIDGE_PRIMAL) ? 0.0f : a.y[m];
+        int ci[R];
+        float cv[R];
+#pragma unroll
+        for (int r = 0; r < R; ++r) {
+            const int64_t k = s0 + tid + (int64_t)r * BS;
+            if (k < s1) { ci[r] = a.idx[k]; cv[r] = a.val[k]; }
+            else { ci[r] = -1; cv[r] = 0.0f; }
+        }
+        float acc = 0.0f;
+#pragma unroll
+        for (int r = 0; r < R; ++r)
+            if (ci[r] >= 0) acc = fmaf(cv[r], ld_u<FRESH>(a.u + ci[r]), acc);
+        for (int64_t k = s0 + tid + (int64_t)R * BS; k < s1; k += BS)
+            acc = fmaf(a.val[k], ld_u<FRESH>(a.u + a.idx[k]), acc);
+        acc = group_sum<64>(acc);
+        if ((tid & 63) == 0) part[buf][wave] = acc;
+        __syncthreads();
+        float g = 0.0f;
+#pragma unroll
+        for (int w = 0; w < NW; ++w) g += part[buf][w];
+        float coef;
+        const float m_new = coord_step<FORM>(g, sn, m_old, ylab, a.k, &coef);
+        if (tid == 0) a.model[m] = m_new;
+        if (coef != 0.0f) {
+#pragma unroll
+            for (int r = 0; r < R; ++r)
+                if (ci[r] >= 0) atomic_add_u(a.u + ci[r], coef * cv[r]);
+            for (int64_t k = s0 + tid + (int64_t)R * BS; k < s1; k += BS)
+                atomic_add_u(a.u + a.idx[k], coef * a.val[k]);
+        }
+        if constexpr (ORDERED) {
+            __threadfence();
+            __syncthreads();
+        }
+        buf ^= 1;
+    }
+}
+
+// ----------------------------------------------------------------------------------------
+// Ordered epoch (window 1) with the whole shared vector resident in LDS: one workgroup of
+// 1024 threads walks the permutation in order; gathers and scatters hit LDS only
+// (ds_add_f32), two barriers per coordinate.  The shared vector is loaded at the start and
+// written back at the end of the epoch.
+// ----------------------------------------------------------------------------------------
+template <int FORM>
+__global__ __launch_bounds__(1024) void k_epoch_ordered_lds(EpochArgs a, uint32_t L) {
+    constexpr int BS = 1024, NW = BS / 64;
+    extern __shared__ float lds[];
+    float* su = lds;                    // L floats
+    float* part = lds + ((L + 63) & ~63u);  // 2 * NW floats
+    const int tid = threadIdx.x, wave = tid >> 6;
+    for (uint32_t i = tid; i < L; i += BS) su[i] = a.u[i];
+    __syncthreads();
+    int buf = 0;
+    for (uint32_t j = 0; j < a.perm.n; ++j) {
+        const uint32_t m = perm_at(j, a.perm);
+        const int64_t s0 = a.ptr[m], s1 = a.ptr[m + 1];
+        const float m_old = a.model[m];
+        const float sn = a.norms[m];
+        const float ylab = (FORM == FORM_RIDGE_PRIMAL) ? 0.0f : a.y[m];
+        float acc = 0.0f;
+        for (int64_t k = s0 + tid; k < s1; k += BS) acc = fmaf(a.val[k], su[a.idx[k]], acc);
+        acc = group_sum<64>(acc);
+        if ((tid & 63) == 0) part[buf * NW + wave] = acc;
+        __syncthreads();
+        float g = 0.0f;
+#pragma unroll
+        for (int w = 0; w < NW; ++w) g += part[buf * NW + w];
+        float coef;
+        const float m_new = coord_step<FORM>(g, sn, m_old, ylab, a.k, &coef);
+        if (tid == 0) a.model[m] = m_new;
+        if (coef != 0.0f)
+            for (int64_t k = s0 + tid; k < s1; k += BS) atomicAdd(su + a.idx[k], coef * a.val[k]);
+        __syncthreads();
+        buf ^= 1;
+    }
+    for (uint32_t i = tid; i < L; i += BS) a.u[i] = su[i];
+}
+
+// ----------------------------------------------------------------------------------------
+// Frozen gather-dot: out[c] = <a_c, u> with the epoch kernel's arithmetic (fp32 FMA per
+// lane, group butterfly), for every coordinate in index order.
+// ----------------------------------------------------------------------------------------
+template <int G>
+__global__ __launch_bounds__(256) void k_gather_dots(const int64_t* __restrict__ ptr, const int32_t* __restrict__ idx,
+                                                     const float* __restrict__ val, const float* __restrict__ u,
+                                                     uint32_t C, float* __restrict__ out) {
+    const int lane = threadIdx.x & (G - 1);
+    const uint32_t ngroups = gridDim.x * (256u / G);
+    for (uint32_t c = (blockIdx.x * 256u + threadIdx.x) / G; c < C; c += ngroups) {
+        const int64_t s0 = ptr[c], s1 = ptr[c + 1];
+        float acc = 0.0f;
+        for (int64_t k = s0 + lane; k < s1; k += G) acc = fmaf(val[k], u[idx[k]], acc);
+        acc = group_sum<G>(acc);
+        if (lane == 0) out[c] = acc;
+    }
+}
+
+// ----------------------------------------------------------------------------------------
+// Set-up: squared segment norms (fp64 accumulation, fp32 result) and input validation.
+// ----------------------------------------------------------------------------------------
+template <int G>
+__global__ __launch_bounds__(256) void k_norms(const int64_t* __restrict__ ptr, const float* __restrict__ val,
+                                               uint32_t C, float* __restrict__ out) {
+    const int lane = threadIdx.x & (G - 1);
+    const uint32_t ngroups = gridDim.x * (256u / G);
+    for (uint32_t c = (blockIdx.x * 256u + threadIdx.x) / G; c < C; c += ngroups) {
+        double acc = 0.0;
+        for (int64_t k = ptr[c] + lane; k < ptr[c + 1]; k += G) acc += (double)val[k] * (double)val[k];
+        acc = group_sum_f64<G>(acc);
+        if (lane == 0) out[c] = (float)acc;
+    }
+}
+
+// flags bits: 1 ptr not monotone / wrong ends, 2 index out of range, 4 non-finite value,
+// 8 non-finite label, 16 label not +-1.
+// flags[1] (as unsigned long long) receives the longest segment.
+__global__ void k_validate_ptr(const int64_t* __restrict__ ptr, uint32_t S, int64_t nnz, int* flags) {
+    uint32_t c = blockIdx.x * blockDim.x + threadIdx.x;
+    if (c == 0 && (ptr[0] != 0 || ptr[S] != nnz)) atomicOr(flags, 1);
+    if (c < S) {
+        const int64_t len = ptr[c + 1] - ptr[c];
+        if (len < 0) atomicOr(flags, 1);
+        else atomicMax(reinterpret_cast<unsigned long long*>(flags) + 1, (unsigned long long)len);
+    }
+}
+
+__global__ void k_validate_entries(const int32_t* __restrict__ idx, const float* __restrict__ val, int64_t nnz,
+                                   int64_t bound, int* flags) {
+    int f = 0;
+    for (int64_t k = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; k < nnz; k += (int64_t)gridDim.x * blockDim.x) {
+        const int32_t i = idx[k];
+        if (i < 0 || (int64_t)i >= bound) f |= 2;
+        if (!isfinite(val[k])) f |= 4;
+    }
+    if (f) atomicOr(flags, f);
+}
+
+__global__ void k_validate_labels(const float* __restrict__ y, int64_t n, int pm1, int* flags) {
+    int f = 0;
+    for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += (int64_t)gridDim.x * blockDim.x) {
+        const float v = y[i];
+        if (!isfinite(v)) f |= 8;
+        else if (pm1 && v != 1.0f && v != -1.0f) f |= 16;
+    }
+    if (f) atomicOr(flags, f);
+}
+
+// out = a - b (elementwise): converts between the residual r = y - w and w.
+__global__ void k_sub(const float* __restrict__ a, const float* __restrict__ b, int64_t n, float* __restrict__ out) {
+    for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += (int64_t)gridDim.x * blockDim.x)
+        out[i] = a[i] - b[i];
+}
+
+// ----------------------------------------------------------------------------------------
+// Objective / duality-gap reductions (fp64).  Coordinate pass: per coordinate the fp64 dot
+// d_c = <a_c, u> and up to three sums; vector pass: two sums over the shared vector.  Every
+// workgroup writes its partial sums; one final workgroup adds the partials in a fixed order.
+//   ridge primal (u = r = y - w):  S0 += d^2,  S1 += beta^2          | V0 += r^2, V1 += r*y
+//   svm dual     (u = w):          S0 += max(0, 1 - y d), S1 += alpha | V0 += w^2
+//   ridge dual   (u = wbar):       S0 += (d/lambda - y)^2, S1 += alpha^2, S2 += alpha*y | V0 += wbar^2
+// ----------------------------------------------------------------------------------------
+template <int NS>
+__device__ __forceinline__ void block_reduce_store(double (&v)[NS], double* out) {
+    __shared__ double red[NS][256 / 64];
+    const int tid = threadIdx.x;
+#pragma unroll
+    for (int s = 0; s < NS; ++s) {
+        double x = v[s];
+        x = group_sum_f64<64>(x);
+        if ((tid & 63) == 0) red[s][tid >> 6] = x;
+    }
+    __syncthreads();
+    if (tid == 0) {
+#pragma unroll
+        for (int s = 0; s < NS; ++s) out[s] = red[s][0] + red[s][1] + red[s][2] + red[s][3];
+    }
+}
+
+template <int FORM, int G>
+__global__ __launch_bounds__(256) void k_obj_coords(const int64_t* __restrict__ ptr, const int32_t* __restrict__ idx,
+                                                    const float* __restrict__ val, const float* __restrict__ u,
+                                                    const float* __restrict__ model, const float* __restrict__ y,
+                                                    uint32_t C, double lam, double* __restrict__ partials) {
+    const int lane = threadIdx.x & (G - 1);
+    const uint32_t ngroups = gridDim.x * (256u / G);
+    double t[3] = {0.0, 0.0, 0.0};
+    for (uint32_t c = (blockIdx.x * 256u + threadIdx.x) / G; c < C; c += ngroups) {
+        double d = 0.0;
+        for (int64_t k = ptr[c] + lane; k < ptr[c + 1]; k += G) d += (double)val[k] * (double)u[idx[k]];
+        d = group_sum_f64<G>(d);
+        if (lane == 0) {
+            const double mo = model[c];
+            if constexpr (FORM == FORM_RIDGE_PRIMAL) {
+                t[0] += d * d;
+                t[1] += mo * mo;
+            } else if constexpr (FORM == FORM_SVM_DUAL) {
+                const double l = 1.0 - (double)y[c] * d;
+                t[0] += l > 0.0 ? l : 0.0;
+                t[1] += mo;
+            } else {
+                const double e = d / lam - (double)y[c];
+                t[0] += e * e;
+                t[1] += mo * mo;
+                t[2] += mo * (double)y[c];
+            }
+        }
+    }
+    block_reduce_store<3>(t, partials + (size_t)blockIdx.x * 3);
+}
+
+template <int FORM>
+__global__ __launch_bounds__(256) void k_obj_vector(const float* __restrict__ u, const float* __restrict__ y, int64_t L,
+                                                    double* __restrict__ partials) {
+    double t[2] = {0.0, 0.0};
+    for (int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x; i < L; i += (int64_t)gridDim.x * 256) {
+        const double x = u[i];
+        t[0] += x * x;
+        if constexpr (FORM == FORM_RIDGE_PRIMAL) t[1] += x * (double)y[i];
+    }
+    block_reduce_store<2>(t, partials + (size_t)blockIdx.x * 2);
+}
+
+// Sum `nparts` rows of `width` doubles in index order (one workgroup; deterministic).
+__global__ __launch_bounds__(256) void k_sum_partials(const double* __restrict__ partials, int nparts, int width,
+                                                      double* __restrict__ out) {
+    __shared__ double sh[256];
+    for (int w = 0; w < width; ++w) {
+        double x = 0.0;
+        for (int p = threadIdx.x; p < nparts; p += 256) x += partials[(size_t)p * width + w];
+        sh[threadIdx.x] = x;
+        __syncthreads();
+        for (int s = 128; s > 0; s >>= 1) {
+            if ((int)threadIdx.x < s) sh[threadIdx.x] += sh[threadIdx.x + s];
+            __syncthreads();
+        }
+        if (threadIdx.x == 0) out[w] = sh[0];
+        __syncthreads();
+    }
+}
+
+// ----------------------------------------------------------------------------------------
+// Host-side launchers.
+// ----------------------------------------------------------------------------------------
+template <int FORM, int G, bool FRESH>
+static hipError_t launch_group(const EpochArgs& a, int blocks, hipStream_t s) {
+    constexpr int R = (G <= 4) ? 4 : (G <= 16) ? 6 : (G == 32) ? 5 : 4;
+    hipLaunchKernelGGL((k_epoch_group<FORM, G, R, FRESH>), dim3(blocks), dim3(256), 0, s, a);
+    return hipGetLastError();
+}
+
+template <int FORM, bool FRESH>
+static hipError_t launch_group_g(const EpochArgs& a, int G, int blocks, hipStream_t s) {
+    switch (G) {
+        case 4: return launch_group<FORM, 4, FRESH>(a, blocks, s);
+        case 8: return launch_group<FORM, 8, FRESH>(a, blocks, s);
+        case 16: return launch_group<FORM, 16, FRESH>(a, blocks, s);
+        case 32: return launch_group<FORM, 32, FRESH>(a, blocks, s);
+        case 64: return launch_group<FORM, 64, FRESH>(a, blocks, s);
+        default: return hipErrorInvalidValue;
+    }
+}
+
+template <int FORM>
+static hipError_t launch_epoch_form(const EpochArgs& a, const LaunchPlan& lp, hipStream_t s) {
+    if (lp.kind == PLAN_ORDERED_LDS) {
+        hipLaunchKernelGGL((k_epoch_ordered_lds<FORM>), dim3(1), dim3(1024), lp.lds_bytes, s, a, lp.L);
+        return hipGetLastError();
+    }
+    if (lp.kind == PLAN_BLOCK) {
+        if (lp.ordered) {
+            hipLaunchKernelGGL((k_epoch_block<FORM, 256, 16, true, true>), dim3(lp.blocks), dim3(256), 0, s, a);
+        } else if (lp.fresh) {
+            hipLaunchKernelGGL((k_epoch_block<FORM, 256, 16, true, false>), dim3(lp.blocks), dim3(256), 0, s, a);
+        } else {
+            hipLaunchKernelGGL((k_epoch_block<FORM, 256, 16, false, false>), dim3(lp.blocks), dim3(256), 0, s, a);
+        }
+        return hipGetLastError();
+    }
+    return lp.fresh ? launch_group_g<FORM, true>(a, lp.group, lp.blocks, s)
+                    : launch_group_g<FORM, false>(a, lp.group, lp.blocks, s);
+}
+
+hipError_t launch_epoch(int form, const EpochArgs& a, const LaunchPlan& lp, hipStream_t s) {
+    switch (form) {
+        case FORM_RIDGE_PRIMAL: return launch_epoch_form<FORM_RIDGE_PRIMAL>(a, lp, s);
+        case FORM_SVM_DUAL: return launch_epoch_form<FORM_SVM_DUAL>(a, lp, s);
+        case FORM_RIDGE_DUAL: return launch_epoch_form<FORM_RIDGE_DUAL>(a, lp, s);
+        default: return hipErrorInvalidValue;
+    }
+}
+
+hipError_t ordered_lds_prepare(int form, size_t lds_bytes) {
+    switch (form) {
+        case FORM_RIDGE_PRIMAL:
+            return hipFuncSetAttribute(reinterpret_cast<const void*>(&k_epoch_ordered_lds<FORM_RIDGE_PRIMAL>),
+                                       hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds_bytes);
+        case FORM_SVM_DUAL:
+            return hipFuncSetAttribute(reinterpret_cast<const void*>(&k_epoch_ordered_lds<FORM_SVM_DUAL>),
+                                       hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds_bytes);
+        case FORM_RIDGE_DUAL:
+            return hipFuncSetAttribute(reinterpret_cast<const void*>(&k_epoch_ordered_lds<FORM_RIDGE_DUAL>),
+                                       hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds_bytes);
+        default: return hipErrorInvalidValue;
+    }
+}
+
+hipError_t launch_perm_fill(const PermKeys& p, int32_t* out, hipStream_t s) {
+    const uint32_t blocks = (p.n + 255) / 256;
+    hipLaunchKernelGGL(k_perm_fill, dim3(blocks), dim3(256), 0, s, p, out);
+    return hipGetLastError();
+}
+
+hipError_t launch_gather_dots(const int64_t* ptr, const int32_t* idx, const float* val, const float* u, uint32_t C,
+                              int G, int blocks, float* out, hipStream_t s) {
+    switch (G) {
+        case 4: hipLaunchKernelGGL(k_gather_dots<4>, dim3(blocks), dim3(256), 0, s, ptr, idx, val, u, C, out); break;
+        case 8: hipLaunchKernelGGL(k_gather_dots<8>, dim3(blocks), dim3(256), 0, s, ptr, idx, val, u, C, out); break;
+        case 16: hipLaunchKernelGGL(k_gather_dots<16>, dim3(blocks), dim3(256), 0, s, ptr, idx, val, u, C, out); break;
+        case 32: hipLaunchKernelGGL(k_gather_dots<32>, dim3(blocks), dim3(256), 0, s, ptr, idx, val, u, C, out); break;
+        default: hipLaunchKernelGGL(k_gather_dots<64>, dim3(blocks), dim3(256), 0, s, ptr, idx, val, u, C, out); break;
+    }
+    return hipGetLastError();
+}
+
+hipError_t launch_norms(const int64_t* ptr, const float* val, uint32_t C, int G, int blocks, float* out,
+                        hipStream_t s) {
+    switch (G) {
+        case 4: hipLaunchKernelGGL(k_norms<4>, dim3(blocks), dim3(256), 0, s, ptr, val, C, out); break;
+        case 8: hipLaunchKernelGGL(k_norms<8>, dim3(blocks), dim3(256), 0, s, ptr, val, C, out); break;
+        case 16: hipLaunchKernelGGL(k_norms<16>, dim3(blocks), dim3(256), 0, s, ptr, val, C, out); break;
+        case 32: hipLaunchKernelGGL(k_norms<32>, dim3(blocks), dim3(256), 0, s, ptr, val, C, out); break;
+        default: hipLaunchKernelGGL(k_norms<64>, dim3(blocks), dim3(256), 0, s, ptr, val, C, out); break;
+    }
+    return hipGetLastError();
+}
+
+hipError_t launch_validate(const int64_t* ptr, uint32_t S, const int32_t* idx, const float* val, int64_t nnz,
+                           int64_t bound, const float* y, int64_t ny, int pm1, int* flags, hipStream_t s) {
+    hipLaunchKernelGGL(k_validate_ptr, dim3((S + 256) / 256), dim3(256), 0, s, ptr, S, nnz, flags);
+    if (nnz > 0) {
+        int64_t b = (nnz + 255) / 256;
+        if (b > 8192) b = 8192;
+        hipLaunchKernelGGL(k_validate_entries, dim3((unsigned)b), dim3(256), 0, s, idx, val, nnz, bound, flags);
+    }
+    int64_t b = (ny + 255) / 256;
+    if (b > 4096) b = 4096;
+    if (b < 1) b = 1;
+    hipLaunchKernelGGL(k_validate_labels, dim3((unsigned)b), dim3(256), 0, s, y, ny, pm1, flags);
+    return hipGetLastError();
+}
+
+hipError_t launch_sub(const float* a, const float* b, int64_t n, float* out, hipStream_t s) {
+    int64_t blocks = (n + 255) / 256;
+    if (blocks > 8192) blocks = 8192;
+    if (blocks < 1) blocks = 1;
+    hipLaunchKernelGGL(k_sub, dim3((unsigned)blocks), dim3(256), 0, s, a, b, n, out);
+    return hipGetLastError();
+}
+
+template <int FORM>
+static void obj_coords_g(int G, int blocks, const ObjArgs& o, double* partials, hipStream_t s) {
+    switch (G) {
+        case 4: hipLaunchKernelGGL((k_obj_coords<FORM, 4>), dim3(blocks), dim3(256), 0, s, o.ptr, o.idx, o.val, o.u, o.model, o.y, o.C, o.lam, partials); break;
+        case 8: hipLaunchKernelGGL((k_obj_coords<FORM, 8>), dim3(blocks), dim3(256), 0, s, o.ptr, o.idx, o.val, o.u, o.model, o.y, o.C, o.lam, partials); break;
+        case 16: hipLaunchKernelGGL((k_obj_coords<FORM, 16>), dim3(blocks), dim3(256), 0, s, o.ptr, o.idx, o.val, o.u, o.model, o.y, o.C, o.lam, partials); break;
+        case 32: hipLaunchKernelGGL((k_obj_coords<FORM, 32>), dim3(blocks), dim3(256), 0, s, o.ptr, o.idx, o.val, o.u, o.model, o.y, o.C, o.lam, partials); break;
+        default: hipLaunchKernelGGL((k_obj_coords<FORM, 64>), dim3(blocks), dim3(256), 0, s, o.ptr, o.idx, o.val, o.u, o.model, o.y, o.C, o.lam, partials); break;
+    }
+}
+
+// sums[0..2] = coordinate sums, sums[3..4] = vector sums.
+hipError_t launch_objective(int form, const ObjArgs& o, int G, int blocks, double* partials, double* sums,
+                            hipStream_t s) {
+    double* pc = partials;                       // blocks x 3
+    double* pv = partials + (size_t)blocks * 3;  // blocks x 2
+    switch (form) {
+        case FORM_RIDGE_PRIMAL:
+            obj_coords_g<FORM_RIDGE_PRIMAL>(G, blocks, o, pc, s);
+            hipLaunchKernelGGL(k_obj_vector<FORM_RIDGE_PRIMAL>, dim3(blocks), dim3(256), 0, s, o.u, o.yv, o.L, pv);
+            break;
+        case FORM_SVM_DUAL:
+            obj_coords_g<FORM_SVM_DUAL>(G, blocks, o, pc, s);
+            hipLaunchKernelGGL(k_obj_vector<FORM_SVM_DUAL>, dim3(blocks), dim3(256), 0, s, o.u, o.yv, o.L, pv);
+            break;
+        case FORM_RIDGE_DUAL:
+            obj_coords_g<FORM_RIDGE_DUAL>(G, blocks, o, pc, s);
+            hipLaunchKernelGGL(k_obj_vector<FORM_RIDGE_DUAL>, dim3(blocks), dim3(256), 0, s, o.u, o.yv, o.L, pv);
+            break;
+        default: return hipErrorInvalidValue;
+    }
+    hipLaunchKernelGGL(k_sum_partials, dim3(1), dim3(256), 0, s, pc, blocks, 3, sums);
+    hipLaunchKernelGGL(k_sum_partials, dim3(1), dim3(256), 0, s, pv, blocks, 2, sums + 3);
+    return hipGetLastError();
+}
+
+}  // namespace scd
