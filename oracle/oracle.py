@@ -21,6 +21,8 @@ import numpy as np
 _HERE = os.path.dirname(os.path.abspath(__file__))
 _SRC = os.path.join(_HERE, "scd_oracle.c")
 _LIB_PATH = os.path.join(_HERE, "liboracle.so")
+# A different build of the same source (used by the planted-mistake test) can be selected here.
+_LOAD_PATH = os.environ.get("SCD_ORACLE_LIB", _LIB_PATH)
 
 _i64 = ctypes.c_int64
 _u64 = ctypes.c_uint64
@@ -46,9 +48,9 @@ _lib = None
 def lib():
     global _lib
     if _lib is None:
-        if not os.path.exists(_LIB_PATH):
+        if _LOAD_PATH == _LIB_PATH and not os.path.exists(_LIB_PATH):
             build()
-        L = ctypes.CDLL(_LIB_PATH)
+        L = ctypes.CDLL(_LOAD_PATH)
         L.oracle_splitmix64_mix.restype = _u64
         L.oracle_splitmix64_mix.argtypes = [_u64]
         L.oracle_splitmix64_nth.restype = _u64

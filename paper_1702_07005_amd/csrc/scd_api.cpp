@@ -392,12 +392,7 @@ int scd_get_state(scd_handle_t h, float* model, float* shared, int64_t* epoch, v
     if (int r = set_device(h)) return r;
     hipStream_t s = (hipStream_t)stream;
     if (model) HIP_TRY(hipMemcpyAsync(model, h->model, sizeof(float) * (size_t)h->C, hipMemcpyDeviceToDevice, s));
-    if (shared) {
-        if (h->form == FORM_RIDGE_PRIMAL)
-            HIP_TRY(launch_sub(h->y, h->u, h->L, shared, s));  // w = y - r
-        else
-            HIP_TRY(hipMemcpyAsync(shared, h->u, sizeof(float) * (size_t)h->L, hipMemcpyDeviceToDevice, s));
-    }
+    if (shared) HIP_TRY(hipMemcpyAsync(shared, h->u, sizeof(float) * (size_t)h->L, hipMemcpyDeviceToDevice, s));
     if (epoch) *epoch = h->epoch;
     return SCD_OK;
 }
@@ -408,12 +403,7 @@ int scd_set_state(scd_handle_t h, const float* model, const float* shared, int64
     if (int r = set_device(h)) return r;
     hipStream_t s = (hipStream_t)stream;
     if (model) HIP_TRY(hipMemcpyAsync(h->model, model, sizeof(float) * (size_t)h->C, hipMemcpyDeviceToDevice, s));
-    if (shared) {
-        if (h->form == FORM_RIDGE_PRIMAL)
-            HIP_TRY(launch_sub(h->y, shared, h->L, h->u, s));  // r = y - w
-        else
-            HIP_TRY(hipMemcpyAsync(h->u, shared, sizeof(float) * (size_t)h->L, hipMemcpyDeviceToDevice, s));
-    }
+    if (shared) HIP_TRY(hipMemcpyAsync(h->u, shared, sizeof(float) * (size_t)h->L, hipMemcpyDeviceToDevice, s));
     h->epoch = epoch;
     return SCD_OK;
 }

@@ -73,7 +73,6 @@ hipError_t launch_norms(const int64_t* ptr, const float* val, uint32_t C, int G,
                         hipStream_t s);
 hipError_t launch_validate(const int64_t* ptr, uint32_t S, const int32_t* idx, const float* val, int64_t nnz,
                            int64_t bound, const float* y, int64_t ny, int pm1, int* flags, hipStream_t s);
-hipError_t launch_sub(const float* a, const float* b, int64_t n, float* out, hipStream_t s);
 hipError_t launch_objective(int form, const ObjArgs& o, int G, int blocks, double* partials, double* sums,
                             hipStream_t s);
 

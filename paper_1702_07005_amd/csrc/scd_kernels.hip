@@ -341,12 +341,6 @@ __global__ void k_validate_labels(const float* __restrict__ y, int64_t n, int pm
     if (f) atomicOr(flags, f);
 }
 
-// out = a - b (elementwise): converts between the residual r = y - w and w.
-__global__ void k_sub(const float* __restrict__ a, const float* __restrict__ b, int64_t n, float* __restrict__ out) {
-    for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += (int64_t)gridDim.x * blockDim.x)
-        out[i] = a[i] - b[i];
-}
-
 // ----------------------------------------------------------------------------------------
 // Objective / duality-gap reductions (fp64).  Coordinate pass: per coordinate the fp64 dot
 // d_c = <a_c, u> and up to three sums; vector pass: two sums over the shared vector.  Every
@@ -542,14 +536,6 @@ hipError_t launch_validate(const int64_t* ptr, uint32_t S, const int32_t* idx, c
     if (b > 4096) b = 4096;
     if (b < 1) b = 1;
     hipLaunchKernelGGL(k_validate_labels, dim3((unsigned)b), dim3(256), 0, s, y, ny, pm1, flags);
-    return hipGetLastError();
-}
-
-hipError_t launch_sub(const float* a, const float* b, int64_t n, float* out, hipStream_t s) {
-    int64_t blocks = (n + 255) / 256;
-    if (blocks > 8192) blocks = 8192;
-    if (blocks < 1) blocks = 1;
-    hipLaunchKernelGGL(k_sub, dim3((unsigned)blocks), dim3(256), 0, s, a, b, n, out);
     return hipGetLastError();
 }
 

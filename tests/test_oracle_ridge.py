@@ -190,3 +190,21 @@ def test_dual_step_is_exact_1d_maximiser(oracle):
         res = minimize_scalar(lambda t: -_D(A, y, lam, before + t * e), bracket=(-1, 1), tol=1e-12)
         assert abs((alpha[n] - before[n]) - res.x) <= 1e-6 * max(1.0, abs(res.x))
         np.testing.assert_allclose(wbar, A.T @ alpha, rtol=0, atol=1e-12)
+
+
+def test_gather_dots_and_norms_match_sparse_library(oracle, synth):
+    # The per-coordinate inner products <a_c, u> are A^T u (CSC) or A u (CSR): scipy's sparse product.
+    import scipy.sparse as sps
+    p = synth.make("sparse_ridge", n_rows=4000, n_cols=3000, density=0.01)
+    A = sps.csc_matrix((p.val.astype(np.float64), p.idx, p.ptr), shape=(p.n_rows, p.n_cols))
+    u = np.random.default_rng(0).standard_normal(p.n_rows).astype(np.float32)
+    d, cond = oracle.gather_dots(p.ptr, p.idx, p.val, u)
+    np.testing.assert_allclose(d, A.T @ u.astype(np.float64), rtol=1e-12, atol=1e-12)
+    np.testing.assert_allclose(cond, abs(A).T @ np.abs(u.astype(np.float64)), rtol=1e-12)
+    np.testing.assert_allclose(oracle.norms(p.ptr, p.val), np.asarray(A.multiply(A).sum(axis=0)).ravel(),
+                               rtol=1e-12)
+    q = synth.make("click_svm", n_rows=2000, n_cols=5000, row_nnz=10)
+    X = sps.csr_matrix((q.val.astype(np.float64), q.idx, q.ptr), shape=(q.n_rows, q.n_cols))
+    v = np.random.default_rng(1).standard_normal(q.n_cols).astype(np.float32)
+    np.testing.assert_allclose(oracle.gather_dots(q.ptr, q.idx, q.val, v)[0], X @ v.astype(np.float64),
+                               rtol=1e-12, atol=1e-12)
