@@ -113,12 +113,10 @@ def main():
     solver = scd.solver_for(prob, device=dev)
     info = solver.info()
     zeros_m = torch.zeros(prob.C, dtype=torch.float32, device=dev)
-    # Zero model; its shared vector in the solver's layout (the ridge primal keeps r = y - A beta = y).
-    start_s = solver._keep[3].clone() if prob.form == "ridge_primal" else \
-        torch.zeros(prob.L, dtype=torch.float32, device=dev)
+    zeros_s = torch.zeros(prob.L, dtype=torch.float32, device=dev)
 
     def reset():
-        solver.set_state(zeros_m, start_s, 0)
+        solver.set_state(zeros_m, zeros_s, 0)
 
     # --- time to duality gap (epoch kernels only, gap evaluation excluded) ------------------
     print("# time to gap", file=sys.stderr, flush=True)

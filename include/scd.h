@@ -16,9 +16,7 @@
  *
  * Formulations:
  *   SCD_RIDGE_PRIMAL  coordinates = features; A given by columns (CSC); model beta in R^M;
- *                     shared vector w = A beta in R^N, kept (and exchanged through the state
- *                     calls) as the residual r = y - w, which is all eq. (update_primal)
- *                     reads: <y - w, a_m> = <r, a_m>.
+ *                     shared vector w = A beta in R^N.  Step: eq. (update_primal).
  *   SCD_SVM_DUAL      coordinates = examples; A given by rows (CSR); y in {-1, +1};
  *                     model alpha in [0,1]^N; shared vector w = sum_i alpha_i y_i x_i/(lambda N)
  *                     in R^M.  Hinge-loss SVM, P(w) = (1/N) sum max(0, 1 - y_i x_i.w)
@@ -107,8 +105,7 @@ typedef struct {
  *   lambda:  the paper's normalised lambda (> 0, finite).
  *   stream:  hipStream_t used for the set-up work; the call synchronises it.
  * Validates A and y on the device (one pass), computes |a_c|^2 for every coordinate and sets
- * model = 0, shared vector = 0 (Alg. 1/2 initialisation; the ridge primal's residual is then
- * r = y), epoch = 0.
+ * model = 0, shared vector = 0 (Alg. 1/2 initialisation), epoch = 0.
  * Errors: SCD_ERR_INVALID (null/negative sizes, wrong layout, ptr not monotone, index out of
  * range, labels not +-1 for the SVM, lambda <= 0), SCD_ERR_NUMERIC (non-finite values or labels),
  * SCD_ERR_OOM, SCD_ERR_HIP.  On error *out is set to NULL. */
@@ -128,7 +125,7 @@ int scd_epochs(scd_handle_t h, uint64_t seed, int32_t n_epochs, void *stream);
 
 /* Primal and dual objective of the current state, in fp64 (synchronises):
  *   SCD_RIDGE_PRIMAL: P(beta) of eq. (primal_obj) and D((y - w)/N) of eq. (dual_obj), with the
- *                     maintained residual r = y - w standing in for y - A beta (Sec. II-C).
+ *                     maintained shared vector w standing in for A beta (Sec. II-C).
  *   SCD_RIDGE_DUAL:   P(wbar/lambda) and D(alpha) (Sec. II-C), wbar = maintained A^T alpha.
  *   SCD_SVM_DUAL:     P(w) and D(alpha) of the hinge SVM, w = maintained shared vector.
  * Either output pointer may be NULL. */
@@ -140,8 +137,7 @@ int scd_duality_gap(scd_handle_t h, void *stream, double *gap);
 
 /* Copy the state out (device buffers, may be NULL to skip), exactly as the solver holds it:
  *   model_dev:  float32[n_coords]   (beta, or alpha)
- *   shared_dev: float32[shared_len] (ridge primal: residual r = y - A beta; SVM dual:
- *               w(alpha); ridge dual: wbar = A^T alpha)
+ *   shared_dev: float32[shared_len] (w = A beta, or w(alpha), or wbar = A^T alpha)
  *   epoch:      host int64 (may be NULL).  Enqueues only.  A state copied out and written
  *   back with scd_set_state resumes bit-exactly. */
 int scd_get_state(scd_handle_t h, float *model_dev, float *shared_dev, int64_t *epoch, void *stream);

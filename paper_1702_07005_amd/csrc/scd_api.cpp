@@ -76,6 +76,7 @@ struct scd_solver {
     float* model = nullptr;
     float* u = nullptr;
     float* norms = nullptr;
+    float* cy = nullptr;  // ridge primal: <y, a_c> per coordinate
     int* flags = nullptr;
     double* partials = nullptr;
     double* sums = nullptr;
@@ -174,6 +175,7 @@ void release(scd_solver* h) {
     (void)hipFree(h->model);
     (void)hipFree(h->u);
     (void)hipFree(h->norms);
+    (void)hipFree(h->cy);
     (void)hipFree(h->flags);
     (void)hipFree(h->partials);
     (void)hipFree(h->sums);
@@ -206,7 +208,7 @@ void objectives_from_sums(const scd_solver* h, double* P, double* D) {
     const double* t = h->host_sums;
     const double N = (double)h->n_rows, lam = h->lambda;
     if (h->form == FORM_RIDGE_PRIMAL) {
-        // t0 = sum_m <a_m, r>^2, t1 = |beta|^2, t3 = |r|^2, t4 = <r, y>,  r = y - A beta.
+        // t0 = sum_m <a_m, r>^2, t1 = |beta|^2, t3 = |r|^2, t4 = <r, y>,  r = y - w, w = A beta.
         *P = t[3] / (2.0 * N) + 0.5 * lam * t[1];
         *D = -t[3] / (2.0 * N) - t[0] / (2.0 * lam * N * N) + t[4] / N;
     } else if (h->form == FORM_SVM_DUAL) {
@@ -285,6 +287,7 @@ int scd_create(const scd_matrix_t* A, const float* y, double lambda, int32_t for
     hip(hipMalloc(&h->model, sizeof(float) * (size_t)h->C), "hipMalloc(model)");
     hip(hipMalloc(&h->u, sizeof(float) * (size_t)h->L), "hipMalloc(shared)");
     hip(hipMalloc(&h->norms, sizeof(float) * (size_t)h->C), "hipMalloc(norms)");
+    if (formulation == SCD_RIDGE_PRIMAL) hip(hipMalloc(&h->cy, sizeof(float) * (size_t)h->C), "hipMalloc(cy)");
     hip(hipMalloc(&h->flags, 2 * sizeof(int64_t)), "hipMalloc(flags)");
     hip(hipMalloc(&h->partials, sizeof(double) * (size_t)kObjBlocksMax * 5), "hipMalloc(partials)");
     hip(hipMalloc(&h->sums, sizeof(double) * 8), "hipMalloc(sums)");
@@ -308,12 +311,11 @@ int scd_create(const scd_matrix_t* A, const float* y, double lambda, int32_t for
     }
     if (rc == SCD_OK) {
         const int G = obj_group(h);
-        hip(launch_norms(h->ptr, h->val, (uint32_t)h->C, G, obj_blocks(h, G), h->norms, s), "norms");
+        hip(launch_norms(h->ptr, h->idx, h->val, formulation == SCD_RIDGE_PRIMAL ? h->y : nullptr, (uint32_t)h->C,
+                         G, obj_blocks(h, G), h->norms, h->cy, s),
+            "norms");
         hip(hipMemsetAsync(h->model, 0, sizeof(float) * (size_t)h->C, s), "zero model");
-        if (formulation == SCD_RIDGE_PRIMAL)  // beta = 0: w = 0, residual r = y
-            hip(hipMemcpyAsync(h->u, h->y, sizeof(float) * (size_t)h->L, hipMemcpyDeviceToDevice, s), "r = y");
-        else
-            hip(hipMemsetAsync(h->u, 0, sizeof(float) * (size_t)h->L, s), "zero shared");
+        hip(hipMemsetAsync(h->u, 0, sizeof(float) * (size_t)h->L, s), "zero shared");
         hip(hipStreamSynchronize(s), "synchronize");
     }
     if (rc != SCD_OK) {
@@ -349,7 +351,7 @@ int scd_epochs(scd_handle_t h, uint64_t seed, int32_t n_epochs, void* stream) {
     a.ptr = h->ptr;
     a.idx = h->idx;
     a.val = h->val;
-    a.y = h->y;
+    a.y = h->form == FORM_RIDGE_PRIMAL ? h->cy : h->y;
     a.model = h->model;
     a.u = h->u;
     a.norms = h->norms;

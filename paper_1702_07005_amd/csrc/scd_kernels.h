@@ -29,9 +29,9 @@ struct EpochArgs {
     const int64_t* ptr;
     const int32_t* idx;
     const float* val;
-    const float* y;      // per-coordinate labels (duals); unused by the ridge primal
+    const float* y;      // per-coordinate constant: <y, a_c> (ridge primal) or the label (duals)
     float* model;        // [C]
-    float* u;            // shared vector [L] (residual y - A beta for the ridge primal)
+    float* u;            // shared vector [L]
     const float* norms;  // [C]
     StepConsts k;
     PermKeys perm;       // perm.n = C
@@ -69,8 +69,8 @@ hipError_t ordered_lds_prepare(int form, size_t lds_bytes);
 hipError_t launch_perm_fill(const PermKeys& p, int32_t* out, hipStream_t s);
 hipError_t launch_gather_dots(const int64_t* ptr, const int32_t* idx, const float* val, const float* u, uint32_t C,
                               int G, int blocks, float* out, hipStream_t s);
-hipError_t launch_norms(const int64_t* ptr, const float* val, uint32_t C, int G, int blocks, float* out,
-                        hipStream_t s);
+hipError_t launch_norms(const int64_t* ptr, const int32_t* idx, const float* val, const float* y, uint32_t C, int G,
+                        int blocks, float* out, float* cy, hipStream_t s);
 hipError_t launch_validate(const int64_t* ptr, uint32_t S, const int32_t* idx, const float* val, int64_t nnz,
                            int64_t bound, const float* y, int64_t ny, int pm1, int* flags, hipStream_t s);
 hipError_t launch_objective(int form, const ObjArgs& o, int G, int blocks, double* partials, double* sums,

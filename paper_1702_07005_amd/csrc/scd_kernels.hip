@@ -11,11 +11,13 @@
 //   4. scatter u[idx] += coef * val  with device-scope fp32 atomics (no return).
 //
 // Shared vector kept on the device, per formulation:
-//   ridge primal : the residual r = y - A beta (the paper's w = A beta is y - r); the step
-//                  needs <y - w, a_m> (eq. update_primal) = <r, a_m>, one gather instead of
-//                  two, and r carries the small quantity itself near the optimum.
+//   ridge primal : w = A beta.  The step needs <y - w, a_m> (eq. update_primal); it is taken
+//                  as cy_m - <w, a_m> with cy_m = <y, a_m> computed once at set-up, so each
+//                  stored entry costs one gather (w) instead of two (y and w).
 //   SVM dual     : w = sum_i alpha_i y_i x_i / (lambda N).
 //   ridge dual   : wbar = A^T alpha (eq. update_dual).
+// `y` in the epoch arguments is the per-coordinate constant: cy for the ridge primal, the
+// label for the duals.
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
@@ -103,7 +105,8 @@ __device__ __forceinline__ void atomic_add_u(float* p, float v) {
 }
 
 // ----------------------------------------------------------------------------------------
-// Closed-form coordinate steps.  g = <a_m, u>, s = |a_m|^2, m_old = model[m].
+// Closed-form coordinate steps.  g = <a_m, u>, s = |a_m|^2, m_old = model[m], ylab = the
+// coordinate's constant (cy_m = <y, a_m> for the ridge primal, the label for the duals).
 // Returns the new model value; *coef is the factor of val in the scatter u += coef * a_m.
 // ----------------------------------------------------------------------------------------
 template <int FORM>
@@ -111,9 +114,9 @@ __device__ __forceinline__ float coord_step(float g, float s, float m_old, float
                                             float* coef) {
     if constexpr (FORM == FORM_RIDGE_PRIMAL) {
         // eq. (update_primal): d = (<y - w, a_m> - lambda N beta_m) / (|a_m|^2 + lambda N);
-        // r = y - w moves by -d a_m.
-        float d = (g - k.lamN * m_old) / (s + k.lamN);
-        *coef = -d;
+        // w moves by d a_m.
+        float d = ((ylab - g) - k.lamN * m_old) / (s + k.lamN);
+        *coef = d;
         return m_old + d;
     } else if constexpr (FORM == FORM_SVM_DUAL) {
         // exact maximisation of the hinge dual along alpha_i, projected on [0, 1].
@@ -145,7 +148,7 @@ __global__ __launch_bounds__(256) void k_epoch_group(EpochArgs a) {
         const int64_t s0 = a.ptr[m], s1 = a.ptr[m + 1];
         const float m_old = a.model[m];
         const float sn = a.norms[m];
-        const float ylab = (FORM == FORM_RIDGE_PRIMAL) ? 0.0f : a.y[m];
+        const float ylab = a.y[m];
         int ci[R];
         float cv[R];
 #pragma unroll
@@ -192,7 +195,7 @@ __global__ __launch_bounds__(BS) void k_epoch_block(EpochArgs a) {
         const int64_t s0 = a.ptr[m], s1 = a.ptr[m + 1];
         const float m_old = a.model[m];
         const float sn = a.norms[m];
-        const float ylab = (FORM == FORM_RIDGE_PRIMAL) ? 0.0f : a.y[m];
+        const float ylab = a.y[m];
         int ci[R];
         float cv[R];
 #pragma unroll
@@ -252,7 +255,7 @@ __global__ __launch_bounds__(1024) void k_epoch_ordered_lds(EpochArgs a, uint32_
         const int64_t s0 = a.ptr[m], s1 = a.ptr[m + 1];
         const float m_old = a.model[m];
         const float sn = a.norms[m];
-        const float ylab = (FORM == FORM_RIDGE_PRIMAL) ? 0.0f : a.y[m];
+        const float ylab = a.y[m];
         float acc = 0.0f;
         for (int64_t k = s0 + tid; k < s1; k += BS) acc = fmaf(a.val[k], su[a.idx[k]], acc);
         acc = group_sum<64>(acc);
@@ -292,18 +295,27 @@ __global__ __launch_bounds__(256) void k_gather_dots(const int64_t* __restrict__
 }
 
 // ----------------------------------------------------------------------------------------
-// Set-up: squared segment norms (fp64 accumulation, fp32 result) and input validation.
+// Set-up: squared segment norms and, when y is given (ridge primal), cy_c = <y, a_c>
+// (fp64 accumulation, fp32 results); input validation.
 // ----------------------------------------------------------------------------------------
 template <int G>
-__global__ __launch_bounds__(256) void k_norms(const int64_t* __restrict__ ptr, const float* __restrict__ val,
-                                               uint32_t C, float* __restrict__ out) {
+__global__ __launch_bounds__(256) void k_norms(const int64_t* __restrict__ ptr, const int32_t* __restrict__ idx,
+                                               const float* __restrict__ val, const float* __restrict__ y,
+                                               uint32_t C, float* __restrict__ out, float* __restrict__ cy) {
     const int lane = threadIdx.x & (G - 1);
     const uint32_t ngroups = gridDim.x * (256u / G);
     for (uint32_t c = (blockIdx.x * 256u + threadIdx.x) / G; c < C; c += ngroups) {
-        double acc = 0.0;
-        for (int64_t k = ptr[c] + lane; k < ptr[c + 1]; k += G) acc += (double)val[k] * (double)val[k];
+        double acc = 0.0, dy = 0.0;
+        for (int64_t k = ptr[c] + lane; k < ptr[c + 1]; k += G) {
+            acc += (double)val[k] * (double)val[k];
+            if (y) dy += (double)val[k] * (double)y[idx[k]];
+        }
         acc = group_sum_f64<G>(acc);
-        if (lane == 0) out[c] = (float)acc;
+        if (y) dy = group_sum_f64<G>(dy);
+        if (lane == 0) {
+            out[c] = (float)acc;
+            if (y) cy[c] = (float)dy;
+        }
     }
 }
 
@@ -343,9 +355,10 @@ __global__ void k_validate_labels(const float* __restrict__ y, int64_t n, int pm
 
 // ----------------------------------------------------------------------------------------
 // Objective / duality-gap reductions (fp64).  Coordinate pass: per coordinate the fp64 dot
-// d_c = <a_c, u> and up to three sums; vector pass: two sums over the shared vector.  Every
-// workgroup writes its partial sums; one final workgroup adds the partials in a fixed order.
-//   ridge primal (u = r = y - w):  S0 += d^2,  S1 += beta^2          | V0 += r^2, V1 += r*y
+// d_c and up to three sums; vector pass: two sums over the shared vector.  Every workgroup
+// writes its partial sums; one final workgroup adds the partials in a fixed order.
+//   ridge primal (u = w, r = y - w in fp64, d = <a_c, r>):
+//                                  S0 += d^2,  S1 += beta^2          | V0 += r^2, V1 += r*y
 //   svm dual     (u = w):          S0 += max(0, 1 - y d), S1 += alpha | V0 += w^2
 //   ridge dual   (u = wbar):       S0 += (d/lambda - y)^2, S1 += alpha^2, S2 += alpha*y | V0 += wbar^2
 // ----------------------------------------------------------------------------------------
@@ -370,13 +383,21 @@ template <int FORM, int G>
 __global__ __launch_bounds__(256) void k_obj_coords(const int64_t* __restrict__ ptr, const int32_t* __restrict__ idx,
                                                     const float* __restrict__ val, const float* __restrict__ u,
                                                     const float* __restrict__ model, const float* __restrict__ y,
-                                                    uint32_t C, double lam, double* __restrict__ partials) {
+                                                    const float* __restrict__ yv, uint32_t C, double lam,
+                                                    double* __restrict__ partials) {
     const int lane = threadIdx.x & (G - 1);
     const uint32_t ngroups = gridDim.x * (256u / G);
     double t[3] = {0.0, 0.0, 0.0};
     for (uint32_t c = (blockIdx.x * 256u + threadIdx.x) / G; c < C; c += ngroups) {
         double d = 0.0;
-        for (int64_t k = ptr[c] + lane; k < ptr[c + 1]; k += G) d += (double)val[k] * (double)u[idx[k]];
+        if constexpr (FORM == FORM_RIDGE_PRIMAL) {
+            for (int64_t k = ptr[c] + lane; k < ptr[c + 1]; k += G) {
+                const int32_t i = idx[k];
+                d += (double)val[k] * ((double)yv[i] - (double)u[i]);
+            }
+        } else {
+            for (int64_t k = ptr[c] + lane; k < ptr[c + 1]; k += G) d += (double)val[k] * (double)u[idx[k]];
+        }
         d = group_sum_f64<G>(d);
         if (lane == 0) {
             const double mo = model[c];
@@ -403,9 +424,14 @@ __global__ __launch_bounds__(256) void k_obj_vector(const float* __restrict__ u,
                                                     double* __restrict__ partials) {
     double t[2] = {0.0, 0.0};
     for (int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x; i < L; i += (int64_t)gridDim.x * 256) {
-        const double x = u[i];
-        t[0] += x * x;
-        if constexpr (FORM == FORM_RIDGE_PRIMAL) t[1] += x * (double)y[i];
+        if constexpr (FORM == FORM_RIDGE_PRIMAL) {
+            const double r = (double)y[i] - (double)u[i];
+            t[0] += r * r;
+            t[1] += r * (double)y[i];
+        } else {
+            const double x = u[i];
+            t[0] += x * x;
+        }
     }
     block_reduce_store<2>(t, partials + (size_t)blockIdx.x * 2);
 }
@@ -512,14 +538,14 @@ hipError_t launch_gather_dots(const int64_t* ptr, const int32_t* idx, const floa
     return hipGetLastError();
 }
 
-hipError_t launch_norms(const int64_t* ptr, const float* val, uint32_t C, int G, int blocks, float* out,
-                        hipStream_t s) {
+hipError_t launch_norms(const int64_t* ptr, const int32_t* idx, const float* val, const float* y, uint32_t C, int G,
+                        int blocks, float* out, float* cy, hipStream_t s) {
     switch (G) {
-        case 4: hipLaunchKernelGGL(k_norms<4>, dim3(blocks), dim3(256), 0, s, ptr, val, C, out); break;
-        case 8: hipLaunchKernelGGL(k_norms<8>, dim3(blocks), dim3(256), 0, s, ptr, val, C, out); break;
-        case 16: hipLaunchKernelGGL(k_norms<16>, dim3(blocks), dim3(256), 0, s, ptr, val, C, out); break;
-        case 32: hipLaunchKernelGGL(k_norms<32>, dim3(blocks), dim3(256), 0, s, ptr, val, C, out); break;
-        default: hipLaunchKernelGGL(k_norms<64>, dim3(blocks), dim3(256), 0, s, ptr, val, C, out); break;
+        case 4: hipLaunchKernelGGL(k_norms<4>, dim3(blocks), dim3(256), 0, s, ptr, idx, val, y, C, out, cy); break;
+        case 8: hipLaunchKernelGGL(k_norms<8>, dim3(blocks), dim3(256), 0, s, ptr, idx, val, y, C, out, cy); break;
+        case 16: hipLaunchKernelGGL(k_norms<16>, dim3(blocks), dim3(256), 0, s, ptr, idx, val, y, C, out, cy); break;
+        case 32: hipLaunchKernelGGL(k_norms<32>, dim3(blocks), dim3(256), 0, s, ptr, idx, val, y, C, out, cy); break;
+        default: hipLaunchKernelGGL(k_norms<64>, dim3(blocks), dim3(256), 0, s, ptr, idx, val, y, C, out, cy); break;
     }
     return hipGetLastError();
 }
@@ -542,11 +568,11 @@ hipError_t launch_validate(const int64_t* ptr, uint32_t S, const int32_t* idx, c
 template <int FORM>
 static void obj_coords_g(int G, int blocks, const ObjArgs& o, double* partials, hipStream_t s) {
     switch (G) {
-        case 4: hipLaunchKernelGGL((k_obj_coords<FORM, 4>), dim3(blocks), dim3(256), 0, s, o.ptr, o.idx, o.val, o.u, o.model, o.y, o.C, o.lam, partials); break;
-        case 8: hipLaunchKernelGGL((k_obj_coords<FORM, 8>), dim3(blocks), dim3(256), 0, s, o.ptr, o.idx, o.val, o.u, o.model, o.y, o.C, o.lam, partials); break;
-        case 16: hipLaunchKernelGGL((k_obj_coords<FORM, 16>), dim3(blocks), dim3(256), 0, s, o.ptr, o.idx, o.val, o.u, o.model, o.y, o.C, o.lam, partials); break;
-        case 32: hipLaunchKernelGGL((k_obj_coords<FORM, 32>), dim3(blocks), dim3(256), 0, s, o.ptr, o.idx, o.val, o.u, o.model, o.y, o.C, o.lam, partials); break;
-        default: hipLaunchKernelGGL((k_obj_coords<FORM, 64>), dim3(blocks), dim3(256), 0, s, o.ptr, o.idx, o.val, o.u, o.model, o.y, o.C, o.lam, partials); break;
+        case 4: hipLaunchKernelGGL((k_obj_coords<FORM, 4>), dim3(blocks), dim3(256), 0, s, o.ptr, o.idx, o.val, o.u, o.model, o.y, o.yv, o.C, o.lam, partials); break;
+        case 8: hipLaunchKernelGGL((k_obj_coords<FORM, 8>), dim3(blocks), dim3(256), 0, s, o.ptr, o.idx, o.val, o.u, o.model, o.y, o.yv, o.C, o.lam, partials); break;
+        case 16: hipLaunchKernelGGL((k_obj_coords<FORM, 16>), dim3(blocks), dim3(256), 0, s, o.ptr, o.idx, o.val, o.u, o.model, o.y, o.yv, o.C, o.lam, partials); break;
+        case 32: hipLaunchKernelGGL((k_obj_coords<FORM, 32>), dim3(blocks), dim3(256), 0, s, o.ptr, o.idx, o.val, o.u, o.model, o.y, o.yv, o.C, o.lam, partials); break;
+        default: hipLaunchKernelGGL((k_obj_coords<FORM, 64>), dim3(blocks), dim3(256), 0, s, o.ptr, o.idx, o.val, o.u, o.model, o.y, o.yv, o.C, o.lam, partials); break;
     }
 }
 

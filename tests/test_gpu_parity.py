@@ -56,16 +56,6 @@ def rel_inf(a, b):
     return float(np.max(np.abs(a - b)) / max(np.max(np.abs(b)), 1e-30))
 
 
-def paper_shared(p, gs):
-    """The shared vector of Sec. II from the solver's state: w = y - r for the ridge primal."""
-    g = f64(gs) if isinstance(gs, torch.Tensor) else np.asarray(gs, dtype=np.float64)
-    return p.y.astype(np.float64) - g if p.form == "ridge_primal" else g
-
-
-def solver_shared(p, w):
-    """The solver's layout of a shared vector w (residual y - w for the ridge primal), fp32."""
-    w = np.asarray(w, dtype=np.float64)
-    return (p.y.astype(np.float64) - w if p.form == "ridge_primal" else w).astype(np.float32)
 
 
 # ---------------------------------------------------------------------------------- a2 permutation
@@ -111,12 +101,12 @@ def test_objectives_of_given_state(key):
     rng = np.random.default_rng(2)
     model = rng.random(p.C).astype(np.float32) if p.form == "svm_dual" else \
         (0.01 * rng.standard_normal(p.C)).astype(np.float32)
-    shared = solver_shared(p, fresh(p, model.astype(np.float64)))
+    shared = fresh(p, model.astype(np.float64)).astype(np.float32)
     s.set_state(torch.from_numpy(model).to(DEV), torch.from_numpy(shared).to(DEV), 0)
     P, D = s.objective()
     gm, gs, _ = s.get_state()
     Pr, Dr, Gr = orc.objectives(p.form, p.n_rows, p.n_cols, p.ptr, p.idx, p.val, p.y, p.lam, f64(gm),
-                                paper_shared(p, gs))
+                                f64(gs))
     scale = max(abs(Pr), abs(Dr))
     assert abs(P - Pr) <= 1e-9 * scale and abs(D - Dr) <= 1e-9 * scale
     G = s.duality_gap()
@@ -165,7 +155,7 @@ def test_ordered_epochs_track_oracle(key):
         Pr = curve[e][0]
         assert abs(P - Pr) <= 1e-4 * abs(Pr), (e, P, Pr)
         gm, gs, _ = s.get_state()
-        assert rel_inf(paper_shared(p, gs), fresh(p, f64(gm))) <= 1e-4
+        assert rel_inf(f64(gs), fresh(p, f64(gm))) <= 1e-4
     gm, _, ep = s.get_state()
     assert ep == E
     s.close()
@@ -227,7 +217,7 @@ def test_async_epochs_invariant_and_gap_curve(key, E):
         s.epochs(0, 1)
         gm, gs, _ = s.get_state()
         model = f64(gm)
-        assert rel_inf(paper_shared(p, gs), fresh(p, model)) <= 1e-4, e
+        assert rel_inf(f64(gs), fresh(p, model)) <= 1e-4, e
         if p.form == "svm_dual":
             assert model.min() >= 0.0 and model.max() <= 1.0
         G = s.duality_gap()
@@ -267,7 +257,7 @@ def test_ridge_dual_async_and_ordered():
         s.epochs(3, 1)
         o.epochs(3, 1)
         gm, gs, _ = s.get_state()
-        assert rel_inf(paper_shared(p, gs), fresh(p, f64(gm))) <= 1e-4
+        assert rel_inf(f64(gs), fresh(p, f64(gm))) <= 1e-4
         Po, _ = o.objective()
         assert abs(Po - curve[e][0]) <= 1e-4 * abs(curve[e][0])
         if curve[e][2] > 1e-6 * abs(curve[0][0]):
@@ -289,7 +279,7 @@ def test_every_group_width_keeps_invariant(group, fresh_reads):
     assert s.info()["group_lanes"] == group
     s.epochs(1, 3)
     gm, gs, _ = s.get_state()
-    assert rel_inf(paper_shared(p, gs), fresh(p, f64(gm))) <= 1e-4
+    assert rel_inf(f64(gs), fresh(p, f64(gm))) <= 1e-4
     d = f64(s.gather_dots(gs))  # a3 against the solver's own shared vector, frozen
     dref, cond = orc.gather_dots(p.ptr, p.idx, p.val, gs.cpu().numpy())
     assert np.all(np.abs(d - dref) <= 1e-4 * cond + 1e-30)
@@ -304,7 +294,7 @@ def test_windowed_epochs(window):
     assert s.info()["window"] == window
     s.epochs(0, 3)
     gm, gs, _ = s.get_state()
-    assert rel_inf(paper_shared(p, gs), fresh(p, f64(gm))) <= 1e-4
+    assert rel_inf(f64(gs), fresh(p, f64(gm))) <= 1e-4
     s.close()
 
 
