@@ -2,7 +2,9 @@
 // objectives and state.  All compute runs in the HIP kernels of scd_kernels.hip.
 #include <hip/hip_runtime.h>
 
+#include <algorithm>
 #include <cmath>
+#include <climits>
 #include <cstdarg>
 #include <cstdio>
 #include <cstring>
@@ -62,6 +64,8 @@ int cached_per_lane(int G) { return G <= 4 ? 4 : G <= 16 ? 6 : G == 32 ? 5 : 4; 
 constexpr int kBlockThreads = 256;
 constexpr int kBlocksPerCU = 8;
 constexpr int kObjBlocksMax = 2048;
+constexpr double kCouplingBudget = 0.05;  // target of (window - 1) x coupling
+constexpr int kProbes = 8;                // Hutchinson probes of the coupling estimate
 
 }  // namespace
 
@@ -86,6 +90,8 @@ struct scd_solver {
     int cus = 0;
     size_t max_lds = 0;
     int64_t max_seg = 0;
+    double coupling = 0.0, coherence = 0.0;
+    int64_t auto_window = 0;
     // options
     int64_t window = 0;
     int64_t group = 0;
@@ -106,7 +112,8 @@ int plan_epoch(const scd_solver* h, LaunchPlan* lp, uint32_t* n_groups) {
     memset(lp, 0, sizeof *lp);
     lp->fresh = (int)h->fresh;
     const int G = h->group ? (int)h->group : auto_group(h);
-    if (h->window == 1) {
+    const int64_t window = h->window ? h->window : h->auto_window;
+    if (window == 1) {
         const size_t need = ((size_t)((h->L + 63) & ~int64_t(63)) + 2 * 16) * sizeof(float);
         if (need <= h->max_lds) {
             lp->kind = PLAN_ORDERED_LDS;
@@ -126,7 +133,7 @@ int plan_epoch(const scd_solver* h, LaunchPlan* lp, uint32_t* n_groups) {
     const int64_t cap_blocks = (int64_t)h->cus * kBlocksPerCU;
     if (G == kBlockThreads) {
         int64_t groups = cap_blocks;
-        if (h->window > 0 && h->window < groups) groups = h->window;
+        if (window > 0 && window < groups) groups = window;
         if (groups > h->C) groups = h->C;
         if (groups < 1) groups = 1;
         lp->kind = PLAN_BLOCK;
@@ -136,7 +143,7 @@ int plan_epoch(const scd_solver* h, LaunchPlan* lp, uint32_t* n_groups) {
     }
     const int64_t per_block = kBlockThreads / G;
     int64_t groups = cap_blocks * per_block;
-    if (h->window > 0 && h->window < groups) groups = h->window;
+    if (window > 0 && window < groups) groups = window;
     if (groups > h->C) groups = h->C;
     if (groups < 1) groups = 1;
     lp->kind = PLAN_GROUP;
@@ -314,6 +321,35 @@ int scd_create(const scd_matrix_t* A, const float* y, double lambda, int32_t for
         hip(launch_norms(h->ptr, h->idx, h->val, formulation == SCD_RIDGE_PRIMAL ? h->y : nullptr, (uint32_t)h->C,
                          G, obj_blocks(h, G), h->norms, h->cy, s),
             "norms");
+        // Coupling of the coordinates (sets the default window), using h->u as the probe vector.
+        const float mu = formulation == SCD_SVM_DUAL ? 0.0f : (float)(lambda * (double)h->n_rows);
+        const float* sign = formulation == SCD_SVM_DUAL ? h->y : nullptr;
+        double fro2 = 0.0, coh2 = 0.0, diag2 = 0.0, diag1 = 0.0, cn = 0.0;
+        for (uint32_t probe = 0; probe <= (uint32_t)kProbes && rc == SCD_OK; ++probe) {
+            hip(launch_probe(h->ptr, h->idx, h->val, h->norms, sign, (uint32_t)h->C, h->L, mu, probe, G,
+                             obj_blocks(h, G), h->u, h->partials, h->sums, s),
+                "coupling probe");
+            hip(hipMemcpyAsync(h->host_sums, h->sums, 4 * sizeof(double), hipMemcpyDeviceToHost, s), "copy probe");
+            hip(hipStreamSynchronize(s), "synchronize");
+            if (rc != SCD_OK) break;
+            if (probe == 0) {
+                coh2 = h->host_sums[0];
+                diag2 = h->host_sums[1];
+                diag1 = h->host_sums[2];
+                cn = h->host_sums[3];
+            } else {
+                fro2 += h->host_sums[0] / kProbes;
+            }
+        }
+        if (rc == SCD_OK) {
+            const double pairs = cn * (cn - 1.0);
+            h->coupling = pairs > 0.0 ? std::max(0.0, fro2 - diag2) / pairs : 0.0;
+            h->coherence = pairs > 0.0 ? (coh2 - diag1) / pairs : 0.0;
+            int64_t w = INT64_MAX;
+            if (h->coupling > 0.0) w = (int64_t)std::min(9.0e18, std::floor(kCouplingBudget / h->coupling));
+            if (h->coupling > 1e-6) w = std::min<int64_t>(w, std::max<int64_t>(1, h->C / 16));
+            h->auto_window = std::max<int64_t>(1, std::min<int64_t>(w, h->C));
+        }
         hip(hipMemsetAsync(h->model, 0, sizeof(float) * (size_t)h->C, s), "zero model");
         hip(hipMemsetAsync(h->u, 0, sizeof(float) * (size_t)h->L, s), "zero shared");
         hip(hipStreamSynchronize(s), "synchronize");
@@ -455,6 +491,9 @@ int scd_get_info(scd_handle_t h, scd_info_t* info) {
     info->max_segment = h->max_seg;
     info->window = n_groups;
     info->lambda = h->lambda;
+    info->coupling = h->coupling;
+    info->coherence = h->coherence;
+    info->auto_window = h->auto_window;
     return SCD_OK;
 }
 

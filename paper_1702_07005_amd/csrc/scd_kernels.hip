@@ -436,6 +436,70 @@ __global__ __launch_bounds__(256) void k_obj_vector(const float* __restrict__ u,
     block_reduce_store<2>(t, partials + (size_t)blockIdx.x * 2);
 }
 
+// ----------------------------------------------------------------------------------------
+// Coupling probe (set-up only).  With a~_c = sigma_c a_c / sqrt(|a_c|^2 + mu) (sigma_c = the
+// label for the SVM, 1 otherwise; mu = lambda N for the ridge steps, 0 for the SVM step),
+// G = A~^T A~ holds the step-normalised couplings between coordinates.  A probe with signs
+// z_c scatters T = A~ z; the gather pass then sums |(A~^T T)_c|^2 = |G z|^2_c (Hutchinson:
+// E|G z|^2 = |G|_F^2) and the diagonal terms G_cc^2.  z = 1 (probe 0) gives the coherent
+// sum |A~ 1|^2 instead (vector pass).
+// ----------------------------------------------------------------------------------------
+__device__ __forceinline__ float probe_sign(uint32_t c, uint32_t probe) {
+    if (probe == 0) return 1.0f;
+    return (murmur_fmix32(c ^ (probe * 0x9E3779B9u)) & 1u) ? 1.0f : -1.0f;
+}
+
+template <int G>
+__global__ __launch_bounds__(256) void k_probe_scatter(const int64_t* __restrict__ ptr, const int32_t* __restrict__ idx,
+                                                       const float* __restrict__ val, const float* __restrict__ norms,
+                                                       const float* __restrict__ sign, uint32_t C, float mu,
+                                                       uint32_t probe, float* __restrict__ T) {
+    const int lane = threadIdx.x & (G - 1);
+    const uint32_t ngroups = gridDim.x * (256u / G);
+    for (uint32_t c = (blockIdx.x * 256u + threadIdx.x) / G; c < C; c += ngroups) {
+        const float sc = norms[c];
+        if (!(sc > 0.0f)) continue;
+        const float coef = probe_sign(c, probe) * (sign ? sign[c] : 1.0f) * rsqrtf(sc + mu);
+        for (int64_t k = ptr[c] + lane; k < ptr[c + 1]; k += G) atomic_add_u(T + idx[k], coef * val[k]);
+    }
+}
+
+template <int G>
+__global__ __launch_bounds__(256) void k_probe_gather(const int64_t* __restrict__ ptr, const int32_t* __restrict__ idx,
+                                                      const float* __restrict__ val, const float* __restrict__ norms,
+                                                      const float* __restrict__ sign, const float* __restrict__ T,
+                                                      uint32_t C, float mu, double* __restrict__ partials) {
+    const int lane = threadIdx.x & (G - 1);
+    const uint32_t ngroups = gridDim.x * (256u / G);
+    double t[4] = {0.0, 0.0, 0.0, 0.0};  // |G z|^2, sum G_cc^2, sum G_cc, non-empty coordinates
+    for (uint32_t c = (blockIdx.x * 256u + threadIdx.x) / G; c < C; c += ngroups) {
+        const float sc = norms[c];
+        if (!(sc > 0.0f)) continue;
+        double d = 0.0;
+        for (int64_t k = ptr[c] + lane; k < ptr[c + 1]; k += G) d += (double)val[k] * (double)T[idx[k]];
+        d = group_sum_f64<G>(d);
+        if (lane == 0) {
+            const double scale = (sign ? (double)sign[c] : 1.0) / sqrt((double)sc + (double)mu);
+            const double g = d * scale;
+            const double diag = (double)sc / ((double)sc + (double)mu);
+            t[0] += g * g;
+            t[1] += diag * diag;
+            t[2] += diag;
+            t[3] += 1.0;
+        }
+    }
+    block_reduce_store<4>(t, partials + (size_t)blockIdx.x * 4);
+}
+
+__global__ __launch_bounds__(256) void k_sumsq(const float* __restrict__ T, int64_t L, double* __restrict__ partials) {
+    double t[1] = {0.0};
+    for (int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x; i < L; i += (int64_t)gridDim.x * 256) {
+        const double x = T[i];
+        t[0] += x * x;
+    }
+    block_reduce_store<1>(t, partials + blockIdx.x);
+}
+
 // Sum `nparts` rows of `width` doubles in index order (one workgroup; deterministic).
 __global__ __launch_bounds__(256) void k_sum_partials(const double* __restrict__ partials, int nparts, int width,
                                                       double* __restrict__ out) {
@@ -598,6 +662,34 @@ hipError_t launch_objective(int form, const ObjArgs& o, int G, int blocks, doubl
     }
     hipLaunchKernelGGL(k_sum_partials, dim3(1), dim3(256), 0, s, pc, blocks, 3, sums);
     hipLaunchKernelGGL(k_sum_partials, dim3(1), dim3(256), 0, s, pv, blocks, 2, sums + 3);
+    return hipGetLastError();
+}
+
+// out[0] = |G z|^2 (probe > 0) or |A~ 1|^2 (probe 0), out[1] = sum G_cc^2, out[2] = sum G_cc,
+// out[3] = non-empty coordinates.
+hipError_t launch_probe(const int64_t* ptr, const int32_t* idx, const float* val, const float* norms,
+                        const float* sign, uint32_t C, int64_t L, float mu, uint32_t probe, int G, int blocks,
+                        float* T, double* partials, double* out, hipStream_t s) {
+    hipError_t e = hipMemsetAsync(T, 0, sizeof(float) * (size_t)L, s);
+    if (e != hipSuccess) return e;
+#define SCD_PROBE(GW)                                                                                          \
+    hipLaunchKernelGGL(k_probe_scatter<GW>, dim3(blocks), dim3(256), 0, s, ptr, idx, val, norms, sign, C, mu, \
+                       probe, T);                                                                              \
+    hipLaunchKernelGGL(k_probe_gather<GW>, dim3(blocks), dim3(256), 0, s, ptr, idx, val, norms, sign, T, C,   \
+                       mu, partials)
+    switch (G) {
+        case 4: SCD_PROBE(4); break;
+        case 8: SCD_PROBE(8); break;
+        case 16: SCD_PROBE(16); break;
+        case 32: SCD_PROBE(32); break;
+        default: SCD_PROBE(64); break;
+    }
+#undef SCD_PROBE
+    hipLaunchKernelGGL(k_sum_partials, dim3(1), dim3(256), 0, s, partials, blocks, 4, out);
+    if (probe == 0) {
+        hipLaunchKernelGGL(k_sumsq, dim3(blocks), dim3(256), 0, s, T, L, partials);
+        hipLaunchKernelGGL(k_sum_partials, dim3(1), dim3(256), 0, s, partials, blocks, 1, out);
+    }
     return hipGetLastError();
 }
 

@@ -399,3 +399,37 @@ def test_state_roundtrip_and_options():
     assert torch.equal(m, m2) and torch.equal(w, w2) and ep2 == 2
     s.close()
     t.close()
+
+
+# ---------------------------------------------------------------------------------- coupling / window
+
+def _exact_coupling(p):
+    """Mean squared off-diagonal entry of the step-normalised Gram matrix, computed densely."""
+    import scipy.sparse as sps
+    A = sps.csc_matrix((p.val.astype(np.float64), p.idx, p.ptr), shape=(p.L, p.C))
+    s = np.asarray(A.multiply(A).sum(axis=0)).ravel()
+    mu = 0.0 if p.form == "svm_dual" else p.lam * p.n_rows
+    nz = s > 0
+    sig = p.y.astype(np.float64) if p.form == "svm_dual" else np.ones(p.C)
+    At = (A @ sps.diags(np.where(nz, sig / np.sqrt(s + mu), 0.0))).toarray()
+    G = At.T @ At
+    cn = nz.sum()
+    off = (G * G).sum() - (np.diag(G) ** 2).sum()
+    return off / (cn * (cn - 1))
+
+
+@pytest.mark.parametrize("key,over", [("dense_ridge", {}),
+                                      ("text_svm", dict(n_rows=1500, n_cols=40_000, row_nnz=200)),
+                                      ("click_svm", dict(n_rows=2000, n_cols=5000)),
+                                      ("sparse_ridge", dict(n_rows=4000, n_cols=1500, density=0.01))])
+def test_coupling_estimate_and_default_window(key, over):
+    p = synth.make(key, **over)
+    s = scd.solver_for(p)
+    info = s.info()
+    exact = _exact_coupling(p)
+    est = info["coupling"]
+    assert 0.3 * exact <= est <= 3.0 * exact, (est, exact)
+    w = info["auto_window"]
+    assert 1 <= w <= p.C
+    assert w <= max(1, int(0.05 / est)) if est > 0 else True
+    s.close()
