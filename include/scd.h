@@ -97,9 +97,10 @@ typedef struct {
     int64_t max_segment;  /* longest coordinate segment                                */
     int64_t window;       /* coordinates in flight at most (persistent groups)         */
     double lambda;
-    double coupling;      /* mean squared off-diagonal entry of the step-normalised Gram
-                             matrix of the coordinates (estimated at create)            */
-    double coherence;     /* mean off-diagonal entry of the same matrix (signed sum)     */
+    double coupling;      /* largest over coordinates c of sum_{j != c} G_cj^2 / (C - 1), G the
+                             step-normalised Gram matrix of the coordinates (estimated at
+                             create with Rademacher probes)                             */
+    double coherence;     /* mean off-diagonal entry of G (signed sum)                  */
     int64_t auto_window;  /* window chosen from `coupling` when the option is 0         */
 } scd_info_t;
 
@@ -156,8 +157,8 @@ int scd_set_state(scd_handle_t h, const float *model_dev, const float *shared_de
 /* Tuning and test options (host-side, take effect at the next scd_epochs):
  *   "window"      coordinates in flight at most; 1 = ordered (Alg. 1's sequence exactly);
  *                 0 (default) = chosen at create from the measured coupling of the coordinates:
- *                 W = 0.05 / coupling, at most C/16 when the coupling exceeds 1e-6, at most what
- *                 the GPU holds.  Concurrent coordinates read each other's stale shared-vector
+ *                 W = 1 + b / coupling (b = 0.15 for the SVM dual, 0.02 for the ridge forms), at
+ *                 most C/16 when the coupling exceeds 1e-6, at most what the GPU holds.  Concurrent coordinates read each other's stale shared-vector
  *                 entries; strongly coupled problems need a small window to keep the per-epoch
  *                 convergence of the sequential algorithm.
  *   "group"       lanes per coordinate: 0 = by segment length (default), 4, 8, 16, 32, 64, or

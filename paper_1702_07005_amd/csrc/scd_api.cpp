@@ -64,7 +64,10 @@ int cached_per_lane(int G) { return G <= 4 ? 4 : G <= 16 ? 6 : G == 32 ? 5 : 4; 
 constexpr int kBlockThreads = 256;
 constexpr int kBlocksPerCU = 8;
 constexpr int kObjBlocksMax = 2048;
-constexpr double kCouplingBudget = 0.05;  // target of (window - 1) x coupling
+// Window rule: (window - 1) x (worst coordinate's mean squared coupling) <= budget.  The SVM's
+// box projection tolerates stale reads far better than the unconstrained ridge steps.
+constexpr double kCouplingBudgetSvm = 0.15;
+constexpr double kCouplingBudgetRidge = 0.02;
 constexpr int kProbes = 8;                // Hutchinson probes of the coupling estimate
 
 }  // namespace
@@ -325,9 +328,10 @@ int scd_create(const scd_matrix_t* A, const float* y, double lambda, int32_t for
         const float mu = formulation == SCD_SVM_DUAL ? 0.0f : (float)(lambda * (double)h->n_rows);
         const float* sign = formulation == SCD_SVM_DUAL ? h->y : nullptr;
         double fro2 = 0.0, coh2 = 0.0, diag2 = 0.0, diag1 = 0.0, cn = 0.0;
+        hip(hipMemsetAsync(h->model, 0, sizeof(float) * (size_t)h->C, s), "zero probe sums");  // K[c]
         for (uint32_t probe = 0; probe <= (uint32_t)kProbes && rc == SCD_OK; ++probe) {
             hip(launch_probe(h->ptr, h->idx, h->val, h->norms, sign, (uint32_t)h->C, h->L, mu, probe, G,
-                             obj_blocks(h, G), h->u, h->partials, h->sums, s),
+                             obj_blocks(h, G), h->u, h->model, h->partials, h->sums, s),
                 "coupling probe");
             hip(hipMemcpyAsync(h->host_sums, h->sums, 4 * sizeof(double), hipMemcpyDeviceToHost, s), "copy probe");
             hip(hipStreamSynchronize(s), "synchronize");
@@ -341,12 +345,25 @@ int scd_create(const scd_matrix_t* A, const float* y, double lambda, int32_t for
                 fro2 += h->host_sums[0] / kProbes;
             }
         }
+        unsigned kmax_bits = 0;
+        hip(hipMemsetAsync(h->flags, 0, sizeof(unsigned), s), "zero kappa");
+        hip(launch_kappa_max(h->model, h->norms, (uint32_t)h->C, mu, kProbes, obj_blocks(h, G),
+                             reinterpret_cast<unsigned*>(h->flags), s),
+            "kappa max");
+        hip(hipMemcpyAsync(&kmax_bits, h->flags, sizeof(unsigned), hipMemcpyDeviceToHost, s), "copy kappa");
+        hip(hipStreamSynchronize(s), "synchronize");
         if (rc == SCD_OK) {
+            float kmax = 0.0f;
+            memcpy(&kmax, &kmax_bits, sizeof kmax);
             const double pairs = cn * (cn - 1.0);
-            h->coupling = pairs > 0.0 ? std::max(0.0, fro2 - diag2) / pairs : 0.0;
             h->coherence = pairs > 0.0 ? (coh2 - diag1) / pairs : 0.0;
+            // Worst coordinate's mean squared coupling to one other coordinate.
+            h->coupling = cn > 1.0 ? (double)kmax / (cn - 1.0) : 0.0;
+            (void)fro2;
+            (void)diag2;
+            const double budget = formulation == SCD_SVM_DUAL ? kCouplingBudgetSvm : kCouplingBudgetRidge;
             int64_t w = INT64_MAX;
-            if (h->coupling > 0.0) w = (int64_t)std::min(9.0e18, std::floor(kCouplingBudget / h->coupling));
+            if (h->coupling > 0.0) w = 1 + (int64_t)std::min(9.0e18, std::floor(budget / h->coupling));
             if (h->coupling > 1e-6) w = std::min<int64_t>(w, std::max<int64_t>(1, h->C / 16));
             h->auto_window = std::max<int64_t>(1, std::min<int64_t>(w, h->C));
         }

@@ -468,7 +468,8 @@ template <int G>
 __global__ __launch_bounds__(256) void k_probe_gather(const int64_t* __restrict__ ptr, const int32_t* __restrict__ idx,
                                                       const float* __restrict__ val, const float* __restrict__ norms,
                                                       const float* __restrict__ sign, const float* __restrict__ T,
-                                                      uint32_t C, float mu, double* __restrict__ partials) {
+                                                      uint32_t C, float mu, float* __restrict__ K,
+                                                      double* __restrict__ partials) {
     const int lane = threadIdx.x & (G - 1);
     const uint32_t ngroups = gridDim.x * (256u / G);
     double t[4] = {0.0, 0.0, 0.0, 0.0};  // |G z|^2, sum G_cc^2, sum G_cc, non-empty coordinates
@@ -486,9 +487,25 @@ __global__ __launch_bounds__(256) void k_probe_gather(const int64_t* __restrict_
             t[1] += diag * diag;
             t[2] += diag;
             t[3] += 1.0;
+            if (K) K[c] += (float)(g * g);  // per-coordinate |(G z)_c|^2, summed over probes
         }
     }
     block_reduce_store<4>(t, partials + (size_t)blockIdx.x * 4);
+}
+
+// Largest per-coordinate off-diagonal row mass kappa_c = |G_c,:|^2 - G_cc^2, from the probe sums
+// K[c] over `probes` Rademacher probes.  Non-negative floats order like their bit patterns.
+__global__ __launch_bounds__(256) void k_kappa_max(const float* __restrict__ K, const float* __restrict__ norms,
+                                                   uint32_t C, float mu, float inv_probes, unsigned* __restrict__ out) {
+    float best = 0.0f;
+    for (uint32_t c = blockIdx.x * 256u + threadIdx.x; c < C; c += gridDim.x * 256u) {
+        const float sc = norms[c];
+        if (!(sc > 0.0f)) continue;
+        const float d = sc / (sc + mu);
+        best = fmaxf(best, K[c] * inv_probes - d * d);
+    }
+    for (int o = 32; o > 0; o >>= 1) best = fmaxf(best, __shfl_xor(best, o, 64));
+    if ((threadIdx.x & 63) == 0 && best > 0.0f) atomicMax(out, __float_as_uint(best));
 }
 
 __global__ __launch_bounds__(256) void k_sumsq(const float* __restrict__ T, int64_t L, double* __restrict__ partials) {
@@ -669,14 +686,14 @@ hipError_t launch_objective(int form, const ObjArgs& o, int G, int blocks, doubl
 // out[3] = non-empty coordinates.
 hipError_t launch_probe(const int64_t* ptr, const int32_t* idx, const float* val, const float* norms,
                         const float* sign, uint32_t C, int64_t L, float mu, uint32_t probe, int G, int blocks,
-                        float* T, double* partials, double* out, hipStream_t s) {
+                        float* T, float* K, double* partials, double* out, hipStream_t s) {
     hipError_t e = hipMemsetAsync(T, 0, sizeof(float) * (size_t)L, s);
     if (e != hipSuccess) return e;
 #define SCD_PROBE(GW)                                                                                          \
     hipLaunchKernelGGL(k_probe_scatter<GW>, dim3(blocks), dim3(256), 0, s, ptr, idx, val, norms, sign, C, mu, \
                        probe, T);                                                                              \
     hipLaunchKernelGGL(k_probe_gather<GW>, dim3(blocks), dim3(256), 0, s, ptr, idx, val, norms, sign, T, C,   \
-                       mu, partials)
+                       mu, probe ? K : nullptr, partials)
     switch (G) {
         case 4: SCD_PROBE(4); break;
         case 8: SCD_PROBE(8); break;
@@ -690,6 +707,12 @@ hipError_t launch_probe(const int64_t* ptr, const int32_t* idx, const float* val
         hipLaunchKernelGGL(k_sumsq, dim3(blocks), dim3(256), 0, s, T, L, partials);
         hipLaunchKernelGGL(k_sum_partials, dim3(1), dim3(256), 0, s, partials, blocks, 1, out);
     }
+    return hipGetLastError();
+}
+
+hipError_t launch_kappa_max(const float* K, const float* norms, uint32_t C, float mu, int probes, int blocks,
+                            unsigned* out, hipStream_t s) {
+    hipLaunchKernelGGL(k_kappa_max, dim3(blocks), dim3(256), 0, s, K, norms, C, mu, 1.0f / (float)probes, out);
     return hipGetLastError();
 }
 

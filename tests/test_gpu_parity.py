@@ -404,7 +404,8 @@ def test_state_roundtrip_and_options():
 # ---------------------------------------------------------------------------------- coupling / window
 
 def _exact_coupling(p):
-    """Mean squared off-diagonal entry of the step-normalised Gram matrix, computed densely."""
+    """Largest per-coordinate mean squared off-diagonal entry of the step-normalised Gram
+    matrix, computed densely."""
     import scipy.sparse as sps
     A = sps.csc_matrix((p.val.astype(np.float64), p.idx, p.ptr), shape=(p.L, p.C))
     s = np.asarray(A.multiply(A).sum(axis=0)).ravel()
@@ -414,8 +415,8 @@ def _exact_coupling(p):
     At = (A @ sps.diags(np.where(nz, sig / np.sqrt(s + mu), 0.0))).toarray()
     G = At.T @ At
     cn = nz.sum()
-    off = (G * G).sum() - (np.diag(G) ** 2).sum()
-    return off / (cn * (cn - 1))
+    kappa = (G * G).sum(axis=1) - np.diag(G) ** 2
+    return kappa.max() / (cn - 1)
 
 
 @pytest.mark.parametrize("key,over", [("dense_ridge", {}),
@@ -428,8 +429,9 @@ def test_coupling_estimate_and_default_window(key, over):
     info = s.info()
     exact = _exact_coupling(p)
     est = info["coupling"]
-    assert 0.3 * exact <= est <= 3.0 * exact, (est, exact)
+    # The maximum of noisy per-coordinate estimates is biased upwards (conservative).
+    assert 0.5 * exact <= est <= 4.0 * exact, (est, exact)
     w = info["auto_window"]
-    assert 1 <= w <= p.C
-    assert w <= max(1, int(0.05 / est)) if est > 0 else True
+    budget = 0.15 if p.form == "svm_dual" else 0.02
+    assert 1 <= w <= min(p.C, 1 + int(budget / est))
     s.close()
