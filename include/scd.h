@@ -102,6 +102,8 @@ typedef struct {
                              create with Rademacher probes)                             */
     double coherence;     /* mean off-diagonal entry of G (signed sum)                  */
     int64_t auto_window;  /* window chosen from `coupling` when the option is 0         */
+    int64_t long_len;     /* segments longer than this are processed by a whole
+                             workgroup inside the group kernel (0 = none are)          */
 } scd_info_t;
 
 /* Create a solver for min P / max D of the chosen formulation (Sec. II; Sec. III-C).

@@ -149,9 +149,18 @@ int plan_epoch(const scd_solver* h, LaunchPlan* lp, uint32_t* n_groups) {
     if (window > 0 && window < groups) groups = window;
     if (groups > h->C) groups = h->C;
     if (groups < 1) groups = 1;
-    lp->kind = PLAN_GROUP;
+    // Segments longer than twice the group's register cache would keep their gather-to-scatter
+    // interval open far longer than the others: give them the whole workgroup.
+    const int64_t long_len = 2 * (int64_t)G * cached_per_lane(G);
+    lp->kind = h->max_seg > long_len ? PLAN_MIXED : PLAN_GROUP;
+    lp->long_len = (uint32_t)long_len;
     lp->group = G;
     lp->blocks = (int)((groups + per_block - 1) / per_block);
+    if (lp->kind == PLAN_MIXED) {
+        // Each workgroup takes ceil(groups / blocks) positions per batch.
+        const int64_t ng = (groups + lp->blocks - 1) / lp->blocks;
+        groups = ng * lp->blocks;
+    }
     *n_groups = (uint32_t)groups;
     return SCD_OK;
 }
@@ -500,7 +509,9 @@ int scd_get_info(scd_handle_t h, scd_info_t* info) {
     uint32_t n_groups = 1;
     plan_epoch(h, &lp, &n_groups);
     info->formulation = h->form;
-    info->group_lanes = lp.kind == PLAN_GROUP ? lp.group : lp.kind == PLAN_BLOCK && !lp.ordered ? kBlockThreads : 1024;
+    info->group_lanes = (lp.kind == PLAN_GROUP || lp.kind == PLAN_MIXED) ? lp.group
+                        : lp.kind == PLAN_BLOCK && !lp.ordered ? kBlockThreads : 1024;
+    info->long_len = lp.kind == PLAN_MIXED ? lp.long_len : 0;
     info->n_coords = h->C;
     info->shared_len = h->L;
     info->nnz = h->nnz;

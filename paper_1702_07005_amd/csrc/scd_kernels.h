@@ -39,7 +39,7 @@ struct EpochArgs {
     uint32_t pad_;
 };
 
-enum { PLAN_GROUP = 0, PLAN_BLOCK = 1, PLAN_ORDERED_LDS = 2 };
+enum { PLAN_GROUP = 0, PLAN_BLOCK = 1, PLAN_ORDERED_LDS = 2, PLAN_MIXED = 3 };
 
 struct LaunchPlan {
     int kind;        // PLAN_*
@@ -48,6 +48,7 @@ struct LaunchPlan {
     int fresh;       // device-scope gathers
     int ordered;     // PLAN_BLOCK with a single workgroup, fenced between coordinates
     uint32_t L;      // shared-vector length (PLAN_ORDERED_LDS)
+    uint32_t long_len;  // PLAN_MIXED: segments longer than this go to the whole workgroup
     size_t lds_bytes;
 };
 

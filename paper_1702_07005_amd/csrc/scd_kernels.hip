@@ -178,6 +178,91 @@ __global__ __launch_bounds__(256) void k_epoch_group(EpochArgs a) {
 }
 
 // ----------------------------------------------------------------------------------------
+// Epoch kernel for skewed segment lengths: a 256-thread workgroup takes a batch of NG = 256/G
+// consecutive permutation positions per round, one per group.  Segments up to `long_len`
+// entries are processed by their group as in k_epoch_group; longer ones are handed to the
+// whole workgroup (LDS combine), one after the other, so that a long segment's gather-to-
+// scatter interval stays as short as a short segment's.  One barrier per batch (vote) plus
+// one per long segment.
+// ----------------------------------------------------------------------------------------
+// `ng` (<= NG) groups of each workgroup take positions, so that gridDim.x * ng coordinates
+// are in flight at most.
+template <int FORM, int G, int R, bool FRESH>
+__global__ __launch_bounds__(256) void k_epoch_mixed(EpochArgs a, uint32_t long_len, uint32_t ng) {
+    constexpr int NG = 256 / G, NW = 4;
+    __shared__ uint32_t longs[2][NG];
+    __shared__ float part[2][NW];
+    const int tid = threadIdx.x, lane = tid & (G - 1), grp = tid / G, wave = tid >> 6;
+    const uint32_t n_batches = (a.perm.n + ng - 1) / ng;
+    int lb = 0, pb = 0;
+    for (uint32_t b = blockIdx.x; b < n_batches; b += gridDim.x) {
+        const uint32_t j = b * ng + grp;
+        uint32_t my_long = 0xFFFFFFFFu;
+        if ((uint32_t)grp < ng && j < a.perm.n) {
+            const uint32_t m = perm_at(j, a.perm);
+            const int64_t s0 = a.ptr[m], s1 = a.ptr[m + 1];
+            if (s1 - s0 > (int64_t)long_len) {
+                my_long = m;
+            } else {
+                const float m_old = a.model[m];
+                const float sn = a.norms[m];
+                const float ylab = a.y[m];
+                int ci[R];
+                float cv[R];
+#pragma unroll
+                for (int r = 0; r < R; ++r) {
+                    const int64_t k = s0 + lane + (int64_t)r * G;
+                    if (k < s1) { ci[r] = a.idx[k]; cv[r] = a.val[k]; }
+                    else { ci[r] = -1; cv[r] = 0.0f; }
+                }
+                float acc = 0.0f;
+#pragma unroll
+                for (int r = 0; r < R; ++r)
+                    if (ci[r] >= 0) acc = fmaf(cv[r], ld_u<FRESH>(a.u + ci[r]), acc);
+                for (int64_t k = s0 + lane + (int64_t)R * G; k < s1; k += G)
+                    acc = fmaf(a.val[k], ld_u<FRESH>(a.u + a.idx[k]), acc);
+                const float g = group_sum<G>(acc);
+                float coef;
+                const float m_new = coord_step<FORM>(g, sn, m_old, ylab, a.k, &coef);
+                if (lane == 0) a.model[m] = m_new;
+                if (coef != 0.0f) {
+#pragma unroll
+                    for (int r = 0; r < R; ++r)
+                        if (ci[r] >= 0) atomic_add_u(a.u + ci[r], coef * cv[r]);
+                    for (int64_t k = s0 + lane + (int64_t)R * G; k < s1; k += G)
+                        atomic_add_u(a.u + a.idx[k], coef * a.val[k]);
+                }
+            }
+        }
+        if (lane == 0) longs[lb][grp] = my_long;
+        const int any_long = __syncthreads_or(my_long != 0xFFFFFFFFu);
+        if (any_long) {
+            for (int q = 0; q < NG; ++q) {
+                const uint32_t m = longs[lb][q];
+                if (m == 0xFFFFFFFFu) continue;
+                const int64_t s0 = a.ptr[m], s1 = a.ptr[m + 1];
+                const float m_old = a.model[m];
+                const float sn = a.norms[m];
+                const float ylab = a.y[m];
+                float acc = 0.0f;
+                for (int64_t k = s0 + tid; k < s1; k += 256) acc = fmaf(a.val[k], ld_u<FRESH>(a.u + a.idx[k]), acc);
+                acc = group_sum<64>(acc);
+                if ((tid & 63) == 0) part[pb][wave] = acc;
+                __syncthreads();
+                const float g = part[pb][0] + part[pb][1] + part[pb][2] + part[pb][3];
+                float coef;
+                const float m_new = coord_step<FORM>(g, sn, m_old, ylab, a.k, &coef);
+                if (tid == 0) a.model[m] = m_new;
+                if (coef != 0.0f)
+                    for (int64_t k = s0 + tid; k < s1; k += 256) atomic_add_u(a.u + a.idx[k], coef * a.val[k]);
+                pb ^= 1;
+            }
+        }
+        lb ^= 1;
+    }
+}
+
+// ----------------------------------------------------------------------------------------
 // Epoch kernel, one workgroup of BS threads per coordinate (long segments): wave sums by
 // DPP, then the BS/64 wave sums through a double-buffered LDS array (one barrier per
 // coordinate).  ORDERED adds a device-scope fence and a barrier after the scatter so that
@@ -545,6 +630,26 @@ static hipError_t launch_group(const EpochArgs& a, int blocks, hipStream_t s) {
     return hipGetLastError();
 }
 
+template <int FORM, int G, bool FRESH>
+static hipError_t launch_mixed(const EpochArgs& a, int blocks, uint32_t long_len, hipStream_t s) {
+    constexpr int R = (G <= 4) ? 4 : (G <= 16) ? 6 : (G == 32) ? 5 : 4;
+    const uint32_t ng = (a.n_groups + blocks - 1) / blocks;  // <= 256 / G by construction of the plan
+    hipLaunchKernelGGL((k_epoch_mixed<FORM, G, R, FRESH>), dim3(blocks), dim3(256), 0, s, a, long_len, ng);
+    return hipGetLastError();
+}
+
+template <int FORM, bool FRESH>
+static hipError_t launch_mixed_g(const EpochArgs& a, int G, int blocks, uint32_t long_len, hipStream_t s) {
+    switch (G) {
+        case 4: return launch_mixed<FORM, 4, FRESH>(a, blocks, long_len, s);
+        case 8: return launch_mixed<FORM, 8, FRESH>(a, blocks, long_len, s);
+        case 16: return launch_mixed<FORM, 16, FRESH>(a, blocks, long_len, s);
+        case 32: return launch_mixed<FORM, 32, FRESH>(a, blocks, long_len, s);
+        case 64: return launch_mixed<FORM, 64, FRESH>(a, blocks, long_len, s);
+        default: return hipErrorInvalidValue;
+    }
+}
+
 template <int FORM, bool FRESH>
 static hipError_t launch_group_g(const EpochArgs& a, int G, int blocks, hipStream_t s) {
     switch (G) {
@@ -573,6 +678,9 @@ static hipError_t launch_epoch_form(const EpochArgs& a, const LaunchPlan& lp, hi
         }
         return hipGetLastError();
     }
+    if (lp.kind == PLAN_MIXED)
+        return lp.fresh ? launch_mixed_g<FORM, true>(a, lp.group, lp.blocks, lp.long_len, s)
+                        : launch_mixed_g<FORM, false>(a, lp.group, lp.blocks, lp.long_len, s);
     return lp.fresh ? launch_group_g<FORM, true>(a, lp.group, lp.blocks, s)
                     : launch_group_g<FORM, false>(a, lp.group, lp.blocks, s);
 }
