@@ -351,7 +351,7 @@ int scd_create(const scd_matrix_t* A, const float* y, double lambda, int32_t for
                 diag1 = h->host_sums[2];
                 cn = h->host_sums[3];
             } else {
-                fro2 += h->host_sums[0] / kProbes;
+                fro2 += h->host_sums[0] / kProbes;  // estimate of sum_c kappa_c
             }
         }
         unsigned kmax_bits = 0;

@@ -524,10 +524,11 @@ __global__ __launch_bounds__(256) void k_obj_vector(const float* __restrict__ u,
 // ----------------------------------------------------------------------------------------
 // Coupling probe (set-up only).  With a~_c = sigma_c a_c / sqrt(|a_c|^2 + mu) (sigma_c = the
 // label for the SVM, 1 otherwise; mu = lambda N for the ridge steps, 0 for the SVM step),
-// G = A~^T A~ holds the step-normalised couplings between coordinates.  A probe with signs
-// z_c scatters T = A~ z; the gather pass then sums |(A~^T T)_c|^2 = |G z|^2_c (Hutchinson:
-// E|G z|^2 = |G|_F^2) and the diagonal terms G_cc^2.  z = 1 (probe 0) gives the coherent
-// sum |A~ 1|^2 instead (vector pass).
+// G = A~^T A~ holds the step-normalised couplings between coordinates.  A probe with
+// Rademacher signs z_c scatters T = A~ z; the gather pass forms (A~^T T)_c - G_cc z_c, the
+// off-diagonal part of (G z)_c, whose square has expectation kappa_c = sum_{j != c} G_cj^2
+// (Hutchinson), accumulated per coordinate in K.  z = 1 (probe 0) gives the coherent sum
+// |A~ 1|^2 instead (vector pass).
 // ----------------------------------------------------------------------------------------
 __device__ __forceinline__ float probe_sign(uint32_t c, uint32_t probe) {
     if (probe == 0) return 1.0f;
@@ -553,7 +554,7 @@ template <int G>
 __global__ __launch_bounds__(256) void k_probe_gather(const int64_t* __restrict__ ptr, const int32_t* __restrict__ idx,
                                                       const float* __restrict__ val, const float* __restrict__ norms,
                                                       const float* __restrict__ sign, const float* __restrict__ T,
-                                                      uint32_t C, float mu, float* __restrict__ K,
+                                                      uint32_t C, float mu, uint32_t probe, float* __restrict__ K,
                                                       double* __restrict__ partials) {
     const int lane = threadIdx.x & (G - 1);
     const uint32_t ngroups = gridDim.x * (256u / G);
@@ -566,28 +567,28 @@ __global__ __launch_bounds__(256) void k_probe_gather(const int64_t* __restrict_
         d = group_sum_f64<G>(d);
         if (lane == 0) {
             const double scale = (sign ? (double)sign[c] : 1.0) / sqrt((double)sc + (double)mu);
-            const double g = d * scale;
             const double diag = (double)sc / ((double)sc + (double)mu);
+            // Off-diagonal part of (G z)_c: its square has expectation sum_{j != c} G_cj^2.
+            const double g = d * scale - diag * (double)probe_sign(c, probe);
             t[0] += g * g;
             t[1] += diag * diag;
             t[2] += diag;
             t[3] += 1.0;
-            if (K) K[c] += (float)(g * g);  // per-coordinate |(G z)_c|^2, summed over probes
+            if (K) K[c] += (float)(g * g);  // summed over probes
         }
     }
     block_reduce_store<4>(t, partials + (size_t)blockIdx.x * 4);
 }
 
-// Largest per-coordinate off-diagonal row mass kappa_c = |G_c,:|^2 - G_cc^2, from the probe sums
-// K[c] over `probes` Rademacher probes.  Non-negative floats order like their bit patterns.
+// Largest per-coordinate off-diagonal row mass kappa_c = sum_{j != c} G_cj^2, from the probe
+// sums K[c] over `probes` Rademacher probes.  Non-negative floats order like their bit patterns.
 __global__ __launch_bounds__(256) void k_kappa_max(const float* __restrict__ K, const float* __restrict__ norms,
                                                    uint32_t C, float mu, float inv_probes, unsigned* __restrict__ out) {
     float best = 0.0f;
     for (uint32_t c = blockIdx.x * 256u + threadIdx.x; c < C; c += gridDim.x * 256u) {
         const float sc = norms[c];
         if (!(sc > 0.0f)) continue;
-        const float d = sc / (sc + mu);
-        best = fmaxf(best, K[c] * inv_probes - d * d);
+        best = fmaxf(best, K[c] * inv_probes);
     }
     for (int o = 32; o > 0; o >>= 1) best = fmaxf(best, __shfl_xor(best, o, 64));
     if ((threadIdx.x & 63) == 0 && best > 0.0f) atomicMax(out, __float_as_uint(best));
@@ -801,7 +802,7 @@ hipError_t launch_probe(const int64_t* ptr, const int32_t* idx, const float* val
     hipLaunchKernelGGL(k_probe_scatter<GW>, dim3(blocks), dim3(256), 0, s, ptr, idx, val, norms, sign, C, mu, \
                        probe, T);                                                                              \
     hipLaunchKernelGGL(k_probe_gather<GW>, dim3(blocks), dim3(256), 0, s, ptr, idx, val, norms, sign, T, C,   \
-                       mu, probe ? K : nullptr, partials)
+                       mu, probe, probe ? K : nullptr, partials)
     switch (G) {
         case 4: SCD_PROBE(4); break;
         case 8: SCD_PROBE(8); break;
