@@ -58,8 +58,6 @@ PermKeys make_perm(uint64_t seed, uint64_t epoch, uint32_t n) {
     return p;
 }
 
-// Register-cache depth of the group kernels (elements per lane kept between gather and scatter).
-int cached_per_lane(int G) { return G <= 4 ? 4 : G <= 16 ? 6 : G == 32 ? 5 : 4; }
 
 constexpr int kBlockThreads = 256;
 constexpr int kBlocksPerCU = 8;
@@ -84,6 +82,7 @@ struct scd_solver {
     float* u = nullptr;
     float* norms = nullptr;
     float* cy = nullptr;  // ridge primal: <y, a_c> per coordinate
+    void* dummy = nullptr;  // one zero entry standing in for idx/val of an all-empty matrix
     int* flags = nullptr;
     double* partials = nullptr;
     double* sums = nullptr;
@@ -107,7 +106,7 @@ int auto_group(const scd_solver* h) {
     const double mean = h->C > 0 ? (double)h->nnz / (double)h->C : 0.0;
     const int widths[5] = {4, 8, 16, 32, 64};
     for (int G : widths)
-        if (mean <= (double)(G * cached_per_lane(G))) return G;
+        if (mean <= (double)(G * slice_depth(G))) return G;
     return kBlockThreads;  // one workgroup per coordinate
 }
 
@@ -151,9 +150,10 @@ int plan_epoch(const scd_solver* h, LaunchPlan* lp, uint32_t* n_groups) {
     if (groups < 1) groups = 1;
     // Segments longer than twice the group's register cache would keep their gather-to-scatter
     // interval open far longer than the others: give them the whole workgroup.
-    const int64_t long_len = 2 * (int64_t)G * cached_per_lane(G);
+    const int64_t long_len = 2 * (int64_t)G * slice_depth(G);
     lp->kind = h->max_seg > long_len ? PLAN_MIXED : PLAN_GROUP;
     lp->long_len = (uint32_t)long_len;
+    lp->tail = h->max_seg > (int64_t)G * slice_depth(G);
     lp->group = G;
     lp->blocks = (int)((groups + per_block - 1) / per_block);
     if (lp->kind == PLAN_MIXED) {
@@ -195,6 +195,7 @@ void release(scd_solver* h) {
     (void)hipFree(h->u);
     (void)hipFree(h->norms);
     (void)hipFree(h->cy);
+    (void)hipFree(h->dummy);
     (void)hipFree(h->flags);
     (void)hipFree(h->partials);
     (void)hipFree(h->sums);
@@ -308,6 +309,13 @@ int scd_create(const scd_matrix_t* A, const float* y, double lambda, int32_t for
     hip(hipMalloc(&h->norms, sizeof(float) * (size_t)h->C), "hipMalloc(norms)");
     if (formulation == SCD_RIDGE_PRIMAL) hip(hipMalloc(&h->cy, sizeof(float) * (size_t)h->C), "hipMalloc(cy)");
     hip(hipMalloc(&h->flags, 2 * sizeof(int64_t)), "hipMalloc(flags)");
+    if (h->nnz == 0) {
+        // The epoch kernels read element 0 of idx/val unconditionally (weight 0 when unused).
+        hip(hipMalloc(&h->dummy, 8), "hipMalloc(dummy)");
+        hip(hipMemsetAsync(h->dummy, 0, 8, s), "zero dummy");
+        h->idx = static_cast<const int32_t*>(h->dummy);
+        h->val = static_cast<const float*>(h->dummy);
+    }
     hip(hipMalloc(&h->partials, sizeof(double) * (size_t)kObjBlocksMax * 5), "hipMalloc(partials)");
     hip(hipMalloc(&h->sums, sizeof(double) * 8), "hipMalloc(sums)");
     hip(hipHostMalloc(&h->host_sums, sizeof(double) * 8, hipHostMallocDefault), "hipHostMalloc");

@@ -8,6 +8,10 @@ namespace scd {
 
 enum { FORM_RIDGE_PRIMAL = 0, FORM_SVM_DUAL = 1, FORM_RIDGE_DUAL = 2 };
 
+// Register-slice depth of the G-lane epoch kernels: each lane keeps up to slice_depth(G)
+// entries of its coordinate's segment between the gather and the scatter.
+constexpr int slice_depth(int G) { return G <= 4 ? 4 : G <= 8 ? 6 : G == 16 ? 10 : G == 32 ? 5 : 4; }
+
 // Keys of one epoch's permutation of [0, n): 4 Feistel round keys on 2h bits.
 struct PermKeys {
     uint32_t k[4];
@@ -49,6 +53,7 @@ struct LaunchPlan {
     int ordered;     // PLAN_BLOCK with a single workgroup, fenced between coordinates
     uint32_t L;      // shared-vector length (PLAN_ORDERED_LDS)
     uint32_t long_len;  // PLAN_MIXED: segments longer than this go to the whole workgroup
+    int tail;           // PLAN_GROUP: some segment is longer than the register slices
     size_t lds_bytes;
 };
 

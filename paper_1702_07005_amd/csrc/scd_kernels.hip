@@ -133,46 +133,104 @@ __device__ __forceinline__ float coord_step(float g, float s, float m_old, float
 }
 
 // ----------------------------------------------------------------------------------------
-// Epoch kernel, sub-wave / wave groups: G lanes per coordinate, 256-thread workgroups,
-// persistent over permutation positions.  The first R*G elements of a segment stay in
-// registers between the gather and the scatter (A is read once); longer segments stream
-// their tail twice.
+// Per-coordinate metadata and register-cached segment slices.
 // ----------------------------------------------------------------------------------------
-template <int FORM, int G, int R, bool FRESH>
+struct CoordMeta {
+    int64_t s0, s1;
+    uint32_t m;
+    float m_old, sn, ylab;
+};
+
+__device__ __forceinline__ CoordMeta load_meta(const EpochArgs& a, uint32_t j) {
+    CoordMeta c;
+    c.m = perm_at(j, a.perm);
+    c.s0 = a.ptr[c.m];
+    c.s1 = a.ptr[c.m + 1];
+    c.m_old = a.model[c.m];
+    c.sn = a.norms[c.m];
+    c.ylab = a.y[c.m];
+    return c;
+}
+
+// Register slice r of a segment: element s0 + lane + r*G.  Lanes past the end read element 0
+// (always present: the library never hands the kernels an empty idx/val) with weight 0, so the
+// hot path needs no branches and the compiler can count outstanding loads exactly.
+template <int G, int R>
+__device__ __forceinline__ void load_seg(const EpochArgs& a, const CoordMeta& c, int lane, int (&ci)[R],
+                                         float (&cv)[R]) {
+#pragma unroll
+    for (int r = 0; r < R; ++r) {
+        const int64_t k = c.s0 + lane + (int64_t)r * G;
+        const bool in = k < c.s1;
+        const int64_t kk = in ? k : 0;
+        ci[r] = a.idx[kk];
+        const float v = a.val[kk];
+        cv[r] = in ? v : 0.0f;
+    }
+}
+
+
+// ----------------------------------------------------------------------------------------
+// Epoch kernel, sub-wave / wave groups: G lanes per coordinate, 256-thread workgroups,
+// persistent over permutation positions j = g, g + P, ...  The first R*G elements of a
+// segment stay in registers between the gather and the scatter (A is read once); longer
+// segments stream their tail twice; TAIL = false is the instantiation for matrices whose
+// segments all fit the register slices (no tail code, exact load counting).
+//
+// Software pipeline: loads and no-return atomics share one in-order completion counter per
+// wave, so waiting for a load also waits for every atomic issued before it.  Each group
+// therefore issues the NEXT coordinate's metadata and segment loads before the CURRENT
+// coordinate's atomics; consuming them later never waits on the scatter.  Issue order per
+// iteration: gathers(k), meta(k+1), [reduce + step k], segment(k+1), atomics(k).
+// ----------------------------------------------------------------------------------------
+template <int FORM, int G, int R, bool FRESH, bool TAIL>
 __global__ __launch_bounds__(256) void k_epoch_group(EpochArgs a) {
     const int lane = threadIdx.x & (G - 1);
     const uint32_t gid = (blockIdx.x * 256u + threadIdx.x) / G;
-    if (gid >= a.n_groups) return;
-    for (uint32_t j = gid; j < a.perm.n; j += a.n_groups) {
-        const uint32_t m = perm_at(j, a.perm);
-        const int64_t s0 = a.ptr[m], s1 = a.ptr[m + 1];
-        const float m_old = a.model[m];
-        const float sn = a.norms[m];
-        const float ylab = a.y[m];
-        int ci[R];
-        float cv[R];
+    if (gid >= a.n_groups || gid >= a.perm.n) return;
+    uint32_t j = gid;
+    CoordMeta cur = load_meta(a, j);
+    int ci[R];
+    float cv[R];
+    load_seg<G, R>(a, cur, lane, ci, cv);
+    for (;;) {
+        float gv[R];
 #pragma unroll
-        for (int r = 0; r < R; ++r) {
-            const int64_t k = s0 + lane + (int64_t)r * G;
-            if (k < s1) { ci[r] = a.idx[k]; cv[r] = a.val[k]; }
-            else { ci[r] = -1; cv[r] = 0.0f; }
-        }
+        for (int r = 0; r < R; ++r) gv[r] = ld_u<FRESH>(a.u + ci[r]);
+        const uint32_t jn = j + a.n_groups;
+        const bool more = jn < a.perm.n;
+        const CoordMeta nxt = load_meta(a, more ? jn : j);
         float acc = 0.0f;
 #pragma unroll
-        for (int r = 0; r < R; ++r)
-            if (ci[r] >= 0) acc = fmaf(cv[r], ld_u<FRESH>(a.u + ci[r]), acc);
-        for (int64_t k = s0 + lane + (int64_t)R * G; k < s1; k += G)
-            acc = fmaf(a.val[k], ld_u<FRESH>(a.u + a.idx[k]), acc);
+        for (int r = 0; r < R; ++r) acc = fmaf(cv[r], gv[r], acc);
+        const int64_t len = cur.s1 - cur.s0;
+        if constexpr (TAIL) {
+            for (int64_t k = cur.s0 + lane + (int64_t)R * G; k < cur.s1; k += G)
+                acc = fmaf(a.val[k], ld_u<FRESH>(a.u + a.idx[k]), acc);
+        }
         const float g = group_sum<G>(acc);
         float coef;
-        const float m_new = coord_step<FORM>(g, sn, m_old, ylab, a.k, &coef);
-        if (lane == 0) a.model[m] = m_new;
+        const float m_new = coord_step<FORM>(g, cur.sn, cur.m_old, cur.ylab, a.k, &coef);
+        if (lane == 0) a.model[cur.m] = m_new;
+        int ni[R];
+        float nv[R];
+        load_seg<G, R>(a, nxt, lane, ni, nv);
         if (coef != 0.0f) {
 #pragma unroll
             for (int r = 0; r < R; ++r)
-                if (ci[r] >= 0) atomic_add_u(a.u + ci[r], coef * cv[r]);
-            for (int64_t k = s0 + lane + (int64_t)R * G; k < s1; k += G)
-                atomic_add_u(a.u + a.idx[k], coef * a.val[k]);
+                if ((int64_t)(lane + r * G) < len) atomic_add_u(a.u + ci[r], coef * cv[r]);
+            if constexpr (TAIL) {
+                for (int64_t k = cur.s0 + lane + (int64_t)R * G; k < cur.s1; k += G)
+                    atomic_add_u(a.u + a.idx[k], coef * a.val[k]);
+            }
+        }
+        if (!more) break;
+        j = jn;
+        cur = nxt;
+#pragma unroll
+        for (int r = 0; r < R; ++r) {
+            ci[r] = ni[r];
+            cv[r] = nv[r];
         }
     }
 }
@@ -625,15 +683,18 @@ __global__ __launch_bounds__(256) void k_sum_partials(const double* __restrict__
 // Host-side launchers.
 // ----------------------------------------------------------------------------------------
 template <int FORM, int G, bool FRESH>
-static hipError_t launch_group(const EpochArgs& a, int blocks, hipStream_t s) {
-    constexpr int R = (G <= 4) ? 4 : (G <= 16) ? 6 : (G == 32) ? 5 : 4;
-    hipLaunchKernelGGL((k_epoch_group<FORM, G, R, FRESH>), dim3(blocks), dim3(256), 0, s, a);
+static hipError_t launch_group(const EpochArgs& a, int blocks, bool tail, hipStream_t s) {
+    constexpr int R = slice_depth(G);
+    if (tail)
+        hipLaunchKernelGGL((k_epoch_group<FORM, G, R, FRESH, true>), dim3(blocks), dim3(256), 0, s, a);
+    else
+        hipLaunchKernelGGL((k_epoch_group<FORM, G, R, FRESH, false>), dim3(blocks), dim3(256), 0, s, a);
     return hipGetLastError();
 }
 
 template <int FORM, int G, bool FRESH>
 static hipError_t launch_mixed(const EpochArgs& a, int blocks, uint32_t long_len, hipStream_t s) {
-    constexpr int R = (G <= 4) ? 4 : (G <= 16) ? 6 : (G == 32) ? 5 : 4;
+    constexpr int R = slice_depth(G);
     const uint32_t ng = (a.n_groups + blocks - 1) / blocks;  // <= 256 / G by construction of the plan
     hipLaunchKernelGGL((k_epoch_mixed<FORM, G, R, FRESH>), dim3(blocks), dim3(256), 0, s, a, long_len, ng);
     return hipGetLastError();
@@ -652,13 +713,13 @@ static hipError_t launch_mixed_g(const EpochArgs& a, int G, int blocks, uint32_t
 }
 
 template <int FORM, bool FRESH>
-static hipError_t launch_group_g(const EpochArgs& a, int G, int blocks, hipStream_t s) {
+static hipError_t launch_group_g(const EpochArgs& a, int G, int blocks, bool tail, hipStream_t s) {
     switch (G) {
-        case 4: return launch_group<FORM, 4, FRESH>(a, blocks, s);
-        case 8: return launch_group<FORM, 8, FRESH>(a, blocks, s);
-        case 16: return launch_group<FORM, 16, FRESH>(a, blocks, s);
-        case 32: return launch_group<FORM, 32, FRESH>(a, blocks, s);
-        case 64: return launch_group<FORM, 64, FRESH>(a, blocks, s);
+        case 4: return launch_group<FORM, 4, FRESH>(a, blocks, tail, s);
+        case 8: return launch_group<FORM, 8, FRESH>(a, blocks, tail, s);
+        case 16: return launch_group<FORM, 16, FRESH>(a, blocks, tail, s);
+        case 32: return launch_group<FORM, 32, FRESH>(a, blocks, tail, s);
+        case 64: return launch_group<FORM, 64, FRESH>(a, blocks, tail, s);
         default: return hipErrorInvalidValue;
     }
 }
@@ -682,8 +743,8 @@ static hipError_t launch_epoch_form(const EpochArgs& a, const LaunchPlan& lp, hi
     if (lp.kind == PLAN_MIXED)
         return lp.fresh ? launch_mixed_g<FORM, true>(a, lp.group, lp.blocks, lp.long_len, s)
                         : launch_mixed_g<FORM, false>(a, lp.group, lp.blocks, lp.long_len, s);
-    return lp.fresh ? launch_group_g<FORM, true>(a, lp.group, lp.blocks, s)
-                    : launch_group_g<FORM, false>(a, lp.group, lp.blocks, s);
+    return lp.fresh ? launch_group_g<FORM, true>(a, lp.group, lp.blocks, lp.tail, s)
+                    : launch_group_g<FORM, false>(a, lp.group, lp.blocks, lp.tail, s);
 }
 
 hipError_t launch_epoch(int form, const EpochArgs& a, const LaunchPlan& lp, hipStream_t s) {
