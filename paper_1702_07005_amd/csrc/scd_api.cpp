@@ -65,7 +65,7 @@ constexpr int kObjBlocksMax = 2048;
 // Window rule: (window - 1) x (worst coordinate's mean squared coupling) <= budget.  The SVM's
 // box projection tolerates stale reads far better than the unconstrained ridge steps.
 constexpr double kCouplingBudgetSvm = 0.15;
-constexpr double kCouplingBudgetRidge = 0.01;
+constexpr double kCouplingBudgetRidge = 0.1;
 constexpr int kProbes = 8;                // Hutchinson probes of the coupling estimate
 
 }  // namespace
