@@ -58,6 +58,22 @@ def measured_traffic(workload: str):
     return t.get("hbm_bytes_per_launch")
 
 
+def device_ceilings(L: int):
+    """Live device-wide rates on this GPU (libscdprobe.so): scattered fp32 atomic adds into an array
+    the size of the shared vector, the same when each add follows a gather from that array, and
+    a 1 GiB streaming copy."""
+    import ctypes
+    lib = ctypes.CDLL(os.path.join(ROOT, "paper_1702_07005_amd", "libscdprobe.so"))
+    lib.scd_probe_rate.argtypes = [ctypes.c_int, ctypes.c_uint64, ctypes.c_void_p, ctypes.POINTER(ctypes.c_double)]
+    out = {}
+    for mode, key, n in ((0, "atomic_adds_per_s", max(L, 1024)), (1, "gather_then_atomic_per_s", max(L, 1024)),
+                         (2, "copy_bytes_per_s", 1 << 28)):
+        v = ctypes.c_double()
+        rc = lib.scd_probe_rate(mode, n, None, ctypes.byref(v))
+        out[key] = v.value if rc == 0 else None
+    return out
+
+
 def cpu_baseline(prob, budget_s: float):
     """The fp64 sequential oracle on the host, same workload from the zero state, run for
     whole epochs until about `budget_s` seconds have elapsed (at least one epoch)."""
@@ -91,6 +107,9 @@ def main():
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--max-gap-epochs", type=int, default=200)
+    ap.add_argument("--calibrate-copy", action="store_true",
+                    help="after the timed steps, run a plain 1 GiB device-to-device copy twice (a kernel of known "
+                         "traffic for scaling rocprofv3 FETCH_SIZE/WRITE_SIZE counters)")
     args = ap.parse_args()
 
     world = int(os.environ.get("WORLD_SIZE", "1"))
@@ -194,6 +213,23 @@ def main():
                      "algorithmic_bytes_per_launch": alg, "kernel": "scd::k_epoch_*"},
     }
     solver.close()
+    ceil = device_ceilings(prob.L)
+    if ceil["atomic_adds_per_s"]:
+        # The scatter issues one device-scope atomic per stored entry.
+        rate = prob.nnz / epoch_avg
+        out["atomic_roofline"] = {"bound": "device-scope fp32 atomics", "achieved": rate,
+                                  "peak": ceil["atomic_adds_per_s"], "unit": "atomic adds/s",
+                                  "frac": rate / ceil["atomic_adds_per_s"],
+                                  "gather_then_atomic_per_s": ceil["gather_then_atomic_per_s"],
+                                  "copy_GBps": (ceil["copy_bytes_per_s"] or 0) / 1e9}
+    if args.calibrate_copy:
+        src = torch.ones(1 << 28, dtype=torch.float32, device=dev)  # 1 GiB
+        dst = torch.empty_like(src)
+        for _ in range(2):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        out["calibration_copy_bytes"] = src.numel() * 4
+        del src, dst
     if not args.no_cpu_baseline:
         print("# oracle on the host", file=sys.stderr, flush=True)
         out["cpu_baseline"] = cpu_baseline(prob, args.cpu_seconds)
