@@ -104,6 +104,9 @@ typedef struct {
     int64_t auto_window;  /* window chosen from `coupling` when the option is 0         */
     int64_t long_len;     /* segments longer than this are processed by a whole
                              workgroup inside the group kernel (0 = none are)          */
+    int32_t shared_fp64;  /* 1 if the shared vector is stored in fp64                   */
+    uint32_t max_hits;    /* most stored entries sharing one shared-vector index, i.e.
+                             the most atomic adds one entry receives per epoch          */
 } scd_info_t;
 
 /* Create a solver for min P / max D of the chosen formulation (Sec. II; Sec. III-C).
@@ -146,7 +149,8 @@ int scd_duality_gap(scd_handle_t h, void *stream, double *gap);
  *   model_dev:  float32[n_coords]   (beta, or alpha)
  *   shared_dev: float32[shared_len] (w = A beta, or w(alpha), or wbar = A^T alpha)
  *   epoch:      host int64 (may be NULL).  Enqueues only.  A state copied out and written
- *   back with scd_set_state resumes bit-exactly. */
+ *   back with scd_set_state resumes bit-exactly when the shared vector is stored in fp32
+ *   (option "shared_fp64" = 0); an fp64 shared vector is exchanged rounded to fp32. */
 int scd_get_state(scd_handle_t h, float *model_dev, float *shared_dev, int64_t *epoch, void *stream);
 
 /* Overwrite the state (resume from a checkpoint).  model_dev/shared_dev in the layout of
@@ -167,6 +171,10 @@ int scd_set_state(scd_handle_t h, const float *model_dev, const float *shared_de
  *                 256 (one workgroup per coordinate).
  *   "fresh_reads" 1 = gather the shared vector with device-scope loads (bypass non-coherent
  *                 caches), 0 = plain loads.
+ *   "shared_fp64" 1 = store the shared vector in fp64 (fp64 atomic adds), 0 = fp32.  Chosen at
+ *                 create: fp64 when some entry receives more than 28,000 atomic adds per epoch,
+ *                 where fp32 accumulation would drift by more than about 1e-5 of its magnitude.
+ *                 The state calls exchange fp32 copies either way.
  * Errors: SCD_ERR_UNSUPPORTED for an unknown key, SCD_ERR_INVALID for a bad value. */
 int scd_set_option(scd_handle_t h, const char *key, int64_t value);
 int scd_get_option(scd_handle_t h, const char *key, int64_t *value);

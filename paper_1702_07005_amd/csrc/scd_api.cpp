@@ -67,6 +67,9 @@ constexpr int kObjBlocksMax = 2048;
 constexpr double kCouplingBudgetSvm = 0.15;
 constexpr double kCouplingBudgetRidge = 0.1;
 constexpr int kProbes = 8;                // Hutchinson probes of the coupling estimate
+// An entry of the shared vector receiving K atomic adds per epoch drifts by about
+// sqrt(K) * 2^-24 of its magnitude in fp32; above this many it is kept in fp64 (drift < 1e-5).
+constexpr uint32_t kWideHits = 28000;
 
 }  // namespace
 
@@ -79,7 +82,9 @@ struct scd_solver {
     const float* y = nullptr;
     double lambda = 0.0;
     float* model = nullptr;
-    float* u = nullptr;
+    void* u = nullptr;  // shared vector: float, or double when `wide`
+    int wide = 0;
+    uint32_t max_hits = 0;  // most stored entries sharing one shared-vector index
     float* norms = nullptr;
     float* cy = nullptr;  // ridge primal: <y, a_c> per coordinate
     void* dummy = nullptr;  // one zero entry standing in for idx/val of an all-empty matrix
@@ -115,8 +120,10 @@ int plan_epoch(const scd_solver* h, LaunchPlan* lp, uint32_t* n_groups) {
     lp->fresh = (int)h->fresh;
     const int G = h->group ? (int)h->group : auto_group(h);
     const int64_t window = h->window ? h->window : h->auto_window;
+    lp->wide = h->wide;
     if (window == 1) {
-        const size_t need = ((size_t)((h->L + 63) & ~int64_t(63)) + 2 * 16) * sizeof(float);
+        const size_t need = (size_t)((h->L + 63) & ~int64_t(63)) * (h->wide ? sizeof(double) : sizeof(float)) +
+                            2 * 16 * sizeof(float);
         if (need <= h->max_lds) {
             lp->kind = PLAN_ORDERED_LDS;
             lp->L = (uint32_t)h->L;
@@ -210,6 +217,7 @@ int reduce_state(scd_solver* h, hipStream_t s) {
     o.idx = h->idx;
     o.val = h->val;
     o.u = h->u;
+    o.wide = h->wide;
     o.model = h->model;
     o.y = h->form == FORM_RIDGE_PRIMAL ? nullptr : h->y;
     o.yv = h->form == FORM_RIDGE_PRIMAL ? h->y : nullptr;
@@ -337,6 +345,21 @@ int scd_create(const scd_matrix_t* A, const float* y, double lambda, int32_t for
         else step(fail(SCD_ERR_NUMERIC, "non-finite matrix value or label"));
     }
     if (rc == SCD_OK) {
+        // Largest number of updates one shared-vector entry receives per epoch (h->u as counters).
+        unsigned* hits = static_cast<unsigned*>(h->u);
+        hip(hipMemsetAsync(hits, 0, sizeof(unsigned) * (size_t)h->L, s), "zero hits");
+        hip(hipMemsetAsync(h->flags, 0, sizeof(unsigned), s), "zero max hits");
+        hip(launch_max_hits(h->idx, h->nnz, h->L, hits, reinterpret_cast<unsigned*>(h->flags), s), "count hits");
+        hip(hipMemcpyAsync(&h->max_hits, h->flags, sizeof(unsigned), hipMemcpyDeviceToHost, s), "copy hits");
+        hip(hipStreamSynchronize(s), "synchronize");
+        if (rc == SCD_OK && h->max_hits > kWideHits) {
+            h->wide = 1;
+            (void)hipFree(h->u);
+            h->u = nullptr;
+            hip(hipMalloc(&h->u, sizeof(double) * (size_t)h->L), "hipMalloc(shared, fp64)");
+        }
+    }
+    if (rc == SCD_OK) {
         const int G = obj_group(h);
         hip(launch_norms(h->ptr, h->idx, h->val, formulation == SCD_RIDGE_PRIMAL ? h->y : nullptr, (uint32_t)h->C,
                          G, obj_blocks(h, G), h->norms, h->cy, s),
@@ -348,7 +371,7 @@ int scd_create(const scd_matrix_t* A, const float* y, double lambda, int32_t for
         hip(hipMemsetAsync(h->model, 0, sizeof(float) * (size_t)h->C, s), "zero probe sums");  // K[c]
         for (uint32_t probe = 0; probe <= (uint32_t)kProbes && rc == SCD_OK; ++probe) {
             hip(launch_probe(h->ptr, h->idx, h->val, h->norms, sign, (uint32_t)h->C, h->L, mu, probe, G,
-                             obj_blocks(h, G), h->u, h->model, h->partials, h->sums, s),
+                             obj_blocks(h, G), static_cast<float*>(h->u), h->model, h->partials, h->sums, s),
                 "coupling probe");
             hip(hipMemcpyAsync(h->host_sums, h->sums, 4 * sizeof(double), hipMemcpyDeviceToHost, s), "copy probe");
             hip(hipStreamSynchronize(s), "synchronize");
@@ -385,7 +408,7 @@ int scd_create(const scd_matrix_t* A, const float* y, double lambda, int32_t for
             h->auto_window = std::max<int64_t>(1, std::min<int64_t>(w, h->C));
         }
         hip(hipMemsetAsync(h->model, 0, sizeof(float) * (size_t)h->C, s), "zero model");
-        hip(hipMemsetAsync(h->u, 0, sizeof(float) * (size_t)h->L, s), "zero shared");
+        hip(hipMemsetAsync(h->u, 0, (h->wide ? sizeof(double) : sizeof(float)) * (size_t)h->L, s), "zero shared");
         hip(hipStreamSynchronize(s), "synchronize");
     }
     if (rc != SCD_OK) {
@@ -416,7 +439,7 @@ int scd_epochs(scd_handle_t h, uint64_t seed, int32_t n_epochs, void* stream) {
     LaunchPlan lp;
     uint32_t n_groups = 1;
     if (int r = plan_epoch(h, &lp, &n_groups)) return r;
-    if (lp.kind == PLAN_ORDERED_LDS) HIP_TRY(ordered_lds_prepare(h->form, lp.lds_bytes));
+    if (lp.kind == PLAN_ORDERED_LDS) HIP_TRY(ordered_lds_prepare(h->form, lp.wide != 0, lp.lds_bytes));
     EpochArgs a{};
     a.ptr = h->ptr;
     a.idx = h->idx;
@@ -464,7 +487,12 @@ int scd_get_state(scd_handle_t h, float* model, float* shared, int64_t* epoch, v
     if (int r = set_device(h)) return r;
     hipStream_t s = (hipStream_t)stream;
     if (model) HIP_TRY(hipMemcpyAsync(model, h->model, sizeof(float) * (size_t)h->C, hipMemcpyDeviceToDevice, s));
-    if (shared) HIP_TRY(hipMemcpyAsync(shared, h->u, sizeof(float) * (size_t)h->L, hipMemcpyDeviceToDevice, s));
+    if (shared) {
+        if (h->wide)
+            HIP_TRY(launch_convert_f64_to_f32(static_cast<const double*>(h->u), h->L, shared, s));
+        else
+            HIP_TRY(hipMemcpyAsync(shared, h->u, sizeof(float) * (size_t)h->L, hipMemcpyDeviceToDevice, s));
+    }
     if (epoch) *epoch = h->epoch;
     return SCD_OK;
 }
@@ -475,7 +503,12 @@ int scd_set_state(scd_handle_t h, const float* model, const float* shared, int64
     if (int r = set_device(h)) return r;
     hipStream_t s = (hipStream_t)stream;
     if (model) HIP_TRY(hipMemcpyAsync(h->model, model, sizeof(float) * (size_t)h->C, hipMemcpyDeviceToDevice, s));
-    if (shared) HIP_TRY(hipMemcpyAsync(h->u, shared, sizeof(float) * (size_t)h->L, hipMemcpyDeviceToDevice, s));
+    if (shared) {
+        if (h->wide)
+            HIP_TRY(launch_convert_f32_to_f64(shared, h->L, static_cast<double*>(h->u), s));
+        else
+            HIP_TRY(hipMemcpyAsync(h->u, shared, sizeof(float) * (size_t)h->L, hipMemcpyDeviceToDevice, s));
+    }
     h->epoch = epoch;
     return SCD_OK;
 }
@@ -494,6 +527,25 @@ int scd_set_option(scd_handle_t h, const char* key, int64_t value) {
     } else if (!strcmp(key, "fresh_reads")) {
         if (value != 0 && value != 1) return fail(SCD_ERR_INVALID, "fresh_reads must be 0 or 1");
         h->fresh = value;
+    } else if (!strcmp(key, "shared_fp64")) {
+        if (value != 0 && value != 1) return fail(SCD_ERR_INVALID, "shared_fp64 must be 0 or 1");
+        if (value == h->wide) return SCD_OK;
+        if (int r = set_device(h)) return r;
+        // Re-store the shared vector at the other width (synchronises the device).
+        void* nu = nullptr;
+        HIP_TRY(hipMalloc(&nu, (value ? sizeof(double) : sizeof(float)) * (size_t)h->L));
+        hipError_t e = value ? launch_convert_f32_to_f64(static_cast<const float*>(h->u), h->L,
+                                                         static_cast<double*>(nu), nullptr)
+                             : launch_convert_f64_to_f32(static_cast<const double*>(h->u), h->L,
+                                                         static_cast<float*>(nu), nullptr);
+        if (e == hipSuccess) e = hipDeviceSynchronize();
+        if (e != hipSuccess) {
+            (void)hipFree(nu);
+            return fail(SCD_ERR_HIP, "shared_fp64 conversion: %s", hipGetErrorString(e));
+        }
+        (void)hipFree(h->u);
+        h->u = nu;
+        h->wide = (int)value;
     } else {
         return fail(SCD_ERR_UNSUPPORTED, "unknown option '%s'", key);
     }
@@ -506,6 +558,7 @@ int scd_get_option(scd_handle_t h, const char* key, int64_t* value) {
     if (!strcmp(key, "window")) *value = h->window;
     else if (!strcmp(key, "group")) *value = h->group;
     else if (!strcmp(key, "fresh_reads")) *value = h->fresh;
+    else if (!strcmp(key, "shared_fp64")) *value = h->wide;
     else return fail(SCD_ERR_UNSUPPORTED, "unknown option '%s'", key);
     return SCD_OK;
 }
@@ -520,6 +573,8 @@ int scd_get_info(scd_handle_t h, scd_info_t* info) {
     info->group_lanes = (lp.kind == PLAN_GROUP || lp.kind == PLAN_MIXED) ? lp.group
                         : lp.kind == PLAN_BLOCK && !lp.ordered ? kBlockThreads : 1024;
     info->long_len = lp.kind == PLAN_MIXED ? lp.long_len : 0;
+    info->shared_fp64 = h->wide;
+    info->max_hits = h->max_hits;
     info->n_coords = h->C;
     info->shared_len = h->L;
     info->nnz = h->nnz;

@@ -35,7 +35,7 @@ struct EpochArgs {
     const float* val;
     const float* y;      // per-coordinate constant: <y, a_c> (ridge primal) or the label (duals)
     float* model;        // [C]
-    float* u;            // shared vector [L]
+    void* u;             // shared vector [L], float or double (LaunchPlan::wide)
     const float* norms;  // [C]
     StepConsts k;
     PermKeys perm;       // perm.n = C
@@ -54,6 +54,7 @@ struct LaunchPlan {
     uint32_t L;      // shared-vector length (PLAN_ORDERED_LDS)
     uint32_t long_len;  // PLAN_MIXED: segments longer than this go to the whole workgroup
     int tail;           // PLAN_GROUP: some segment is longer than the register slices
+    int wide;           // shared vector stored as double
     size_t lds_bytes;
 };
 
@@ -61,7 +62,8 @@ struct ObjArgs {
     const int64_t* ptr;
     const int32_t* idx;
     const float* val;
-    const float* u;      // shared vector as maintained
+    const void* u;       // shared vector as maintained (float, or double when `wide`)
+    int wide;
     const float* model;
     const float* y;      // per-coordinate labels (duals)
     const float* yv;     // per-shared-entry labels (ridge primal: y over rows)
@@ -71,7 +73,10 @@ struct ObjArgs {
 };
 
 hipError_t launch_epoch(int form, const EpochArgs& a, const LaunchPlan& lp, hipStream_t s);
-hipError_t ordered_lds_prepare(int form, size_t lds_bytes);
+hipError_t ordered_lds_prepare(int form, bool wide, size_t lds_bytes);
+hipError_t launch_convert_f32_to_f64(const float* in, int64_t n, double* out, hipStream_t s);
+hipError_t launch_convert_f64_to_f32(const double* in, int64_t n, float* out, hipStream_t s);
+hipError_t launch_max_hits(const int32_t* idx, int64_t nnz, int64_t L, unsigned* hits, unsigned* out, hipStream_t s);
 hipError_t launch_perm_fill(const PermKeys& p, int32_t* out, hipStream_t s);
 hipError_t launch_gather_dots(const int64_t* ptr, const int32_t* idx, const float* val, const float* u, uint32_t C,
                               int G, int blocks, float* out, hipStream_t s);

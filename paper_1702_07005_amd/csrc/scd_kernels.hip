@@ -92,16 +92,22 @@ __device__ __forceinline__ double group_sum_f64(double x) {
 // ----------------------------------------------------------------------------------------
 // Shared-vector access.
 // ----------------------------------------------------------------------------------------
-template <bool FRESH>
-__device__ __forceinline__ float ld_u(const float* p) {
+// The shared vector is stored as U = float, or double where fp32 accumulation would drift
+// (very frequently updated entries); values enter the fp32 dot products as float.
+template <bool FRESH, typename U>
+__device__ __forceinline__ float ld_u(const U* p) {
     if constexpr (FRESH)
-        return __hip_atomic_load(const_cast<float*>(p), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        return (float)__hip_atomic_load(const_cast<U*>(p), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     else
-        return *p;
+        return (float)*p;
 }
 
 __device__ __forceinline__ void atomic_add_u(float* p, float v) {
     __hip_atomic_fetch_add(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+__device__ __forceinline__ void atomic_add_u(double* p, float v) {
+    __hip_atomic_fetch_add(p, (double)v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 
 // ----------------------------------------------------------------------------------------
@@ -183,8 +189,9 @@ __device__ __forceinline__ void load_seg(const EpochArgs& a, const CoordMeta& c,
 // coordinate's atomics; consuming them later never waits on the scatter.  Issue order per
 // iteration: gathers(k), meta(k+1), [reduce + step k], segment(k+1), atomics(k).
 // ----------------------------------------------------------------------------------------
-template <int FORM, int G, int R, bool FRESH, bool TAIL>
+template <int FORM, int G, int R, bool FRESH, bool TAIL, typename U>
 __global__ __launch_bounds__(256) void k_epoch_group(EpochArgs a) {
+    U* const uu = static_cast<U*>(a.u);
     const int lane = threadIdx.x & (G - 1);
     const uint32_t gid = (blockIdx.x * 256u + threadIdx.x) / G;
     if (gid >= a.n_groups || gid >= a.perm.n) return;
@@ -196,7 +203,7 @@ __global__ __launch_bounds__(256) void k_epoch_group(EpochArgs a) {
     for (;;) {
         float gv[R];
 #pragma unroll
-        for (int r = 0; r < R; ++r) gv[r] = ld_u<FRESH>(a.u + ci[r]);
+        for (int r = 0; r < R; ++r) gv[r] = ld_u<FRESH>(uu + ci[r]);
         const uint32_t jn = j + a.n_groups;
         const bool more = jn < a.perm.n;
         const CoordMeta nxt = load_meta(a, more ? jn : j);
@@ -206,7 +213,7 @@ __global__ __launch_bounds__(256) void k_epoch_group(EpochArgs a) {
         const int64_t len = cur.s1 - cur.s0;
         if constexpr (TAIL) {
             for (int64_t k = cur.s0 + lane + (int64_t)R * G; k < cur.s1; k += G)
-                acc = fmaf(a.val[k], ld_u<FRESH>(a.u + a.idx[k]), acc);
+                acc = fmaf(a.val[k], ld_u<FRESH>(uu + a.idx[k]), acc);
         }
         const float g = group_sum<G>(acc);
         float coef;
@@ -218,17 +225,16 @@ __global__ __launch_bounds__(256) void k_epoch_group(EpochArgs a) {
         if (coef != 0.0f) {
 #pragma unroll
             for (int r = 0; r < R; ++r)
-                if ((int64_t)(lane + r * G) < len) atomic_add_u(a.u + ci[r], coef * cv[r]);
+                if ((int64_t)(lane + r * G) < len) atomic_add_u(uu + ci[r], coef * cv[r]);
             if constexpr (TAIL) {
                 for (int64_t k = cur.s0 + lane + (int64_t)R * G; k < cur.s1; k += G)
-                    atomic_add_u(a.u + a.idx[k], coef * a.val[k]);
+                    atomic_add_u(uu + a.idx[k], coef * a.val[k]);
             }
         }
         if (!more) break;
         j = jn;
         cur = nxt;
-#pragma unroll
-        for (int r = 0; r < R; ++r) {
+        for (int r = 0; r < R; ++r) {  // register renaming; scalarised by the compiler
             ci[r] = ni[r];
             cv[r] = nv[r];
         }
@@ -245,8 +251,9 @@ __global__ __launch_bounds__(256) void k_epoch_group(EpochArgs a) {
 // ----------------------------------------------------------------------------------------
 // `ng` (<= NG) groups of each workgroup take positions, so that gridDim.x * ng coordinates
 // are in flight at most.
-template <int FORM, int G, int R, bool FRESH>
+template <int FORM, int G, int R, bool FRESH, typename U>
 __global__ __launch_bounds__(256) void k_epoch_mixed(EpochArgs a, uint32_t long_len, uint32_t ng) {
+    U* const uu = static_cast<U*>(a.u);
     constexpr int NG = 256 / G, NW = 4;
     __shared__ uint32_t longs[2][NG];
     __shared__ float part[2][NW];
@@ -276,9 +283,9 @@ __global__ __launch_bounds__(256) void k_epoch_mixed(EpochArgs a, uint32_t long_
                 float acc = 0.0f;
 #pragma unroll
                 for (int r = 0; r < R; ++r)
-                    if (ci[r] >= 0) acc = fmaf(cv[r], ld_u<FRESH>(a.u + ci[r]), acc);
+                    if (ci[r] >= 0) acc = fmaf(cv[r], ld_u<FRESH>(uu + ci[r]), acc);
                 for (int64_t k = s0 + lane + (int64_t)R * G; k < s1; k += G)
-                    acc = fmaf(a.val[k], ld_u<FRESH>(a.u + a.idx[k]), acc);
+                    acc = fmaf(a.val[k], ld_u<FRESH>(uu + a.idx[k]), acc);
                 const float g = group_sum<G>(acc);
                 float coef;
                 const float m_new = coord_step<FORM>(g, sn, m_old, ylab, a.k, &coef);
@@ -286,9 +293,9 @@ __global__ __launch_bounds__(256) void k_epoch_mixed(EpochArgs a, uint32_t long_
                 if (coef != 0.0f) {
 #pragma unroll
                     for (int r = 0; r < R; ++r)
-                        if (ci[r] >= 0) atomic_add_u(a.u + ci[r], coef * cv[r]);
+                        if (ci[r] >= 0) atomic_add_u(uu + ci[r], coef * cv[r]);
                     for (int64_t k = s0 + lane + (int64_t)R * G; k < s1; k += G)
-                        atomic_add_u(a.u + a.idx[k], coef * a.val[k]);
+                        atomic_add_u(uu + a.idx[k], coef * a.val[k]);
                 }
             }
         }
@@ -303,7 +310,7 @@ __global__ __launch_bounds__(256) void k_epoch_mixed(EpochArgs a, uint32_t long_
                 const float sn = a.norms[m];
                 const float ylab = a.y[m];
                 float acc = 0.0f;
-                for (int64_t k = s0 + tid; k < s1; k += 256) acc = fmaf(a.val[k], ld_u<FRESH>(a.u + a.idx[k]), acc);
+                for (int64_t k = s0 + tid; k < s1; k += 256) acc = fmaf(a.val[k], ld_u<FRESH>(uu + a.idx[k]), acc);
                 acc = group_sum<64>(acc);
                 if ((tid & 63) == 0) part[pb][wave] = acc;
                 __syncthreads();
@@ -312,7 +319,7 @@ __global__ __launch_bounds__(256) void k_epoch_mixed(EpochArgs a, uint32_t long_
                 const float m_new = coord_step<FORM>(g, sn, m_old, ylab, a.k, &coef);
                 if (tid == 0) a.model[m] = m_new;
                 if (coef != 0.0f)
-                    for (int64_t k = s0 + tid; k < s1; k += 256) atomic_add_u(a.u + a.idx[k], coef * a.val[k]);
+                    for (int64_t k = s0 + tid; k < s1; k += 256) atomic_add_u(uu + a.idx[k], coef * a.val[k]);
                 pb ^= 1;
             }
         }
@@ -326,8 +333,9 @@ __global__ __launch_bounds__(256) void k_epoch_mixed(EpochArgs a, uint32_t long_
 // coordinate).  ORDERED adds a device-scope fence and a barrier after the scatter so that
 // with a single workgroup the next coordinate sees every update (sequential Alg. 1).
 // ----------------------------------------------------------------------------------------
-template <int FORM, int BS, int R, bool FRESH, bool ORDERED>
+template <int FORM, int BS, int R, bool FRESH, bool ORDERED, typename U>
 __global__ __launch_bounds__(BS) void k_epoch_block(EpochArgs a) {
+    U* const uu = static_cast<U*>(a.u);
     constexpr int NW = BS / 64;
     __shared__ float part[2][NW];
     const int tid = threadIdx.x, wave = tid >> 6;
@@ -350,9 +358,9 @@ __global__ __launch_bounds__(BS) void k_epoch_block(EpochArgs a) {
         float acc = 0.0f;
 #pragma unroll
         for (int r = 0; r < R; ++r)
-            if (ci[r] >= 0) acc = fmaf(cv[r], ld_u<FRESH>(a.u + ci[r]), acc);
+            if (ci[r] >= 0) acc = fmaf(cv[r], ld_u<FRESH>(uu + ci[r]), acc);
         for (int64_t k = s0 + tid + (int64_t)R * BS; k < s1; k += BS)
-            acc = fmaf(a.val[k], ld_u<FRESH>(a.u + a.idx[k]), acc);
+            acc = fmaf(a.val[k], ld_u<FRESH>(uu + a.idx[k]), acc);
         acc = group_sum<64>(acc);
         if ((tid & 63) == 0) part[buf][wave] = acc;
         __syncthreads();
@@ -365,9 +373,9 @@ __global__ __launch_bounds__(BS) void k_epoch_block(EpochArgs a) {
         if (coef != 0.0f) {
 #pragma unroll
             for (int r = 0; r < R; ++r)
-                if (ci[r] >= 0) atomic_add_u(a.u + ci[r], coef * cv[r]);
+                if (ci[r] >= 0) atomic_add_u(uu + ci[r], coef * cv[r]);
             for (int64_t k = s0 + tid + (int64_t)R * BS; k < s1; k += BS)
-                atomic_add_u(a.u + a.idx[k], coef * a.val[k]);
+                atomic_add_u(uu + a.idx[k], coef * a.val[k]);
         }
         if constexpr (ORDERED) {
             __threadfence();
@@ -383,14 +391,15 @@ __global__ __launch_bounds__(BS) void k_epoch_block(EpochArgs a) {
 // (ds_add_f32), two barriers per coordinate.  The shared vector is loaded at the start and
 // written back at the end of the epoch.
 // ----------------------------------------------------------------------------------------
-template <int FORM>
+template <int FORM, typename U>
 __global__ __launch_bounds__(1024) void k_epoch_ordered_lds(EpochArgs a, uint32_t L) {
     constexpr int BS = 1024, NW = BS / 64;
-    extern __shared__ float lds[];
-    float* su = lds;                    // L floats
-    float* part = lds + ((L + 63) & ~63u);  // 2 * NW floats
+    extern __shared__ __align__(16) unsigned char lds_bytes[];
+    U* const uu = static_cast<U*>(a.u);
+    U* su = reinterpret_cast<U*>(lds_bytes);                           // L entries
+    float* part = reinterpret_cast<float*>(su + ((L + 63) & ~63u));    // 2 * NW floats
     const int tid = threadIdx.x, wave = tid >> 6;
-    for (uint32_t i = tid; i < L; i += BS) su[i] = a.u[i];
+    for (uint32_t i = tid; i < L; i += BS) su[i] = uu[i];
     __syncthreads();
     int buf = 0;
     for (uint32_t j = 0; j < a.perm.n; ++j) {
@@ -400,7 +409,7 @@ __global__ __launch_bounds__(1024) void k_epoch_ordered_lds(EpochArgs a, uint32_
         const float sn = a.norms[m];
         const float ylab = a.y[m];
         float acc = 0.0f;
-        for (int64_t k = s0 + tid; k < s1; k += BS) acc = fmaf(a.val[k], su[a.idx[k]], acc);
+        for (int64_t k = s0 + tid; k < s1; k += BS) acc = fmaf(a.val[k], (float)su[a.idx[k]], acc);
         acc = group_sum<64>(acc);
         if ((tid & 63) == 0) part[buf * NW + wave] = acc;
         __syncthreads();
@@ -411,11 +420,11 @@ __global__ __launch_bounds__(1024) void k_epoch_ordered_lds(EpochArgs a, uint32_
         const float m_new = coord_step<FORM>(g, sn, m_old, ylab, a.k, &coef);
         if (tid == 0) a.model[m] = m_new;
         if (coef != 0.0f)
-            for (int64_t k = s0 + tid; k < s1; k += BS) atomicAdd(su + a.idx[k], coef * a.val[k]);
+            for (int64_t k = s0 + tid; k < s1; k += BS) atomicAdd(su + a.idx[k], (U)(coef * a.val[k]));
         __syncthreads();
         buf ^= 1;
     }
-    for (uint32_t i = tid; i < L; i += BS) a.u[i] = su[i];
+    for (uint32_t i = tid; i < L; i += BS) uu[i] = su[i];
 }
 
 // ----------------------------------------------------------------------------------------
@@ -522,9 +531,9 @@ __device__ __forceinline__ void block_reduce_store(double (&v)[NS], double* out)
     }
 }
 
-template <int FORM, int G>
+template <int FORM, int G, typename U>
 __global__ __launch_bounds__(256) void k_obj_coords(const int64_t* __restrict__ ptr, const int32_t* __restrict__ idx,
-                                                    const float* __restrict__ val, const float* __restrict__ u,
+                                                    const float* __restrict__ val, const U* __restrict__ u,
                                                     const float* __restrict__ model, const float* __restrict__ y,
                                                     const float* __restrict__ yv, uint32_t C, double lam,
                                                     double* __restrict__ partials) {
@@ -562,8 +571,8 @@ __global__ __launch_bounds__(256) void k_obj_coords(const int64_t* __restrict__ 
     block_reduce_store<3>(t, partials + (size_t)blockIdx.x * 3);
 }
 
-template <int FORM>
-__global__ __launch_bounds__(256) void k_obj_vector(const float* __restrict__ u, const float* __restrict__ y, int64_t L,
+template <int FORM, typename U>
+__global__ __launch_bounds__(256) void k_obj_vector(const U* __restrict__ u, const float* __restrict__ y, int64_t L,
                                                     double* __restrict__ partials) {
     double t[2] = {0.0, 0.0};
     for (int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x; i < L; i += (int64_t)gridDim.x * 256) {
@@ -682,69 +691,63 @@ __global__ __launch_bounds__(256) void k_sum_partials(const double* __restrict__
 // ----------------------------------------------------------------------------------------
 // Host-side launchers.
 // ----------------------------------------------------------------------------------------
-template <int FORM, int G, bool FRESH>
+template <int FORM, int G, bool FRESH, typename U>
 static hipError_t launch_group(const EpochArgs& a, int blocks, bool tail, hipStream_t s) {
     constexpr int R = slice_depth(G);
     if (tail)
-        hipLaunchKernelGGL((k_epoch_group<FORM, G, R, FRESH, true>), dim3(blocks), dim3(256), 0, s, a);
+        hipLaunchKernelGGL((k_epoch_group<FORM, G, R, FRESH, true, U>), dim3(blocks), dim3(256), 0, s, a);
     else
-        hipLaunchKernelGGL((k_epoch_group<FORM, G, R, FRESH, false>), dim3(blocks), dim3(256), 0, s, a);
+        hipLaunchKernelGGL((k_epoch_group<FORM, G, R, FRESH, false, U>), dim3(blocks), dim3(256), 0, s, a);
     return hipGetLastError();
 }
 
-template <int FORM, int G, bool FRESH>
+template <int FORM, int G, bool FRESH, typename U>
 static hipError_t launch_mixed(const EpochArgs& a, int blocks, uint32_t long_len, hipStream_t s) {
     constexpr int R = slice_depth(G);
     const uint32_t ng = (a.n_groups + blocks - 1) / blocks;  // <= 256 / G by construction of the plan
-    hipLaunchKernelGGL((k_epoch_mixed<FORM, G, R, FRESH>), dim3(blocks), dim3(256), 0, s, a, long_len, ng);
+    hipLaunchKernelGGL((k_epoch_mixed<FORM, G, R, FRESH, U>), dim3(blocks), dim3(256), 0, s, a, long_len, ng);
     return hipGetLastError();
 }
 
-template <int FORM, bool FRESH>
-static hipError_t launch_mixed_g(const EpochArgs& a, int G, int blocks, uint32_t long_len, hipStream_t s) {
-    switch (G) {
-        case 4: return launch_mixed<FORM, 4, FRESH>(a, blocks, long_len, s);
-        case 8: return launch_mixed<FORM, 8, FRESH>(a, blocks, long_len, s);
-        case 16: return launch_mixed<FORM, 16, FRESH>(a, blocks, long_len, s);
-        case 32: return launch_mixed<FORM, 32, FRESH>(a, blocks, long_len, s);
-        case 64: return launch_mixed<FORM, 64, FRESH>(a, blocks, long_len, s);
+template <int FORM, bool FRESH, typename U>
+static hipError_t launch_by_width(const EpochArgs& a, const LaunchPlan& lp, hipStream_t s) {
+    const bool mixed = lp.kind == PLAN_MIXED;
+    switch (lp.group) {
+#define SCD_CASE(GW)                                                                           \
+    case GW:                                                                                   \
+        return mixed ? launch_mixed<FORM, GW, FRESH, U>(a, lp.blocks, lp.long_len, s)          \
+                     : launch_group<FORM, GW, FRESH, U>(a, lp.blocks, lp.tail, s);
+        SCD_CASE(4)
+        SCD_CASE(8)
+        SCD_CASE(16)
+        SCD_CASE(32)
+        SCD_CASE(64)
+#undef SCD_CASE
         default: return hipErrorInvalidValue;
     }
 }
 
-template <int FORM, bool FRESH>
-static hipError_t launch_group_g(const EpochArgs& a, int G, int blocks, bool tail, hipStream_t s) {
-    switch (G) {
-        case 4: return launch_group<FORM, 4, FRESH>(a, blocks, tail, s);
-        case 8: return launch_group<FORM, 8, FRESH>(a, blocks, tail, s);
-        case 16: return launch_group<FORM, 16, FRESH>(a, blocks, tail, s);
-        case 32: return launch_group<FORM, 32, FRESH>(a, blocks, tail, s);
-        case 64: return launch_group<FORM, 64, FRESH>(a, blocks, tail, s);
-        default: return hipErrorInvalidValue;
+template <int FORM, typename U>
+static hipError_t launch_epoch_typed(const EpochArgs& a, const LaunchPlan& lp, hipStream_t s) {
+    if (lp.kind == PLAN_ORDERED_LDS) {
+        hipLaunchKernelGGL((k_epoch_ordered_lds<FORM, U>), dim3(1), dim3(1024), lp.lds_bytes, s, a, lp.L);
+        return hipGetLastError();
     }
+    if (lp.kind == PLAN_BLOCK) {
+        if (lp.ordered)
+            hipLaunchKernelGGL((k_epoch_block<FORM, 256, 16, true, true, U>), dim3(lp.blocks), dim3(256), 0, s, a);
+        else if (lp.fresh)
+            hipLaunchKernelGGL((k_epoch_block<FORM, 256, 16, true, false, U>), dim3(lp.blocks), dim3(256), 0, s, a);
+        else
+            hipLaunchKernelGGL((k_epoch_block<FORM, 256, 16, false, false, U>), dim3(lp.blocks), dim3(256), 0, s, a);
+        return hipGetLastError();
+    }
+    return lp.fresh ? launch_by_width<FORM, true, U>(a, lp, s) : launch_by_width<FORM, false, U>(a, lp, s);
 }
 
 template <int FORM>
 static hipError_t launch_epoch_form(const EpochArgs& a, const LaunchPlan& lp, hipStream_t s) {
-    if (lp.kind == PLAN_ORDERED_LDS) {
-        hipLaunchKernelGGL((k_epoch_ordered_lds<FORM>), dim3(1), dim3(1024), lp.lds_bytes, s, a, lp.L);
-        return hipGetLastError();
-    }
-    if (lp.kind == PLAN_BLOCK) {
-        if (lp.ordered) {
-            hipLaunchKernelGGL((k_epoch_block<FORM, 256, 16, true, true>), dim3(lp.blocks), dim3(256), 0, s, a);
-        } else if (lp.fresh) {
-            hipLaunchKernelGGL((k_epoch_block<FORM, 256, 16, true, false>), dim3(lp.blocks), dim3(256), 0, s, a);
-        } else {
-            hipLaunchKernelGGL((k_epoch_block<FORM, 256, 16, false, false>), dim3(lp.blocks), dim3(256), 0, s, a);
-        }
-        return hipGetLastError();
-    }
-    if (lp.kind == PLAN_MIXED)
-        return lp.fresh ? launch_mixed_g<FORM, true>(a, lp.group, lp.blocks, lp.long_len, s)
-                        : launch_mixed_g<FORM, false>(a, lp.group, lp.blocks, lp.long_len, s);
-    return lp.fresh ? launch_group_g<FORM, true>(a, lp.group, lp.blocks, lp.tail, s)
-                    : launch_group_g<FORM, false>(a, lp.group, lp.blocks, lp.tail, s);
+    return lp.wide ? launch_epoch_typed<FORM, double>(a, lp, s) : launch_epoch_typed<FORM, float>(a, lp, s);
 }
 
 hipError_t launch_epoch(int form, const EpochArgs& a, const LaunchPlan& lp, hipStream_t s) {
@@ -756,17 +759,18 @@ hipError_t launch_epoch(int form, const EpochArgs& a, const LaunchPlan& lp, hipS
     }
 }
 
-hipError_t ordered_lds_prepare(int form, size_t lds_bytes) {
+template <int FORM>
+static hipError_t prepare_form(bool wide, size_t lds_bytes) {
+    const void* f = wide ? reinterpret_cast<const void*>(&k_epoch_ordered_lds<FORM, double>)
+                         : reinterpret_cast<const void*>(&k_epoch_ordered_lds<FORM, float>);
+    return hipFuncSetAttribute(f, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds_bytes);
+}
+
+hipError_t ordered_lds_prepare(int form, bool wide, size_t lds_bytes) {
     switch (form) {
-        case FORM_RIDGE_PRIMAL:
-            return hipFuncSetAttribute(reinterpret_cast<const void*>(&k_epoch_ordered_lds<FORM_RIDGE_PRIMAL>),
-                                       hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds_bytes);
-        case FORM_SVM_DUAL:
-            return hipFuncSetAttribute(reinterpret_cast<const void*>(&k_epoch_ordered_lds<FORM_SVM_DUAL>),
-                                       hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds_bytes);
-        case FORM_RIDGE_DUAL:
-            return hipFuncSetAttribute(reinterpret_cast<const void*>(&k_epoch_ordered_lds<FORM_RIDGE_DUAL>),
-                                       hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds_bytes);
+        case FORM_RIDGE_PRIMAL: return prepare_form<FORM_RIDGE_PRIMAL>(wide, lds_bytes);
+        case FORM_SVM_DUAL: return prepare_form<FORM_SVM_DUAL>(wide, lds_bytes);
+        case FORM_RIDGE_DUAL: return prepare_form<FORM_RIDGE_DUAL>(wide, lds_bytes);
         default: return hipErrorInvalidValue;
     }
 }
@@ -816,15 +820,37 @@ hipError_t launch_validate(const int64_t* ptr, uint32_t S, const int32_t* idx, c
     return hipGetLastError();
 }
 
-template <int FORM>
+template <int FORM, typename U>
 static void obj_coords_g(int G, int blocks, const ObjArgs& o, double* partials, hipStream_t s) {
+    const U* u = static_cast<const U*>(o.u);
     switch (G) {
-        case 4: hipLaunchKernelGGL((k_obj_coords<FORM, 4>), dim3(blocks), dim3(256), 0, s, o.ptr, o.idx, o.val, o.u, o.model, o.y, o.yv, o.C, o.lam, partials); break;
-        case 8: hipLaunchKernelGGL((k_obj_coords<FORM, 8>), dim3(blocks), dim3(256), 0, s, o.ptr, o.idx, o.val, o.u, o.model, o.y, o.yv, o.C, o.lam, partials); break;
-        case 16: hipLaunchKernelGGL((k_obj_coords<FORM, 16>), dim3(blocks), dim3(256), 0, s, o.ptr, o.idx, o.val, o.u, o.model, o.y, o.yv, o.C, o.lam, partials); break;
-        case 32: hipLaunchKernelGGL((k_obj_coords<FORM, 32>), dim3(blocks), dim3(256), 0, s, o.ptr, o.idx, o.val, o.u, o.model, o.y, o.yv, o.C, o.lam, partials); break;
-        default: hipLaunchKernelGGL((k_obj_coords<FORM, 64>), dim3(blocks), dim3(256), 0, s, o.ptr, o.idx, o.val, o.u, o.model, o.y, o.yv, o.C, o.lam, partials); break;
+#define SCD_OBJ(GW)                                                                                              \
+    case GW:                                                                                                     \
+        hipLaunchKernelGGL((k_obj_coords<FORM, GW, U>), dim3(blocks), dim3(256), 0, s, o.ptr, o.idx, o.val, u,  \
+                           o.model, o.y, o.yv, o.C, o.lam, partials);                                            \
+        break;
+        SCD_OBJ(4)
+        SCD_OBJ(8)
+        SCD_OBJ(16)
+        SCD_OBJ(32)
+        default: SCD_OBJ(64)
+#undef SCD_OBJ
     }
+}
+
+template <int FORM, typename U>
+static void objective_typed(const ObjArgs& o, int G, int blocks, double* pc, double* pv, hipStream_t s) {
+    obj_coords_g<FORM, U>(G, blocks, o, pc, s);
+    hipLaunchKernelGGL((k_obj_vector<FORM, U>), dim3(blocks), dim3(256), 0, s, static_cast<const U*>(o.u), o.yv, o.L,
+                       pv);
+}
+
+template <int FORM>
+static void objective_form(const ObjArgs& o, int G, int blocks, double* pc, double* pv, hipStream_t s) {
+    if (o.wide)
+        objective_typed<FORM, double>(o, G, blocks, pc, pv, s);
+    else
+        objective_typed<FORM, float>(o, G, blocks, pc, pv, s);
 }
 
 // sums[0..2] = coordinate sums, sums[3..4] = vector sums.
@@ -833,18 +859,9 @@ hipError_t launch_objective(int form, const ObjArgs& o, int G, int blocks, doubl
     double* pc = partials;                       // blocks x 3
     double* pv = partials + (size_t)blocks * 3;  // blocks x 2
     switch (form) {
-        case FORM_RIDGE_PRIMAL:
-            obj_coords_g<FORM_RIDGE_PRIMAL>(G, blocks, o, pc, s);
-            hipLaunchKernelGGL(k_obj_vector<FORM_RIDGE_PRIMAL>, dim3(blocks), dim3(256), 0, s, o.u, o.yv, o.L, pv);
-            break;
-        case FORM_SVM_DUAL:
-            obj_coords_g<FORM_SVM_DUAL>(G, blocks, o, pc, s);
-            hipLaunchKernelGGL(k_obj_vector<FORM_SVM_DUAL>, dim3(blocks), dim3(256), 0, s, o.u, o.yv, o.L, pv);
-            break;
-        case FORM_RIDGE_DUAL:
-            obj_coords_g<FORM_RIDGE_DUAL>(G, blocks, o, pc, s);
-            hipLaunchKernelGGL(k_obj_vector<FORM_RIDGE_DUAL>, dim3(blocks), dim3(256), 0, s, o.u, o.yv, o.L, pv);
-            break;
+        case FORM_RIDGE_PRIMAL: objective_form<FORM_RIDGE_PRIMAL>(o, G, blocks, pc, pv, s); break;
+        case FORM_SVM_DUAL: objective_form<FORM_SVM_DUAL>(o, G, blocks, pc, pv, s); break;
+        case FORM_RIDGE_DUAL: objective_form<FORM_RIDGE_DUAL>(o, G, blocks, pc, pv, s); break;
         default: return hipErrorInvalidValue;
     }
     hipLaunchKernelGGL(k_sum_partials, dim3(1), dim3(256), 0, s, pc, blocks, 3, sums);
@@ -883,6 +900,51 @@ hipError_t launch_probe(const int64_t* ptr, const int32_t* idx, const float* val
 hipError_t launch_kappa_max(const float* K, const float* norms, uint32_t C, float mu, int probes, int blocks,
                             unsigned* out, hipStream_t s) {
     hipLaunchKernelGGL(k_kappa_max, dim3(blocks), dim3(256), 0, s, K, norms, C, mu, 1.0f / (float)probes, out);
+    return hipGetLastError();
+}
+
+// ----------------------------------------------------------------------------------------
+// Storage-width conversions of the shared vector and the per-entry update count.
+// ----------------------------------------------------------------------------------------
+template <typename A, typename B>
+__global__ __launch_bounds__(256) void k_convert(const A* __restrict__ in, int64_t n, B* __restrict__ out) {
+    for (int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x; i < n; i += (int64_t)gridDim.x * 256) out[i] = (B)in[i];
+}
+
+// hits[i] = number of stored entries with index i (one atomic per entry); max into out[0].
+__global__ __launch_bounds__(256) void k_count_hits(const int32_t* __restrict__ idx, int64_t nnz,
+                                                    unsigned* __restrict__ hits) {
+    for (int64_t k = (int64_t)blockIdx.x * 256 + threadIdx.x; k < nnz; k += (int64_t)gridDim.x * 256)
+        atomicAdd(hits + idx[k], 1u);
+}
+
+__global__ __launch_bounds__(256) void k_max_u32(const unsigned* __restrict__ v, int64_t n, unsigned* __restrict__ out) {
+    unsigned best = 0;
+    for (int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x; i < n; i += (int64_t)gridDim.x * 256) best = max(best, v[i]);
+    for (int o = 32; o > 0; o >>= 1) best = max(best, (unsigned)__shfl_xor((int)best, o, 64));
+    if ((threadIdx.x & 63) == 0 && best) atomicMax(out, best);
+}
+
+static unsigned grid_for(int64_t n) {
+    int64_t b = (n + 255) / 256;
+    if (b > 8192) b = 8192;
+    if (b < 1) b = 1;
+    return (unsigned)b;
+}
+
+hipError_t launch_convert_f32_to_f64(const float* in, int64_t n, double* out, hipStream_t s) {
+    hipLaunchKernelGGL((k_convert<float, double>), dim3(grid_for(n)), dim3(256), 0, s, in, n, out);
+    return hipGetLastError();
+}
+
+hipError_t launch_convert_f64_to_f32(const double* in, int64_t n, float* out, hipStream_t s) {
+    hipLaunchKernelGGL((k_convert<double, float>), dim3(grid_for(n)), dim3(256), 0, s, in, n, out);
+    return hipGetLastError();
+}
+
+hipError_t launch_max_hits(const int32_t* idx, int64_t nnz, int64_t L, unsigned* hits, unsigned* out, hipStream_t s) {
+    if (nnz > 0) hipLaunchKernelGGL(k_count_hits, dim3(grid_for(nnz)), dim3(256), 0, s, idx, nnz, hits);
+    hipLaunchKernelGGL(k_max_u32, dim3(grid_for(L)), dim3(256), 0, s, hits, L, out);
     return hipGetLastError();
 }
 

@@ -435,3 +435,56 @@ def test_coupling_estimate_and_default_window(key, over):
     budget = 0.15 if p.form == "svm_dual" else 0.1
     assert 1 <= w <= min(p.C, 1 + int(budget / est))
     s.close()
+
+
+# ---------------------------------------------------------------------------------- fp64 shared vector
+
+def test_hot_entries_select_fp64_shared_vector():
+    # A feature present in most of 40,000 rows receives > 28,000 atomic adds per epoch.
+    p = synth.make("text_svm", n_rows=40_000, n_cols=50_000, row_nnz=20)
+    s = scd.solver_for(p)
+    info = s.info()
+    assert info["max_hits"] == int(np.bincount(p.idx).max())
+    assert info["max_hits"] > 28_000 and info["shared_fp64"] == 1
+    s.epochs(0, 2)
+    gm, gs, _ = s.get_state()
+    assert rel_inf(f64(gs), fresh(p, f64(gm))) <= 1e-4
+    q = problem("sparse_ridge_small")
+    t = scd.solver_for(q)
+    assert t.info()["shared_fp64"] == 0 and t.info()["max_hits"] == int(np.bincount(q.idx).max())
+    s.close()
+    t.close()
+
+
+@pytest.mark.parametrize("group", [8, 32, 256])
+def test_fp64_shared_vector_keeps_parity(group):
+    p = problem("click_svm_twin")
+    s = scd.solver_for(p)
+    s.set_option("shared_fp64", 1)
+    s.set_option("group", group)
+    assert s.get_option("shared_fp64") == 1 and s.info()["shared_fp64"] == 1
+    mo, so, curve = _oracle_curve(p, 0, 3)
+    for e in range(3):
+        s.epochs(0, 1)
+        gm, gs, _ = s.get_state()
+        assert rel_inf(f64(gs), fresh(p, f64(gm))) <= 1e-4
+        if curve[e][2] > 1e-6:
+            assert s.duality_gap() <= 2.0 * curve[e][2]
+    # Switching back keeps the state (rounded to fp32).
+    s.set_option("shared_fp64", 0)
+    gm2, gs2, _ = s.get_state()
+    assert torch.equal(gm, gm2) and torch.equal(gs, gs2)
+    s.close()
+
+
+def test_fp64_ordered_lds_tracks_oracle():
+    p = problem("dense_ridge")
+    _, _, curve = _oracle_curve(p, 0, 6)
+    s = scd.solver_for(p)
+    s.set_option("shared_fp64", 1)
+    s.set_option("window", 1)
+    for e in range(6):
+        s.epochs(0, 1)
+        P, _ = s.objective()
+        assert abs(P - curve[e][0]) <= 1e-4 * abs(curve[e][0])
+    s.close()
