@@ -163,7 +163,7 @@ int scd_set_state(scd_handle_t h, const float *model_dev, const float *shared_de
 /* Tuning and test options (host-side, take effect at the next scd_epochs):
  *   "window"      coordinates in flight at most; 1 = ordered (Alg. 1's sequence exactly);
  *                 0 (default) = chosen at create from the measured coupling of the coordinates:
- *                 W = 1 + b / coupling (b = 0.15 for the SVM dual, 0.1 for the ridge forms), at
+ *                 W = 1 + b / coupling (b = 0.15 for the SVM dual, 0.015 for the ridge forms), at
  *                 most C/16 when the coupling exceeds 1e-6, at most what the GPU holds.  Concurrent coordinates read each other's stale shared-vector
  *                 entries; strongly coupled problems need a small window to keep the per-epoch
  *                 convergence of the sequential algorithm.

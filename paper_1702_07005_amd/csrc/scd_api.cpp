@@ -65,7 +65,7 @@ constexpr int kObjBlocksMax = 2048;
 // Window rule: (window - 1) x (worst coordinate's mean squared coupling) <= budget.  The SVM's
 // box projection tolerates stale reads far better than the unconstrained ridge steps.
 constexpr double kCouplingBudgetSvm = 0.15;
-constexpr double kCouplingBudgetRidge = 0.1;
+constexpr double kCouplingBudgetRidge = 0.015;
 constexpr int kProbes = 8;                // Hutchinson probes of the coupling estimate
 // An entry of the shared vector receiving K atomic adds per epoch drifts by about
 // sqrt(K) * 2^-24 of its magnitude in fp32; above this many it is kept in fp64 (drift < 1e-5).

@@ -432,7 +432,7 @@ def test_coupling_estimate_and_default_window(key, over):
     # The maximum of noisy per-coordinate estimates is biased upwards (conservative).
     assert 0.5 * exact <= est <= 4.0 * exact, (est, exact)
     w = info["auto_window"]
-    budget = 0.15 if p.form == "svm_dual" else 0.1
+    budget = 0.15 if p.form == "svm_dual" else 0.015
     assert 1 <= w <= min(p.C, 1 + int(budget / est))
     s.close()
 
