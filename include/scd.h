@@ -145,6 +145,15 @@ int scd_objective(scd_handle_t h, void *stream, double *primal, double *dual);
  * ridge dual; P - D >= 0 for the SVM).  Synchronises. */
 int scd_duality_gap(scd_handle_t h, void *stream, double *gap);
 
+/* Asynchronous duality gap, for training loops that check convergence without stalling the GPU:
+ * scd_duality_gap_async enqueues the evaluation of the current state (as scd_duality_gap) on
+ * `stream` into one of 4 slots (0..3) and returns at once; scd_duality_gap_wait blocks until that
+ * evaluation is done and returns the gap (and, if not NULL, P and D).  A slot must be waited on
+ * before it is reused (SCD_ERR_INVALID otherwise).  Evaluations share the handle's reduction
+ * scratch, so all of them must be enqueued on the same stream as the epochs. */
+int scd_duality_gap_async(scd_handle_t h, void *stream, int32_t slot);
+int scd_duality_gap_wait(scd_handle_t h, int32_t slot, double *gap, double *primal, double *dual);
+
 /* Copy the state out (device buffers, may be NULL to skip), exactly as the solver holds it:
  *   model_dev:  float32[n_coords]   (beta, or alpha)
  *   shared_dev: float32[shared_len] (w = A beta, or w(alpha), or wbar = A^T alpha)

@@ -62,6 +62,7 @@ PermKeys make_perm(uint64_t seed, uint64_t epoch, uint32_t n) {
 constexpr int kBlockThreads = 256;
 constexpr int kBlocksPerCU = 8;
 constexpr int kObjBlocksMax = 2048;
+constexpr int kGapSlots = 4;
 // Window rule: (window - 1) x (worst coordinate's mean squared coupling) <= budget.  The SVM's
 // box projection tolerates stale reads far better than the unconstrained ridge steps.
 constexpr double kCouplingBudgetSvm = 0.15;
@@ -87,11 +88,17 @@ struct scd_solver {
     uint32_t max_hits = 0;  // most stored entries sharing one shared-vector index
     float* norms = nullptr;
     float* cy = nullptr;  // ridge primal: <y, a_c> per coordinate
+    double* cyd = nullptr;  // the same in fp64 (objective evaluation)
+    unsigned* ticket = nullptr;  // last-workgroup counter of the objective kernel (zero between calls)
     void* dummy = nullptr;  // one zero entry standing in for idx/val of an all-empty matrix
     int* flags = nullptr;
     double* partials = nullptr;
     double* sums = nullptr;
     double* host_sums = nullptr;  // pinned
+    // Asynchronous duality-gap slots: pinned sums and a completion event per slot.
+    double* slot_sums = nullptr;  // pinned, kGapSlots x 5
+    hipEvent_t slot_event[4] = {nullptr, nullptr, nullptr, nullptr};
+    int slot_pending[4] = {0, 0, 0, 0};
     int64_t epoch = 0;
     int device = 0;
     int cus = 0;
@@ -202,16 +209,21 @@ void release(scd_solver* h) {
     (void)hipFree(h->u);
     (void)hipFree(h->norms);
     (void)hipFree(h->cy);
+    (void)hipFree(h->cyd);
+    (void)hipFree(h->ticket);
     (void)hipFree(h->dummy);
     (void)hipFree(h->flags);
     (void)hipFree(h->partials);
     (void)hipFree(h->sums);
     if (h->host_sums) (void)hipHostFree(h->host_sums);
+    if (h->slot_sums) (void)hipHostFree(h->slot_sums);
+    for (hipEvent_t& e : h->slot_event)
+        if (e) (void)hipEventDestroy(e);
     delete h;
 }
 
-// Compute the five reduction sums of the current state into h->host_sums (synchronises).
-int reduce_state(scd_solver* h, hipStream_t s) {
+// Enqueue the five reduction sums of the current state and their copy into host[0..4].
+int enqueue_sums(scd_solver* h, hipStream_t s, double* host) {
     ObjArgs o{};
     o.ptr = h->ptr;
     o.idx = h->idx;
@@ -221,19 +233,25 @@ int reduce_state(scd_solver* h, hipStream_t s) {
     o.model = h->model;
     o.y = h->form == FORM_RIDGE_PRIMAL ? nullptr : h->y;
     o.yv = h->form == FORM_RIDGE_PRIMAL ? h->y : nullptr;
+    o.cyd = h->cyd;
     o.C = (uint32_t)h->C;
     o.L = h->L;
     o.lam = h->lambda;
     const int G = obj_group(h);
     const int blocks = obj_blocks(h, G);
-    HIP_TRY(launch_objective(h->form, o, G, blocks, h->partials, h->sums, s));
-    HIP_TRY(hipMemcpyAsync(h->host_sums, h->sums, 5 * sizeof(double), hipMemcpyDeviceToHost, s));
+    HIP_TRY(launch_objective(h->form, o, G, blocks, h->partials, h->ticket, h->sums, s));
+    HIP_TRY(hipMemcpyAsync(host, h->sums, 5 * sizeof(double), hipMemcpyDeviceToHost, s));
+    return SCD_OK;
+}
+
+// The same, waiting for the result in h->host_sums.
+int reduce_state(scd_solver* h, hipStream_t s) {
+    if (int r = enqueue_sums(h, s, h->host_sums)) return r;
     HIP_TRY(hipStreamSynchronize(s));
     return SCD_OK;
 }
 
-void objectives_from_sums(const scd_solver* h, double* P, double* D) {
-    const double* t = h->host_sums;
+void objectives_from_sums(const scd_solver* h, const double* t, double* P, double* D) {
     const double N = (double)h->n_rows, lam = h->lambda;
     if (h->form == FORM_RIDGE_PRIMAL) {
         // t0 = sum_m <a_m, r>^2, t1 = |beta|^2, t3 = |r|^2, t4 = <r, y>,  r = y - w, w = A beta.
@@ -315,7 +333,12 @@ int scd_create(const scd_matrix_t* A, const float* y, double lambda, int32_t for
     hip(hipMalloc(&h->model, sizeof(float) * (size_t)h->C), "hipMalloc(model)");
     hip(hipMalloc(&h->u, sizeof(float) * (size_t)h->L), "hipMalloc(shared)");
     hip(hipMalloc(&h->norms, sizeof(float) * (size_t)h->C), "hipMalloc(norms)");
-    if (formulation == SCD_RIDGE_PRIMAL) hip(hipMalloc(&h->cy, sizeof(float) * (size_t)h->C), "hipMalloc(cy)");
+    if (formulation == SCD_RIDGE_PRIMAL) {
+        hip(hipMalloc(&h->cy, sizeof(float) * (size_t)h->C), "hipMalloc(cy)");
+        hip(hipMalloc(&h->cyd, sizeof(double) * (size_t)h->C), "hipMalloc(cyd)");
+    }
+    hip(hipMalloc(&h->ticket, sizeof(unsigned)), "hipMalloc(ticket)");
+    hip(hipMemsetAsync(h->ticket, 0, sizeof(unsigned), s), "zero ticket");
     hip(hipMalloc(&h->flags, 2 * sizeof(int64_t)), "hipMalloc(flags)");
     if (h->nnz == 0) {
         // The epoch kernels read element 0 of idx/val unconditionally (weight 0 when unused).
@@ -327,6 +350,9 @@ int scd_create(const scd_matrix_t* A, const float* y, double lambda, int32_t for
     hip(hipMalloc(&h->partials, sizeof(double) * (size_t)kObjBlocksMax * 5), "hipMalloc(partials)");
     hip(hipMalloc(&h->sums, sizeof(double) * 8), "hipMalloc(sums)");
     hip(hipHostMalloc(&h->host_sums, sizeof(double) * 8, hipHostMallocDefault), "hipHostMalloc");
+    hip(hipHostMalloc(&h->slot_sums, sizeof(double) * 5 * kGapSlots, hipHostMallocDefault), "hipHostMalloc(slots)");
+    for (int i = 0; i < kGapSlots; ++i)
+        hip(hipEventCreateWithFlags(&h->slot_event[i], hipEventDisableTiming), "hipEventCreate");
 
     // Validation pass over ptr, idx, val and y.
     int64_t fl[2] = {0, 0};  // validation bits, longest segment
@@ -362,7 +388,7 @@ int scd_create(const scd_matrix_t* A, const float* y, double lambda, int32_t for
     if (rc == SCD_OK) {
         const int G = obj_group(h);
         hip(launch_norms(h->ptr, h->idx, h->val, formulation == SCD_RIDGE_PRIMAL ? h->y : nullptr, (uint32_t)h->C,
-                         G, obj_blocks(h, G), h->norms, h->cy, s),
+                         G, obj_blocks(h, G), h->norms, h->cy, h->cyd, s),
             "norms");
         // Coupling of the coordinates (sets the default window), using h->u as the probe vector.
         const float mu = formulation == SCD_SVM_DUAL ? 0.0f : (float)(lambda * (double)h->n_rows);
@@ -467,7 +493,7 @@ int scd_objective(scd_handle_t h, void* stream, double* primal, double* dual) {
     if (int r = set_device(h)) return r;
     if (int r = reduce_state(h, (hipStream_t)stream)) return r;
     double P, D;
-    objectives_from_sums(h, &P, &D);
+    objectives_from_sums(h, h->host_sums, &P, &D);
     if (!std::isfinite(P) || !std::isfinite(D)) return fail(SCD_ERR_NUMERIC, "non-finite objective (P=%g, D=%g)", P, D);
     if (primal) *primal = P;
     if (dual) *dual = D;
@@ -479,6 +505,33 @@ int scd_duality_gap(scd_handle_t h, void* stream, double* gap) {
     double P = 0, D = 0;
     if (int r = scd_objective(h, stream, &P, &D)) return r;
     *gap = h->form == FORM_SVM_DUAL ? P - D : std::fabs(P - D);
+    return SCD_OK;
+}
+
+int scd_duality_gap_async(scd_handle_t h, void* stream, int32_t slot) {
+    if (int r = check_handle(h)) return r;
+    if (slot < 0 || slot >= kGapSlots) return fail(SCD_ERR_INVALID, "slot must be in [0, %d)", kGapSlots);
+    if (h->slot_pending[slot]) return fail(SCD_ERR_INVALID, "slot %d already holds an unread evaluation", slot);
+    if (int r = set_device(h)) return r;
+    hipStream_t s = (hipStream_t)stream;
+    if (int r = enqueue_sums(h, s, h->slot_sums + 5 * slot)) return r;
+    HIP_TRY(hipEventRecord(h->slot_event[slot], s));
+    h->slot_pending[slot] = 1;
+    return SCD_OK;
+}
+
+int scd_duality_gap_wait(scd_handle_t h, int32_t slot, double* gap, double* primal, double* dual) {
+    if (int r = check_handle(h)) return r;
+    if (slot < 0 || slot >= kGapSlots) return fail(SCD_ERR_INVALID, "slot must be in [0, %d)", kGapSlots);
+    if (!h->slot_pending[slot]) return fail(SCD_ERR_INVALID, "slot %d holds no evaluation", slot);
+    h->slot_pending[slot] = 0;
+    HIP_TRY(hipEventSynchronize(h->slot_event[slot]));
+    double P, D;
+    objectives_from_sums(h, h->slot_sums + 5 * slot, &P, &D);
+    if (!std::isfinite(P) || !std::isfinite(D)) return fail(SCD_ERR_NUMERIC, "non-finite objective (P=%g, D=%g)", P, D);
+    if (gap) *gap = h->form == FORM_SVM_DUAL ? P - D : std::fabs(P - D);
+    if (primal) *primal = P;
+    if (dual) *dual = D;
     return SCD_OK;
 }
 

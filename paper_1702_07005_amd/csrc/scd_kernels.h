@@ -67,6 +67,7 @@ struct ObjArgs {
     const float* model;
     const float* y;      // per-coordinate labels (duals)
     const float* yv;     // per-shared-entry labels (ridge primal: y over rows)
+    const double* cyd;   // ridge primal: <y, a_c> in fp64
     uint32_t C;
     int64_t L;
     double lam;
@@ -81,7 +82,7 @@ hipError_t launch_perm_fill(const PermKeys& p, int32_t* out, hipStream_t s);
 hipError_t launch_gather_dots(const int64_t* ptr, const int32_t* idx, const float* val, const float* u, uint32_t C,
                               int G, int blocks, float* out, hipStream_t s);
 hipError_t launch_norms(const int64_t* ptr, const int32_t* idx, const float* val, const float* y, uint32_t C, int G,
-                        int blocks, float* out, float* cy, hipStream_t s);
+                        int blocks, float* out, float* cy, double* cyd, hipStream_t s);
 hipError_t launch_validate(const int64_t* ptr, uint32_t S, const int32_t* idx, const float* val, int64_t nnz,
                            int64_t bound, const float* y, int64_t ny, int pm1, int* flags, hipStream_t s);
 hipError_t launch_probe(const int64_t* ptr, const int32_t* idx, const float* val, const float* norms,
@@ -89,7 +90,7 @@ hipError_t launch_probe(const int64_t* ptr, const int32_t* idx, const float* val
                         float* T, float* K, double* partials, double* out, hipStream_t s);
 hipError_t launch_kappa_max(const float* K, const float* norms, uint32_t C, float mu, int probes, int blocks,
                             unsigned* out, hipStream_t s);
-hipError_t launch_objective(int form, const ObjArgs& o, int G, int blocks, double* partials, double* sums,
-                            hipStream_t s);
+hipError_t launch_objective(int form, const ObjArgs& o, int G, int blocks, double* partials, unsigned* counter,
+                            double* sums, hipStream_t s);
 
 }  // namespace scd

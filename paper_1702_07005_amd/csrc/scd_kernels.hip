@@ -453,7 +453,8 @@ __global__ __launch_bounds__(256) void k_gather_dots(const int64_t* __restrict__
 template <int G>
 __global__ __launch_bounds__(256) void k_norms(const int64_t* __restrict__ ptr, const int32_t* __restrict__ idx,
                                                const float* __restrict__ val, const float* __restrict__ y,
-                                               uint32_t C, float* __restrict__ out, float* __restrict__ cy) {
+                                               uint32_t C, float* __restrict__ out, float* __restrict__ cy,
+                                               double* __restrict__ cyd) {
     const int lane = threadIdx.x & (G - 1);
     const uint32_t ngroups = gridDim.x * (256u / G);
     for (uint32_t c = (blockIdx.x * 256u + threadIdx.x) / G; c < C; c += ngroups) {
@@ -466,7 +467,10 @@ __global__ __launch_bounds__(256) void k_norms(const int64_t* __restrict__ ptr, 
         if (y) dy = group_sum_f64<G>(dy);
         if (lane == 0) {
             out[c] = (float)acc;
-            if (y) cy[c] = (float)dy;
+            if (y) {
+                cy[c] = (float)dy;
+                cyd[c] = dy;
+            }
         }
     }
 }
@@ -506,10 +510,11 @@ __global__ void k_validate_labels(const float* __restrict__ y, int64_t n, int pm
 }
 
 // ----------------------------------------------------------------------------------------
-// Objective / duality-gap reductions (fp64).  Coordinate pass: per coordinate the fp64 dot
-// d_c and up to three sums; vector pass: two sums over the shared vector.  Every workgroup
-// writes its partial sums; one final workgroup adds the partials in a fixed order.
-//   ridge primal (u = w, r = y - w in fp64, d = <a_c, r>):
+// Objective / duality-gap reductions (fp64), one launch.  Every workgroup sums, over the
+// coordinates it owns, the fp64 dot d_c and up to three terms, and over its slice of the shared
+// vector two more; it stores its five partial sums, and the last workgroup to finish (ticket
+// counter) adds all partials in workgroup order and resets the counter.
+//   ridge primal (u = w, r = y - w, d = <a_c, r> = <a_c, y> - <a_c, w>):
 //                                  S0 += d^2,  S1 += beta^2          | V0 += r^2, V1 += r*y
 //   svm dual     (u = w):          S0 += max(0, 1 - y d), S1 += alpha | V0 += w^2
 //   ridge dual   (u = wbar):       S0 += (d/lambda - y)^2, S1 += alpha^2, S2 += alpha*y | V0 += wbar^2
@@ -532,60 +537,75 @@ __device__ __forceinline__ void block_reduce_store(double (&v)[NS], double* out)
 }
 
 template <int FORM, int G, typename U>
-__global__ __launch_bounds__(256) void k_obj_coords(const int64_t* __restrict__ ptr, const int32_t* __restrict__ idx,
-                                                    const float* __restrict__ val, const U* __restrict__ u,
-                                                    const float* __restrict__ model, const float* __restrict__ y,
-                                                    const float* __restrict__ yv, uint32_t C, double lam,
-                                                    double* __restrict__ partials) {
+__global__ __launch_bounds__(256) void k_objective(ObjArgs o, double* __restrict__ partials, unsigned* counter,
+                                                   double* __restrict__ sums) {
+    constexpr int NS = 5;
+    const U* __restrict__ u = static_cast<const U*>(o.u);
     const int lane = threadIdx.x & (G - 1);
     const uint32_t ngroups = gridDim.x * (256u / G);
-    double t[3] = {0.0, 0.0, 0.0};
-    for (uint32_t c = (blockIdx.x * 256u + threadIdx.x) / G; c < C; c += ngroups) {
+    double t[NS] = {0.0, 0.0, 0.0, 0.0, 0.0};
+    for (uint32_t c = (blockIdx.x * 256u + threadIdx.x) / G; c < o.C; c += ngroups) {
         double d = 0.0;
-        if constexpr (FORM == FORM_RIDGE_PRIMAL) {
-            for (int64_t k = ptr[c] + lane; k < ptr[c + 1]; k += G) {
-                const int32_t i = idx[k];
-                d += (double)val[k] * ((double)yv[i] - (double)u[i]);
-            }
-        } else {
-            for (int64_t k = ptr[c] + lane; k < ptr[c + 1]; k += G) d += (double)val[k] * (double)u[idx[k]];
-        }
+        for (int64_t k = o.ptr[c] + lane; k < o.ptr[c + 1]; k += G) d += (double)o.val[k] * (double)u[o.idx[k]];
         d = group_sum_f64<G>(d);
         if (lane == 0) {
-            const double mo = model[c];
+            const double mo = o.model[c];
             if constexpr (FORM == FORM_RIDGE_PRIMAL) {
-                t[0] += d * d;
+                const double r = o.cyd[c] - d;
+                t[0] += r * r;
                 t[1] += mo * mo;
             } else if constexpr (FORM == FORM_SVM_DUAL) {
-                const double l = 1.0 - (double)y[c] * d;
+                const double l = 1.0 - (double)o.y[c] * d;
                 t[0] += l > 0.0 ? l : 0.0;
                 t[1] += mo;
             } else {
-                const double e = d / lam - (double)y[c];
+                const double e = d / o.lam - (double)o.y[c];
                 t[0] += e * e;
                 t[1] += mo * mo;
-                t[2] += mo * (double)y[c];
+                t[2] += mo * (double)o.y[c];
             }
         }
     }
-    block_reduce_store<3>(t, partials + (size_t)blockIdx.x * 3);
-}
-
-template <int FORM, typename U>
-__global__ __launch_bounds__(256) void k_obj_vector(const U* __restrict__ u, const float* __restrict__ y, int64_t L,
-                                                    double* __restrict__ partials) {
-    double t[2] = {0.0, 0.0};
-    for (int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x; i < L; i += (int64_t)gridDim.x * 256) {
+    for (int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x; i < o.L; i += (int64_t)gridDim.x * 256) {
         if constexpr (FORM == FORM_RIDGE_PRIMAL) {
-            const double r = (double)y[i] - (double)u[i];
-            t[0] += r * r;
-            t[1] += r * (double)y[i];
+            const double r = (double)o.yv[i] - (double)u[i];
+            t[3] += r * r;
+            t[4] += r * (double)o.yv[i];
         } else {
-            const double x = u[i];
-            t[0] += x * x;
+            const double x = (double)u[i];
+            t[3] += x * x;
         }
     }
-    block_reduce_store<2>(t, partials + (size_t)blockIdx.x * 2);
+    block_reduce_store<NS>(t, partials + (size_t)blockIdx.x * NS);
+    // Last workgroup to finish adds the partials in workgroup order.
+    __shared__ int last;
+    if (threadIdx.x == 0) {
+        __threadfence();
+        last = atomicAdd(counter, 1u) == gridDim.x - 1;
+    }
+    __syncthreads();
+    if (!last) return;
+    __threadfence();
+    __shared__ double acc[NS][256];
+#pragma unroll
+    for (int s = 0; s < NS; ++s) {
+        double x = 0.0;
+        for (uint32_t p = threadIdx.x; p < gridDim.x; p += 256)
+            x += __hip_atomic_load(partials + (size_t)p * NS + s, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        acc[s][threadIdx.x] = x;
+    }
+    __syncthreads();
+    for (int w = 128; w > 0; w >>= 1) {
+        if ((int)threadIdx.x < w)
+#pragma unroll
+            for (int s = 0; s < NS; ++s) acc[s][threadIdx.x] += acc[s][threadIdx.x + w];
+        __syncthreads();
+    }
+    if (threadIdx.x == 0) {
+#pragma unroll
+        for (int s = 0; s < NS; ++s) sums[s] = acc[s][0];
+        *counter = 0u;
+    }
 }
 
 // ----------------------------------------------------------------------------------------
@@ -794,13 +814,13 @@ hipError_t launch_gather_dots(const int64_t* ptr, const int32_t* idx, const floa
 }
 
 hipError_t launch_norms(const int64_t* ptr, const int32_t* idx, const float* val, const float* y, uint32_t C, int G,
-                        int blocks, float* out, float* cy, hipStream_t s) {
+                        int blocks, float* out, float* cy, double* cyd, hipStream_t s) {
     switch (G) {
-        case 4: hipLaunchKernelGGL(k_norms<4>, dim3(blocks), dim3(256), 0, s, ptr, idx, val, y, C, out, cy); break;
-        case 8: hipLaunchKernelGGL(k_norms<8>, dim3(blocks), dim3(256), 0, s, ptr, idx, val, y, C, out, cy); break;
-        case 16: hipLaunchKernelGGL(k_norms<16>, dim3(blocks), dim3(256), 0, s, ptr, idx, val, y, C, out, cy); break;
-        case 32: hipLaunchKernelGGL(k_norms<32>, dim3(blocks), dim3(256), 0, s, ptr, idx, val, y, C, out, cy); break;
-        default: hipLaunchKernelGGL(k_norms<64>, dim3(blocks), dim3(256), 0, s, ptr, idx, val, y, C, out, cy); break;
+        case 4: hipLaunchKernelGGL(k_norms<4>, dim3(blocks), dim3(256), 0, s, ptr, idx, val, y, C, out, cy, cyd); break;
+        case 8: hipLaunchKernelGGL(k_norms<8>, dim3(blocks), dim3(256), 0, s, ptr, idx, val, y, C, out, cy, cyd); break;
+        case 16: hipLaunchKernelGGL(k_norms<16>, dim3(blocks), dim3(256), 0, s, ptr, idx, val, y, C, out, cy, cyd); break;
+        case 32: hipLaunchKernelGGL(k_norms<32>, dim3(blocks), dim3(256), 0, s, ptr, idx, val, y, C, out, cy, cyd); break;
+        default: hipLaunchKernelGGL(k_norms<64>, dim3(blocks), dim3(256), 0, s, ptr, idx, val, y, C, out, cy, cyd); break;
     }
     return hipGetLastError();
 }
@@ -821,13 +841,13 @@ hipError_t launch_validate(const int64_t* ptr, uint32_t S, const int32_t* idx, c
 }
 
 template <int FORM, typename U>
-static void obj_coords_g(int G, int blocks, const ObjArgs& o, double* partials, hipStream_t s) {
-    const U* u = static_cast<const U*>(o.u);
+static void objective_typed(const ObjArgs& o, int G, int blocks, double* partials, unsigned* counter, double* sums,
+                            hipStream_t s) {
     switch (G) {
-#define SCD_OBJ(GW)                                                                                              \
-    case GW:                                                                                                     \
-        hipLaunchKernelGGL((k_obj_coords<FORM, GW, U>), dim3(blocks), dim3(256), 0, s, o.ptr, o.idx, o.val, u,  \
-                           o.model, o.y, o.yv, o.C, o.lam, partials);                                            \
+#define SCD_OBJ(GW)                                                                                         \
+    case GW:                                                                                                \
+        hipLaunchKernelGGL((k_objective<FORM, GW, U>), dim3(blocks), dim3(256), 0, s, o, partials, counter, \
+                           sums);                                                                           \
         break;
         SCD_OBJ(4)
         SCD_OBJ(8)
@@ -838,34 +858,24 @@ static void obj_coords_g(int G, int blocks, const ObjArgs& o, double* partials, 
     }
 }
 
-template <int FORM, typename U>
-static void objective_typed(const ObjArgs& o, int G, int blocks, double* pc, double* pv, hipStream_t s) {
-    obj_coords_g<FORM, U>(G, blocks, o, pc, s);
-    hipLaunchKernelGGL((k_obj_vector<FORM, U>), dim3(blocks), dim3(256), 0, s, static_cast<const U*>(o.u), o.yv, o.L,
-                       pv);
-}
-
 template <int FORM>
-static void objective_form(const ObjArgs& o, int G, int blocks, double* pc, double* pv, hipStream_t s) {
+static void objective_form(const ObjArgs& o, int G, int blocks, double* partials, unsigned* counter, double* sums,
+                           hipStream_t s) {
     if (o.wide)
-        objective_typed<FORM, double>(o, G, blocks, pc, pv, s);
+        objective_typed<FORM, double>(o, G, blocks, partials, counter, sums, s);
     else
-        objective_typed<FORM, float>(o, G, blocks, pc, pv, s);
+        objective_typed<FORM, float>(o, G, blocks, partials, counter, sums, s);
 }
 
-// sums[0..2] = coordinate sums, sums[3..4] = vector sums.
-hipError_t launch_objective(int form, const ObjArgs& o, int G, int blocks, double* partials, double* sums,
-                            hipStream_t s) {
-    double* pc = partials;                       // blocks x 3
-    double* pv = partials + (size_t)blocks * 3;  // blocks x 2
+// sums[0..2] = coordinate sums, sums[3..4] = vector sums.  `counter` is zero between calls.
+hipError_t launch_objective(int form, const ObjArgs& o, int G, int blocks, double* partials, unsigned* counter,
+                            double* sums, hipStream_t s) {
     switch (form) {
-        case FORM_RIDGE_PRIMAL: objective_form<FORM_RIDGE_PRIMAL>(o, G, blocks, pc, pv, s); break;
-        case FORM_SVM_DUAL: objective_form<FORM_SVM_DUAL>(o, G, blocks, pc, pv, s); break;
-        case FORM_RIDGE_DUAL: objective_form<FORM_RIDGE_DUAL>(o, G, blocks, pc, pv, s); break;
+        case FORM_RIDGE_PRIMAL: objective_form<FORM_RIDGE_PRIMAL>(o, G, blocks, partials, counter, sums, s); break;
+        case FORM_SVM_DUAL: objective_form<FORM_SVM_DUAL>(o, G, blocks, partials, counter, sums, s); break;
+        case FORM_RIDGE_DUAL: objective_form<FORM_RIDGE_DUAL>(o, G, blocks, partials, counter, sums, s); break;
         default: return hipErrorInvalidValue;
     }
-    hipLaunchKernelGGL(k_sum_partials, dim3(1), dim3(256), 0, s, pc, blocks, 3, sums);
-    hipLaunchKernelGGL(k_sum_partials, dim3(1), dim3(256), 0, s, pv, blocks, 2, sums + 3);
     return hipGetLastError();
 }
 

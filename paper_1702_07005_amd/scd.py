@@ -53,6 +53,9 @@ _SIGS = {
     "scd_objective": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_void_p, ctypes.POINTER(ctypes.c_double),
                                      ctypes.POINTER(ctypes.c_double)]),
     "scd_duality_gap": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_void_p, ctypes.POINTER(ctypes.c_double)]),
+    "scd_duality_gap_async": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int32]),
+    "scd_duality_gap_wait": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_int32, ctypes.POINTER(ctypes.c_double),
+                                            ctypes.POINTER(ctypes.c_double), ctypes.POINTER(ctypes.c_double)]),
     "scd_get_state": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p,
                                      ctypes.POINTER(ctypes.c_int64), ctypes.c_void_p]),
     "scd_set_state": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int64,
@@ -154,6 +157,15 @@ class Solver:
         g = ctypes.c_double()
         _check(lib.scd_duality_gap(self._h, _stream(stream), ctypes.byref(g)))
         return g.value
+
+    def duality_gap_async(self, slot: int, stream=None):
+        _check(lib.scd_duality_gap_async(self._h, _stream(stream), int(slot)))
+
+    def duality_gap_wait(self, slot: int):
+        """(gap, P, D) of the evaluation enqueued in `slot`."""
+        g, P, D = ctypes.c_double(), ctypes.c_double(), ctypes.c_double()
+        _check(lib.scd_duality_gap_wait(self._h, int(slot), ctypes.byref(g), ctypes.byref(P), ctypes.byref(D)))
+        return g.value, P.value, D.value
 
     def get_state(self, stream=None):
         model = torch.empty(self.C, dtype=torch.float32, device=self.device)

@@ -488,3 +488,27 @@ def test_fp64_ordered_lds_tracks_oracle():
         P, _ = s.objective()
         assert abs(P - curve[e][0]) <= 1e-4 * abs(curve[e][0])
     s.close()
+
+
+def test_asynchronous_gap_slots():
+    p = problem("sparse_ridge_small")
+    s = scd.solver_for(p)
+    s.epochs(0, 1)
+    g_sync = s.duality_gap()
+    P_sync, D_sync = s.objective()
+    s.duality_gap_async(0)
+    s.epochs(0, 1)            # queued behind the evaluation: it must not change slot 0's result
+    s.duality_gap_async(1)
+    g0, P0, D0 = s.duality_gap_wait(0)
+    assert (g0, P0, D0) == (g_sync, P_sync, D_sync)
+    g1, _, _ = s.duality_gap_wait(1)
+    assert g1 == s.duality_gap()
+    with pytest.raises(scd.ScdError):
+        s.duality_gap_wait(1)      # nothing pending
+    s.duality_gap_async(2)
+    with pytest.raises(scd.ScdError):
+        s.duality_gap_async(2)     # unread
+    s.duality_gap_wait(2)
+    with pytest.raises(scd.ScdError):
+        s.duality_gap_async(4)     # no such slot
+    s.close()
