@@ -89,7 +89,6 @@ struct scd_solver {
     float* norms = nullptr;
     float* cy = nullptr;  // ridge primal: <y, a_c> per coordinate
     double* cyd = nullptr;  // the same in fp64 (objective evaluation)
-    unsigned* ticket = nullptr;  // last-workgroup counter of the objective kernel (zero between calls)
     void* dummy = nullptr;  // one zero entry standing in for idx/val of an all-empty matrix
     int* flags = nullptr;
     double* partials = nullptr;
@@ -210,7 +209,6 @@ void release(scd_solver* h) {
     (void)hipFree(h->norms);
     (void)hipFree(h->cy);
     (void)hipFree(h->cyd);
-    (void)hipFree(h->ticket);
     (void)hipFree(h->dummy);
     (void)hipFree(h->flags);
     (void)hipFree(h->partials);
@@ -239,7 +237,7 @@ int enqueue_sums(scd_solver* h, hipStream_t s, double* host) {
     o.lam = h->lambda;
     const int G = obj_group(h);
     const int blocks = obj_blocks(h, G);
-    HIP_TRY(launch_objective(h->form, o, G, blocks, h->partials, h->ticket, h->sums, s));
+    HIP_TRY(launch_objective(h->form, o, G, blocks, h->partials, h->sums, s));
     HIP_TRY(hipMemcpyAsync(host, h->sums, 5 * sizeof(double), hipMemcpyDeviceToHost, s));
     return SCD_OK;
 }
@@ -337,8 +335,7 @@ int scd_create(const scd_matrix_t* A, const float* y, double lambda, int32_t for
         hip(hipMalloc(&h->cy, sizeof(float) * (size_t)h->C), "hipMalloc(cy)");
         hip(hipMalloc(&h->cyd, sizeof(double) * (size_t)h->C), "hipMalloc(cyd)");
     }
-    hip(hipMalloc(&h->ticket, sizeof(unsigned)), "hipMalloc(ticket)");
-    hip(hipMemsetAsync(h->ticket, 0, sizeof(unsigned), s), "zero ticket");
+
     hip(hipMalloc(&h->flags, 2 * sizeof(int64_t)), "hipMalloc(flags)");
     if (h->nnz == 0) {
         // The epoch kernels read element 0 of idx/val unconditionally (weight 0 when unused).

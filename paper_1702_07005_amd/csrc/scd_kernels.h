@@ -90,7 +90,7 @@ hipError_t launch_probe(const int64_t* ptr, const int32_t* idx, const float* val
                         float* T, float* K, double* partials, double* out, hipStream_t s);
 hipError_t launch_kappa_max(const float* K, const float* norms, uint32_t C, float mu, int probes, int blocks,
                             unsigned* out, hipStream_t s);
-hipError_t launch_objective(int form, const ObjArgs& o, int G, int blocks, double* partials, unsigned* counter,
-                            double* sums, hipStream_t s);
+hipError_t launch_objective(int form, const ObjArgs& o, int G, int blocks, double* partials, double* sums,
+                            hipStream_t s);
 
 }  // namespace scd

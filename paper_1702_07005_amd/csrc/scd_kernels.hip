@@ -510,10 +510,10 @@ __global__ void k_validate_labels(const float* __restrict__ y, int64_t n, int pm
 }
 
 // ----------------------------------------------------------------------------------------
-// Objective / duality-gap reductions (fp64), one launch.  Every workgroup sums, over the
-// coordinates it owns, the fp64 dot d_c and up to three terms, and over its slice of the shared
-// vector two more; it stores its five partial sums, and the last workgroup to finish (ticket
-// counter) adds all partials in workgroup order and resets the counter.
+// Objective / duality-gap reductions (fp64).  Every workgroup sums, over the coordinates it owns,
+// the fp64 dot d_c and up to three terms, and over its slice of the shared vector two more, and
+// stores its five partial sums; one workgroup then adds the partials in workgroup order
+// (deterministic; no cross-workgroup fences inside the pass).
 //   ridge primal (u = w, r = y - w, d = <a_c, r> = <a_c, y> - <a_c, w>):
 //                                  S0 += d^2,  S1 += beta^2          | V0 += r^2, V1 += r*y
 //   svm dual     (u = w):          S0 += max(0, 1 - y d), S1 += alpha | V0 += w^2
@@ -537,8 +537,7 @@ __device__ __forceinline__ void block_reduce_store(double (&v)[NS], double* out)
 }
 
 template <int FORM, int G, typename U>
-__global__ __launch_bounds__(256) void k_objective(ObjArgs o, double* __restrict__ partials, unsigned* counter,
-                                                   double* __restrict__ sums) {
+__global__ __launch_bounds__(256) void k_objective(ObjArgs o, double* __restrict__ partials) {
     constexpr int NS = 5;
     const U* __restrict__ u = static_cast<const U*>(o.u);
     const int lane = threadIdx.x & (G - 1);
@@ -577,35 +576,6 @@ __global__ __launch_bounds__(256) void k_objective(ObjArgs o, double* __restrict
         }
     }
     block_reduce_store<NS>(t, partials + (size_t)blockIdx.x * NS);
-    // Last workgroup to finish adds the partials in workgroup order.
-    __shared__ int last;
-    if (threadIdx.x == 0) {
-        __threadfence();
-        last = atomicAdd(counter, 1u) == gridDim.x - 1;
-    }
-    __syncthreads();
-    if (!last) return;
-    __threadfence();
-    __shared__ double acc[NS][256];
-#pragma unroll
-    for (int s = 0; s < NS; ++s) {
-        double x = 0.0;
-        for (uint32_t p = threadIdx.x; p < gridDim.x; p += 256)
-            x += __hip_atomic_load(partials + (size_t)p * NS + s, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-        acc[s][threadIdx.x] = x;
-    }
-    __syncthreads();
-    for (int w = 128; w > 0; w >>= 1) {
-        if ((int)threadIdx.x < w)
-#pragma unroll
-            for (int s = 0; s < NS; ++s) acc[s][threadIdx.x] += acc[s][threadIdx.x + w];
-        __syncthreads();
-    }
-    if (threadIdx.x == 0) {
-#pragma unroll
-        for (int s = 0; s < NS; ++s) sums[s] = acc[s][0];
-        *counter = 0u;
-    }
 }
 
 // ----------------------------------------------------------------------------------------
@@ -841,13 +811,11 @@ hipError_t launch_validate(const int64_t* ptr, uint32_t S, const int32_t* idx, c
 }
 
 template <int FORM, typename U>
-static void objective_typed(const ObjArgs& o, int G, int blocks, double* partials, unsigned* counter, double* sums,
-                            hipStream_t s) {
+static void objective_typed(const ObjArgs& o, int G, int blocks, double* partials, hipStream_t s) {
     switch (G) {
 #define SCD_OBJ(GW)                                                                                         \
     case GW:                                                                                                \
-        hipLaunchKernelGGL((k_objective<FORM, GW, U>), dim3(blocks), dim3(256), 0, s, o, partials, counter, \
-                           sums);                                                                           \
+        hipLaunchKernelGGL((k_objective<FORM, GW, U>), dim3(blocks), dim3(256), 0, s, o, partials);         \
         break;
         SCD_OBJ(4)
         SCD_OBJ(8)
@@ -859,23 +827,23 @@ static void objective_typed(const ObjArgs& o, int G, int blocks, double* partial
 }
 
 template <int FORM>
-static void objective_form(const ObjArgs& o, int G, int blocks, double* partials, unsigned* counter, double* sums,
-                           hipStream_t s) {
+static void objective_form(const ObjArgs& o, int G, int blocks, double* partials, hipStream_t s) {
     if (o.wide)
-        objective_typed<FORM, double>(o, G, blocks, partials, counter, sums, s);
+        objective_typed<FORM, double>(o, G, blocks, partials, s);
     else
-        objective_typed<FORM, float>(o, G, blocks, partials, counter, sums, s);
+        objective_typed<FORM, float>(o, G, blocks, partials, s);
 }
 
-// sums[0..2] = coordinate sums, sums[3..4] = vector sums.  `counter` is zero between calls.
-hipError_t launch_objective(int form, const ObjArgs& o, int G, int blocks, double* partials, unsigned* counter,
-                            double* sums, hipStream_t s) {
+// sums[0..2] = coordinate sums, sums[3..4] = vector sums.
+hipError_t launch_objective(int form, const ObjArgs& o, int G, int blocks, double* partials, double* sums,
+                            hipStream_t s) {
     switch (form) {
-        case FORM_RIDGE_PRIMAL: objective_form<FORM_RIDGE_PRIMAL>(o, G, blocks, partials, counter, sums, s); break;
-        case FORM_SVM_DUAL: objective_form<FORM_SVM_DUAL>(o, G, blocks, partials, counter, sums, s); break;
-        case FORM_RIDGE_DUAL: objective_form<FORM_RIDGE_DUAL>(o, G, blocks, partials, counter, sums, s); break;
+        case FORM_RIDGE_PRIMAL: objective_form<FORM_RIDGE_PRIMAL>(o, G, blocks, partials, s); break;
+        case FORM_SVM_DUAL: objective_form<FORM_SVM_DUAL>(o, G, blocks, partials, s); break;
+        case FORM_RIDGE_DUAL: objective_form<FORM_RIDGE_DUAL>(o, G, blocks, partials, s); break;
         default: return hipErrorInvalidValue;
     }
+    hipLaunchKernelGGL(k_sum_partials, dim3(1), dim3(256), 0, s, partials, blocks, 5, sums);
     return hipGetLastError();
 }
 
