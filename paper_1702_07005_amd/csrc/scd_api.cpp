@@ -71,6 +71,10 @@ constexpr int kProbes = 8;                // Hutchinson probes of the coupling e
 // An entry of the shared vector receiving K atomic adds per epoch drifts by about
 // sqrt(K) * 2^-24 of its magnitude in fp32; above this many it is kept in fp64 (drift < 1e-5).
 constexpr uint32_t kWideHits = 28000;
+// The pipelined kernel addresses the shared vector as a raw buffer (byte offsets below 2^31) and
+// keeps up to 256 * 16 entries of a segment in registers when a workgroup takes a coordinate.
+constexpr int64_t kPipeMaxBytes = (int64_t(1) << 31) - 8;
+constexpr int64_t kPipeBlockSlices = 16;
 
 }  // namespace
 
@@ -109,6 +113,8 @@ struct scd_solver {
     int64_t window = 0;
     int64_t group = 0;
     int64_t fresh = 0;
+    int64_t pipeline = 1;
+    double* sink = nullptr;  // pipelined kernel, fp64 shared vector: slots inactive lanes add 0 to
 };
 
 namespace {
@@ -120,6 +126,8 @@ int auto_group(const scd_solver* h) {
         if (mean <= (double)(G * slice_depth(G))) return G;
     return kBlockThreads;  // one workgroup per coordinate
 }
+
+int64_t shared_bytes(const scd_solver* h) { return h->L * (int64_t)(h->wide ? sizeof(double) : sizeof(float)); }
 
 int plan_epoch(const scd_solver* h, LaunchPlan* lp, uint32_t* n_groups) {
     memset(lp, 0, sizeof *lp);
@@ -146,12 +154,16 @@ int plan_epoch(const scd_solver* h, LaunchPlan* lp, uint32_t* n_groups) {
         return SCD_OK;
     }
     const int64_t cap_blocks = (int64_t)h->cus * kBlocksPerCU;
+    // Software-pipelined kernel: shared vector within a raw buffer's range, every segment within
+    // the register slices.
+    const bool pipe_ok = h->pipeline && shared_bytes(h) <= kPipeMaxBytes;
     if (G == kBlockThreads) {
         int64_t groups = cap_blocks;
         if (window > 0 && window < groups) groups = window;
         if (groups > h->C) groups = h->C;
         if (groups < 1) groups = 1;
-        lp->kind = PLAN_BLOCK;
+        lp->kind = pipe_ok && h->max_seg <= (int64_t)kBlockThreads * kPipeBlockSlices ? PLAN_PIPE : PLAN_BLOCK;
+        lp->group = kBlockThreads;
         lp->blocks = (int)groups;
         *n_groups = (uint32_t)groups;
         return SCD_OK;
@@ -167,6 +179,7 @@ int plan_epoch(const scd_solver* h, LaunchPlan* lp, uint32_t* n_groups) {
     lp->kind = h->max_seg > long_len ? PLAN_MIXED : PLAN_GROUP;
     lp->long_len = (uint32_t)long_len;
     lp->tail = h->max_seg > (int64_t)G * slice_depth(G);
+    if (lp->kind == PLAN_GROUP && !lp->tail && pipe_ok) lp->kind = PLAN_PIPE;
     lp->group = G;
     lp->blocks = (int)((groups + per_block - 1) / per_block);
     if (lp->kind == PLAN_MIXED) {
@@ -213,6 +226,7 @@ void release(scd_solver* h) {
     (void)hipFree(h->flags);
     (void)hipFree(h->partials);
     (void)hipFree(h->sums);
+    (void)hipFree(h->sink);
     if (h->host_sums) (void)hipHostFree(h->host_sums);
     if (h->slot_sums) (void)hipHostFree(h->slot_sums);
     for (hipEvent_t& e : h->slot_event)
@@ -346,6 +360,11 @@ int scd_create(const scd_matrix_t* A, const float* y, double lambda, int32_t for
     }
     hip(hipMalloc(&h->partials, sizeof(double) * (size_t)kObjBlocksMax * 5), "hipMalloc(partials)");
     hip(hipMalloc(&h->sums, sizeof(double) * 8), "hipMalloc(sums)");
+    if (rc == SCD_OK) {
+        const size_t sink_bytes = sizeof(double) * 256 * (size_t)h->cus * kBlocksPerCU;
+        hip(hipMalloc(&h->sink, sink_bytes), "hipMalloc(sink)");
+        hip(hipMemsetAsync(h->sink, 0, sink_bytes, s), "zero sink");
+    }
     hip(hipHostMalloc(&h->host_sums, sizeof(double) * 8, hipHostMallocDefault), "hipHostMalloc");
     hip(hipHostMalloc(&h->slot_sums, sizeof(double) * 5 * kGapSlots, hipHostMallocDefault), "hipHostMalloc(slots)");
     for (int i = 0; i < kGapSlots; ++i)
@@ -476,6 +495,8 @@ int scd_epochs(scd_handle_t h, uint64_t seed, int32_t n_epochs, void* stream) {
     a.k.inv_lamN = (float)(1.0 / lamN);
     a.k.lam = (float)h->lambda;
     a.n_groups = n_groups;
+    a.u_bytes = shared_bytes(h) <= kPipeMaxBytes ? (uint32_t)shared_bytes(h) : 0u;
+    a.sink = h->sink;
     hipStream_t s = (hipStream_t)stream;
     for (int32_t e = 0; e < n_epochs; ++e) {
         a.perm = make_perm(seed, (uint64_t)h->epoch, (uint32_t)h->C);
@@ -577,6 +598,9 @@ int scd_set_option(scd_handle_t h, const char* key, int64_t value) {
     } else if (!strcmp(key, "fresh_reads")) {
         if (value != 0 && value != 1) return fail(SCD_ERR_INVALID, "fresh_reads must be 0 or 1");
         h->fresh = value;
+    } else if (!strcmp(key, "pipeline")) {
+        if (value != 0 && value != 1) return fail(SCD_ERR_INVALID, "pipeline must be 0 or 1");
+        h->pipeline = value;
     } else if (!strcmp(key, "shared_fp64")) {
         if (value != 0 && value != 1) return fail(SCD_ERR_INVALID, "shared_fp64 must be 0 or 1");
         if (value == h->wide) return SCD_OK;
@@ -608,6 +632,7 @@ int scd_get_option(scd_handle_t h, const char* key, int64_t* value) {
     if (!strcmp(key, "window")) *value = h->window;
     else if (!strcmp(key, "group")) *value = h->group;
     else if (!strcmp(key, "fresh_reads")) *value = h->fresh;
+    else if (!strcmp(key, "pipeline")) *value = h->pipeline;
     else if (!strcmp(key, "shared_fp64")) *value = h->wide;
     else return fail(SCD_ERR_UNSUPPORTED, "unknown option '%s'", key);
     return SCD_OK;
@@ -620,8 +645,10 @@ int scd_get_info(scd_handle_t h, scd_info_t* info) {
     uint32_t n_groups = 1;
     plan_epoch(h, &lp, &n_groups);
     info->formulation = h->form;
-    info->group_lanes = (lp.kind == PLAN_GROUP || lp.kind == PLAN_MIXED) ? lp.group
+    info->group_lanes = (lp.kind == PLAN_GROUP || lp.kind == PLAN_MIXED || lp.kind == PLAN_PIPE) ? lp.group
                         : lp.kind == PLAN_BLOCK && !lp.ordered ? kBlockThreads : 1024;
+    info->kernel = lp.kind;
+    info->reserved = 0;
     info->long_len = lp.kind == PLAN_MIXED ? lp.long_len : 0;
     info->shared_fp64 = h->wide;
     info->max_hits = h->max_hits;

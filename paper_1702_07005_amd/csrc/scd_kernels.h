@@ -40,14 +40,16 @@ struct EpochArgs {
     StepConsts k;
     PermKeys perm;       // perm.n = C
     uint32_t n_groups;   // persistent groups (coordinates in flight at most)
-    uint32_t pad_;
+    uint32_t u_bytes;    // byte size of the shared vector when below 2^31 (raw-buffer range), else 0
+    double* sink;        // pipelined kernel, fp64 shared vector: 256 slots per workgroup that
+                         // inactive lanes add 0 to
 };
 
-enum { PLAN_GROUP = 0, PLAN_BLOCK = 1, PLAN_ORDERED_LDS = 2, PLAN_MIXED = 3 };
+enum { PLAN_GROUP = 0, PLAN_BLOCK = 1, PLAN_ORDERED_LDS = 2, PLAN_MIXED = 3, PLAN_PIPE = 4 };
 
 struct LaunchPlan {
     int kind;        // PLAN_*
-    int group;       // lanes per coordinate (PLAN_GROUP)
+    int group;       // lanes per coordinate (PLAN_GROUP, PLAN_MIXED, PLAN_PIPE: 4..64 or 256)
     int blocks;      // workgroups launched
     int fresh;       // device-scope gathers
     int ordered;     // PLAN_BLOCK with a single workgroup, fenced between coordinates

@@ -147,15 +147,19 @@ struct CoordMeta {
     float m_old, sn, ylab;
 };
 
-__device__ __forceinline__ CoordMeta load_meta(const EpochArgs& a, uint32_t j) {
+__device__ __forceinline__ CoordMeta load_meta_of(const EpochArgs& a, uint32_t m) {
     CoordMeta c;
-    c.m = perm_at(j, a.perm);
+    c.m = m;
     c.s0 = a.ptr[c.m];
     c.s1 = a.ptr[c.m + 1];
     c.m_old = a.model[c.m];
     c.sn = a.norms[c.m];
     c.ylab = a.y[c.m];
     return c;
+}
+
+__device__ __forceinline__ CoordMeta load_meta(const EpochArgs& a, uint32_t j) {
+    return load_meta_of(a, perm_at(j, a.perm));
 }
 
 // Register slice r of a segment: element s0 + lane + r*G.  Lanes past the end read element 0
@@ -175,6 +179,21 @@ __device__ __forceinline__ void load_seg(const EpochArgs& a, const CoordMeta& c,
     }
 }
 
+
+// As load_seg, but lanes past the end keep entry 0's value: the pipelined kernel masks them
+// through out-of-range shared-vector offsets (the gather returns 0, the atomic is dropped), so
+// no select has to wait for the loaded value next to the load.
+template <int G, int R>
+__device__ __forceinline__ void load_seg_raw(const EpochArgs& a, const CoordMeta& c, int lane, int (&ci)[R],
+                                             float (&cv)[R]) {
+#pragma unroll
+    for (int r = 0; r < R; ++r) {
+        const int64_t k = c.s0 + lane + (int64_t)r * G;
+        const int64_t kk = k < c.s1 ? k : 0;
+        ci[r] = a.idx[kk];
+        cv[r] = a.val[kk];
+    }
+}
 
 // ----------------------------------------------------------------------------------------
 // Epoch kernel, sub-wave / wave groups: G lanes per coordinate, 256-thread workgroups,
@@ -238,6 +257,147 @@ __global__ __launch_bounds__(256) void k_epoch_group(EpochArgs a) {
             ci[r] = ni[r];
             cv[r] = nv[r];
         }
+    }
+}
+
+// ----------------------------------------------------------------------------------------
+// Shared-vector access of the pipelined kernel.  The shared vector is addressed as a raw
+// buffer: the hardware range check returns 0 for a load at an offset outside [0, bytes) and
+// drops an fp32 atomic there.  A lane past its segment's end, or a whole coordinate whose
+// step is zero, thus issues the same instructions as the others with no memory traffic, and
+// each iteration of k_epoch_pipe issues a fixed number of vector memory operations: the
+// compiler can wait for one load without also waiting for atomics issued after it (the
+// completion counter is in order).  There is no fp64 buffer atomic builtin, so an fp64
+// shared vector is updated with unconditional global atomics whose inactive lanes add 0 to a
+// slot of their own in a scratch array (`sink`) instead.  (A FLAT atomic aimed at LDS would
+// avoid that traffic, but a pending FLAT operation makes the compiler wait for everything.)
+// ----------------------------------------------------------------------------------------
+template <typename U>
+struct SharedBuf {
+    __amdgpu_buffer_rsrc_t r;
+    uint32_t oob;  // first out-of-range byte offset
+    U* base;
+    U* sink;       // fp64 only: this lane's scratch slot
+};
+
+template <typename U>
+__device__ __forceinline__ SharedBuf<U> shared_buf(void* u, uint32_t bytes, U* sink) {
+    // word 3 = 0x00020000: 32-bit data format, the gfx9-family raw-buffer setting.
+    return {__builtin_amdgcn_make_buffer_rsrc(u, (short)0, (int)bytes, 0x00020000), bytes, static_cast<U*>(u), sink};
+}
+
+template <bool FRESH, typename U>
+__device__ __forceinline__ float buf_load(const SharedBuf<U>& b, uint32_t i, bool in) {
+    // cache policy 16 = sc1: device-scope load, as __hip_atomic_load at agent scope emits.
+    constexpr int pol = FRESH ? 16 : 0;
+    const uint32_t off = in ? i * (uint32_t)sizeof(U) : b.oob;
+    if constexpr (sizeof(U) == 4) {
+        return __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(b.r, (int)off, 0, pol));
+    } else {
+        const auto v = __builtin_amdgcn_raw_buffer_load_b64(b.r, (int)off, 0, pol);
+        return (float)__builtin_bit_cast(double, v);
+    }
+}
+
+template <typename U>
+__device__ __forceinline__ void buf_atomic_add(const SharedBuf<U>& b, uint32_t i, bool in, float v) {
+    if constexpr (sizeof(U) == 4) {
+        (void)__builtin_amdgcn_raw_ptr_buffer_atomic_fadd_f32(v, b.r, (int)(in ? i * 4u : b.oob), 0, 0);
+    } else {
+        U* p = in ? b.base + i : b.sink;
+        __hip_atomic_fetch_add(p, in ? (double)v : 0.0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    }
+}
+
+// One coordinate of k_epoch_pipe.  On entry `ci/cv` hold the current coordinate's segment
+// and `nxt` the next one's metadata (both loaded one step earlier).  Issue order:
+//   gathers(cur), segment(nxt) -> ni/nv, metadata two positions ahead -> nn,
+//   [wait for the gathers] reduce + step + model store, atomics(cur).
+// The loads consumed by the next step are all issued before this step's atomics, and the
+// gathers of the next step are issued right after them, so a group's critical path per
+// coordinate is one gather round trip (the scatter's completion overlaps it).
+template <int FORM, int G, int R, bool FRESH, typename U>
+__device__ __forceinline__ bool pipe_step(const EpochArgs& a, const SharedBuf<U>& ub, int lane, uint32_t j,
+                                          const CoordMeta& cur, const int (&ci)[R], const float (&cv)[R],
+                                          const CoordMeta& nxt, int (&ni)[R], float (&nv)[R], CoordMeta& nn,
+                                          float (*part)[G > 64 ? G / 64 : 1], int& buf) {
+    const int64_t len = cur.s1 - cur.s0;
+    float gv[R];
+#pragma unroll
+    for (int r = 0; r < R; ++r) gv[r] = buf_load<FRESH>(ub, (uint32_t)ci[r], (int64_t)(lane + r * G) < len);
+    // The scheduler may not move work across these points: the gathers go out first, and the
+    // prefetches are issued before the wait for the gathers (it would otherwise sink them
+    // below the dot product and put their round trip on the critical path).
+    __builtin_amdgcn_sched_barrier(0);
+    const uint64_t P = a.n_groups, n = a.perm.n;
+    const bool more = (uint64_t)j + P < n;
+    load_seg_raw<G, R>(a, nxt, lane, ni, nv);
+    const uint64_t j2 = (uint64_t)j + 2 * P;
+    const uint32_t m2 = perm_at(j2 < n ? (uint32_t)j2 : j, a.perm);
+    nn = load_meta_of(a, m2);
+    __builtin_amdgcn_sched_barrier(0);
+    float acc = 0.0f;
+#pragma unroll
+    for (int r = 0; r < R; ++r) acc = fmaf(cv[r], gv[r], acc);
+    float g;
+    if constexpr (G <= 64) {
+        g = group_sum<G>(acc);
+    } else {
+        constexpr int NW = G / 64;
+        acc = group_sum<64>(acc);
+        if ((threadIdx.x & 63) == 0) part[buf][threadIdx.x >> 6] = acc;
+        __syncthreads();
+        g = 0.0f;
+#pragma unroll
+        for (int w = 0; w < NW; ++w) g += part[buf][w];
+        buf ^= 1;
+    }
+    float coef;
+    const float m_new = coord_step<FORM>(g, cur.sn, cur.m_old, cur.ylab, a.k, &coef);
+    a.model[cur.m] = m_new;  // every lane of the group stores the same value: no branch
+    const bool moves = coef != 0.0f;
+#pragma unroll
+    for (int r = 0; r < R; ++r) buf_atomic_add(ub, (uint32_t)ci[r], moves && (int64_t)(lane + r * G) < len, coef * cv[r]);
+    return more;
+}
+
+// ----------------------------------------------------------------------------------------
+// Epoch kernel, software-pipelined two coordinates deep, shared vector addressed as a raw
+// buffer.  G lanes per coordinate (4..64 in 256-thread workgroups, or G = 256: one
+// workgroup per coordinate, wave sums combined through LDS).  Every segment fits the
+// register slices (length <= G*R).  The loop body is unrolled twice so that the register
+// arrays of consecutive coordinates alternate instead of being copied (a copy would have to
+// wait for the loads that fill it).
+// ----------------------------------------------------------------------------------------
+template <int FORM, int G, int R, bool FRESH, typename U>
+__global__ __launch_bounds__(256) void k_epoch_pipe(EpochArgs a) {
+    __shared__ float part[2][G > 64 ? G / 64 : 1];
+    const int lane = threadIdx.x & (G - 1);
+    const uint32_t gid = (blockIdx.x * 256u + threadIdx.x) / G;
+    if (gid >= a.n_groups || gid >= a.perm.n) return;  // G = 256: the whole workgroup leaves
+    const SharedBuf<U> ub =
+        shared_buf<U>(a.u, a.u_bytes, reinterpret_cast<U*>(a.sink) + (size_t)blockIdx.x * 256 + threadIdx.x);
+    const uint32_t P = a.n_groups;
+    uint32_t j = gid;
+    int buf = 0;
+    CoordMeta cA = load_meta(a, j);
+    int ciA[R], ciB[R];
+    float cvA[R], cvB[R];
+    load_seg_raw<G, R>(a, cA, lane, ciA, cvA);
+    CoordMeta cB = load_meta(a, (uint64_t)j + P < a.perm.n ? j + P : j);
+    // Inactive operations standing in for the model store and the atomics that follow the
+    // metadata loads inside the loop: both ways into the loop then have the same operations
+    // outstanding, and the compiler's wait counts need not assume the shorter one.
+#pragma unroll
+    for (int r = 0; r <= R; ++r) buf_atomic_add(ub, 0u, false, 0.0f);
+    for (;;) {
+        CoordMeta cA2, cB2;
+        if (!pipe_step<FORM, G, R, FRESH>(a, ub, lane, j, cA, ciA, cvA, cB, ciB, cvB, cA2, part, buf)) break;
+        j += P;
+        if (!pipe_step<FORM, G, R, FRESH>(a, ub, lane, j, cB, ciB, cvB, cA2, ciA, cvA, cB2, part, buf)) break;
+        j += P;
+        cA = cA2;
+        cB = cB2;
     }
 }
 
@@ -692,11 +852,31 @@ static hipError_t launch_group(const EpochArgs& a, int blocks, bool tail, hipStr
 }
 
 template <int FORM, int G, bool FRESH, typename U>
+static hipError_t launch_pipe(const EpochArgs& a, int blocks, hipStream_t s) {
+    constexpr int R = G == 256 ? 16 : slice_depth(G);
+    hipLaunchKernelGGL((k_epoch_pipe<FORM, G, R, FRESH, U>), dim3(blocks), dim3(256), 0, s, a);
+    return hipGetLastError();
+}
+
+template <int FORM, int G, bool FRESH, typename U>
 static hipError_t launch_mixed(const EpochArgs& a, int blocks, uint32_t long_len, hipStream_t s) {
     constexpr int R = slice_depth(G);
     const uint32_t ng = (a.n_groups + blocks - 1) / blocks;  // <= 256 / G by construction of the plan
     hipLaunchKernelGGL((k_epoch_mixed<FORM, G, R, FRESH, U>), dim3(blocks), dim3(256), 0, s, a, long_len, ng);
     return hipGetLastError();
+}
+
+template <int FORM, bool FRESH, typename U>
+static hipError_t launch_pipe_by_width(const EpochArgs& a, const LaunchPlan& lp, hipStream_t s) {
+    switch (lp.group) {
+        case 4: return launch_pipe<FORM, 4, FRESH, U>(a, lp.blocks, s);
+        case 8: return launch_pipe<FORM, 8, FRESH, U>(a, lp.blocks, s);
+        case 16: return launch_pipe<FORM, 16, FRESH, U>(a, lp.blocks, s);
+        case 32: return launch_pipe<FORM, 32, FRESH, U>(a, lp.blocks, s);
+        case 64: return launch_pipe<FORM, 64, FRESH, U>(a, lp.blocks, s);
+        case 256: return launch_pipe<FORM, 256, FRESH, U>(a, lp.blocks, s);
+        default: return hipErrorInvalidValue;
+    }
 }
 
 template <int FORM, bool FRESH, typename U>
@@ -723,6 +903,8 @@ static hipError_t launch_epoch_typed(const EpochArgs& a, const LaunchPlan& lp, h
         hipLaunchKernelGGL((k_epoch_ordered_lds<FORM, U>), dim3(1), dim3(1024), lp.lds_bytes, s, a, lp.L);
         return hipGetLastError();
     }
+    if (lp.kind == PLAN_PIPE)
+        return lp.fresh ? launch_pipe_by_width<FORM, true, U>(a, lp, s) : launch_pipe_by_width<FORM, false, U>(a, lp, s);
     if (lp.kind == PLAN_BLOCK) {
         if (lp.ordered)
             hipLaunchKernelGGL((k_epoch_block<FORM, 256, 16, true, true, U>), dim3(lp.blocks), dim3(256), 0, s, a);

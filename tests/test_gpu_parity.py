@@ -205,12 +205,14 @@ ASYNC = [("sparse_ridge", 6), ("sparse_ridge_small", 8), ("text_svm_twin", 8), (
          ("text_ridge_twin", 8)]
 
 
+@pytest.mark.parametrize("pipeline", [1, 0])
 @pytest.mark.parametrize("key,E", ASYNC)
-def test_async_epochs_invariant_and_gap_curve(key, E):
-    print(f"async {key}", flush=True)
+def test_async_epochs_invariant_and_gap_curve(key, E, pipeline):
     p = problem(key)
     mo, so, curve = _oracle_curve(p, 0, E)
     s = scd.solver_for(p)
+    s.set_option("pipeline", pipeline)
+    print(f"async {key} kernel {s.info()['kernel']}", flush=True)
     P0, _ = s.objective()
     floor = 1e-6 * abs(P0)
     for e in range(E):
@@ -270,13 +272,22 @@ def test_ridge_dual_async_and_ordered():
 
 @pytest.mark.parametrize("group", [4, 8, 16, 32, 64, 256])
 @pytest.mark.parametrize("fresh_reads", [0, 1])
-def test_every_group_width_keeps_invariant(group, fresh_reads):
-    print(f"group {group} fresh {fresh_reads}", flush=True)
-    p = problem("click_svm_twin")
+@pytest.mark.parametrize("pipeline", [1, 0])
+def test_every_group_width_keeps_invariant(group, fresh_reads, pipeline):
+    print(f"group {group} fresh {fresh_reads} pipeline {pipeline}", flush=True)
+    p = problem("click_svm_twin")  # 39 entries per row: every width holds a row in registers
     s = scd.solver_for(p)
     s.set_option("group", group)
     s.set_option("fresh_reads", fresh_reads)
-    assert s.info()["group_lanes"] == group
+    s.set_option("pipeline", pipeline)
+    info = s.info()
+    assert info["group_lanes"] == group
+    held = group * {4: 4, 8: 6, 16: 10, 32: 5, 64: 4, 256: 16}[group]  # entries kept in registers
+    if group == 256:
+        plain = "block"
+    else:
+        plain = "mixed" if info["max_segment"] > 2 * held else "group"
+    assert info["kernel"] == ("pipelined" if pipeline and info["max_segment"] <= held else plain)
     s.epochs(1, 3)
     gm, gs, _ = s.get_state()
     assert rel_inf(f64(gs), fresh(p, f64(gm))) <= 1e-4
@@ -284,6 +295,25 @@ def test_every_group_width_keeps_invariant(group, fresh_reads):
     dref, cond = orc.gather_dots(p.ptr, p.idx, p.val, gs.cpu().numpy())
     assert np.all(np.abs(d - dref) <= 1e-4 * cond + 1e-30)
     s.close()
+
+
+def test_epoch_kernel_selection():
+    # every segment within the register slices -> pipelined kernel (fp32 or fp64 shared vector);
+    # long segments -> the mixed kernel; window 1 -> ordered.
+    expect = {"dense_ridge": "pipelined", "sparse_ridge_small": "pipelined", "text_svm_twin": "pipelined",
+              "click_svm_twin": "pipelined", "text_ridge_twin": "mixed"}
+    for key, kernel in expect.items():
+        s = scd.solver_for(problem(key))
+        assert s.info()["kernel"] == kernel, key
+        s.set_option("window", 1)  # ordered: the shared vector in LDS when it fits (160 KiB), else one workgroup
+        p = problem(key)
+        assert s.info()["kernel"] == ("ordered_lds" if p.L * 4 + 128 <= 160 * 1024 else "block"), key
+        s.set_option("window", 0)
+        s.set_option("shared_fp64", 1)
+        assert s.info()["kernel"] == kernel, key
+        s.set_option("pipeline", 0)
+        assert s.info()["kernel"] != "pipelined", key
+        s.close()
 
 
 @pytest.mark.parametrize("window", [2, 7, 64, 1000])
@@ -456,13 +486,16 @@ def test_hot_entries_select_fp64_shared_vector():
     t.close()
 
 
+@pytest.mark.parametrize("pipeline", [1, 0])
 @pytest.mark.parametrize("group", [8, 32, 256])
-def test_fp64_shared_vector_keeps_parity(group):
+def test_fp64_shared_vector_keeps_parity(group, pipeline):
     p = problem("click_svm_twin")
     s = scd.solver_for(p)
     s.set_option("shared_fp64", 1)
     s.set_option("group", group)
+    s.set_option("pipeline", pipeline)
     assert s.get_option("shared_fp64") == 1 and s.info()["shared_fp64"] == 1
+    assert (s.info()["kernel"] == "pipelined") == bool(pipeline)
     mo, so, curve = _oracle_curve(p, 0, 3)
     for e in range(3):
         s.epochs(0, 1)
