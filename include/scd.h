@@ -110,8 +110,7 @@ typedef struct {
     int32_t kernel;       /* epoch kernel the next scd_epochs launches: 0 lane groups,
                              1 one workgroup per coordinate, 2 ordered with the shared
                              vector in LDS, 3 lane groups with long segments handed to the
-                             workgroup, 4 software-pipelined (every segment held in
-                             registers)                                 */
+                             workgroup, 4 software-pipelined                                 */
     int32_t reserved;
 } scd_info_t;
 
@@ -187,8 +186,8 @@ int scd_set_state(scd_handle_t h, const float *model_dev, const float *shared_de
  *   "fresh_reads" 1 = gather the shared vector with device-scope loads (bypass non-coherent
  *                 caches), 0 = plain loads.
  *   "pipeline"    1 (default) = use the software-pipelined epoch kernel where it applies
- *                 (shared vector below 2 GiB, every segment within its group's register
- *                 slices), 0 = the plain kernels.
+ *                 (shared vector below 2 GiB; with skewed segment lengths only when each
+ *                 in-flight coordinate can have a workgroup of its own), 0 = the plain kernels.
  *   "shared_fp64" 1 = store the shared vector in fp64 (fp64 atomic adds), 0 = fp32.  Chosen at
  *                 create: fp64 when some entry receives more than 28,000 atomic adds per epoch,
  *                 where fp32 accumulation would drift by more than about 1e-5 of its magnitude.

@@ -71,10 +71,8 @@ constexpr int kProbes = 8;                // Hutchinson probes of the coupling e
 // An entry of the shared vector receiving K atomic adds per epoch drifts by about
 // sqrt(K) * 2^-24 of its magnitude in fp32; above this many it is kept in fp64 (drift < 1e-5).
 constexpr uint32_t kWideHits = 28000;
-// The pipelined kernel addresses the shared vector as a raw buffer (byte offsets below 2^31) and
-// keeps up to 256 * 16 entries of a segment in registers when a workgroup takes a coordinate.
+// The pipelined kernel addresses the shared vector as a raw buffer (byte offsets below 2^31).
 constexpr int64_t kPipeMaxBytes = (int64_t(1) << 31) - 8;
-constexpr int64_t kPipeBlockSlices = 16;
 
 }  // namespace
 
@@ -154,15 +152,14 @@ int plan_epoch(const scd_solver* h, LaunchPlan* lp, uint32_t* n_groups) {
         return SCD_OK;
     }
     const int64_t cap_blocks = (int64_t)h->cus * kBlocksPerCU;
-    // Software-pipelined kernel: shared vector within a raw buffer's range, every segment within
-    // the register slices.
+    // Software-pipelined kernel: shared vector within a raw buffer's range.
     const bool pipe_ok = h->pipeline && shared_bytes(h) <= kPipeMaxBytes;
     if (G == kBlockThreads) {
         int64_t groups = cap_blocks;
         if (window > 0 && window < groups) groups = window;
         if (groups > h->C) groups = h->C;
         if (groups < 1) groups = 1;
-        lp->kind = pipe_ok && h->max_seg <= (int64_t)kBlockThreads * kPipeBlockSlices ? PLAN_PIPE : PLAN_BLOCK;
+        lp->kind = pipe_ok ? PLAN_PIPE : PLAN_BLOCK;
         lp->group = kBlockThreads;
         lp->blocks = (int)groups;
         *n_groups = (uint32_t)groups;
@@ -174,12 +171,22 @@ int plan_epoch(const scd_solver* h, LaunchPlan* lp, uint32_t* n_groups) {
     if (groups > h->C) groups = h->C;
     if (groups < 1) groups = 1;
     // Segments longer than twice the group's register cache would keep their gather-to-scatter
-    // interval open far longer than the others: give them the whole workgroup.
+    // interval open far longer than the others.
     const int64_t long_len = 2 * (int64_t)G * slice_depth(G);
-    lp->kind = h->max_seg > long_len ? PLAN_MIXED : PLAN_GROUP;
+    const bool skewed = h->max_seg > long_len;
+    if (pipe_ok && skewed && h->group == 0 && groups <= cap_blocks) {
+        // Few coordinates in flight and skewed lengths: each in-flight coordinate gets a workgroup
+        // of its own, so a long segment is streamed by 256 lanes without holding up others.
+        lp->kind = PLAN_PIPE;
+        lp->group = kBlockThreads;
+        lp->blocks = (int)groups;
+        *n_groups = (uint32_t)groups;
+        return SCD_OK;
+    }
+    lp->kind = skewed ? PLAN_MIXED : PLAN_GROUP;
     lp->long_len = (uint32_t)long_len;
     lp->tail = h->max_seg > (int64_t)G * slice_depth(G);
-    if (lp->kind == PLAN_GROUP && !lp->tail && pipe_ok) lp->kind = PLAN_PIPE;
+    if (!skewed && pipe_ok) lp->kind = PLAN_PIPE;  // segments beyond the slices take its long path
     lp->group = G;
     lp->blocks = (int)((groups + per_block - 1) / per_block);
     if (lp->kind == PLAN_MIXED) {

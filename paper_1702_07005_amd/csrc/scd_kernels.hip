@@ -316,12 +316,58 @@ __device__ __forceinline__ void buf_atomic_add(const SharedBuf<U>& b, uint32_t i
 // The loads consumed by the next step are all issued before this step's atomics, and the
 // gathers of the next step are issued right after them, so a group's critical path per
 // coordinate is one gather round trip (the scatter's completion overlaps it).
+template <int G>
+__device__ __forceinline__ float pipe_reduce(float acc, float (*part)[G > 64 ? G / 64 : 1], int& buf) {
+    if constexpr (G <= 64) {
+        return group_sum<G>(acc);
+    } else {
+        constexpr int NW = G / 64;
+        acc = group_sum<64>(acc);
+        if ((threadIdx.x & 63) == 0) part[buf][threadIdx.x >> 6] = acc;
+        __syncthreads();
+        float g = 0.0f;
+#pragma unroll
+        for (int w = 0; w < NW; ++w) g += part[buf][w];
+        buf ^= 1;
+        return g;
+    }
+}
+
+// A segment longer than the register slices (rare; skewed lengths): stream it twice, gather
+// then scatter, with ordinary waits.  It ends by issuing the same operations, in the same
+// order, as the end of the pipelined step (next segment, metadata two ahead, then 1 + R
+// operations standing in for the model store and the atomics), so that the compiler's wait
+// counts after the step stay exact on both paths.
+template <int FORM, int G, int R, bool FRESH, typename U>
+__device__ __forceinline__ void pipe_long(const EpochArgs& a, const SharedBuf<U>& ub, int lane, uint32_t j,
+                                       const CoordMeta& cur, const CoordMeta& nxt, int (&ni)[R], float (&nv)[R],
+                                       CoordMeta& nn, float (*part)[G > 64 ? G / 64 : 1], int& buf) {
+    float acc = 0.0f;
+    for (int64_t k = cur.s0 + lane; k < cur.s1; k += G) acc = fmaf(a.val[k], buf_load<FRESH>(ub, (uint32_t)a.idx[k], true), acc);
+    const float g = pipe_reduce<G>(acc, part, buf);
+    float coef;
+    const float m_new = coord_step<FORM>(g, cur.sn, cur.m_old, cur.ylab, a.k, &coef);
+    a.model[cur.m] = m_new;
+    if (coef != 0.0f)
+        for (int64_t k = cur.s0 + lane; k < cur.s1; k += G) buf_atomic_add(ub, (uint32_t)a.idx[k], true, coef * a.val[k]);
+    const uint64_t P = a.n_groups, n = a.perm.n;
+    load_seg_raw<G, R>(a, nxt, lane, ni, nv);
+    const uint64_t j2 = (uint64_t)j + 2 * P;
+    nn = load_meta_of(a, perm_at(j2 < n ? (uint32_t)j2 : j, a.perm));
+#pragma unroll
+    for (int r = 0; r <= R; ++r) buf_atomic_add(ub, 0u, false, 0.0f);
+}
+
 template <int FORM, int G, int R, bool FRESH, typename U>
 __device__ __forceinline__ bool pipe_step(const EpochArgs& a, const SharedBuf<U>& ub, int lane, uint32_t j,
                                           const CoordMeta& cur, const int (&ci)[R], const float (&cv)[R],
                                           const CoordMeta& nxt, int (&ni)[R], float (&nv)[R], CoordMeta& nn,
                                           float (*part)[G > 64 ? G / 64 : 1], int& buf) {
     const int64_t len = cur.s1 - cur.s0;
+    if (len > (int64_t)G * R) {
+        pipe_long<FORM, G, R, FRESH, U>(a, ub, lane, j, cur, nxt, ni, nv, nn, part, buf);
+        return (uint64_t)j + a.n_groups < a.perm.n;
+    }
     float gv[R];
 #pragma unroll
     for (int r = 0; r < R; ++r) gv[r] = buf_load<FRESH>(ub, (uint32_t)ci[r], (int64_t)(lane + r * G) < len);
@@ -339,19 +385,7 @@ __device__ __forceinline__ bool pipe_step(const EpochArgs& a, const SharedBuf<U>
     float acc = 0.0f;
 #pragma unroll
     for (int r = 0; r < R; ++r) acc = fmaf(cv[r], gv[r], acc);
-    float g;
-    if constexpr (G <= 64) {
-        g = group_sum<G>(acc);
-    } else {
-        constexpr int NW = G / 64;
-        acc = group_sum<64>(acc);
-        if ((threadIdx.x & 63) == 0) part[buf][threadIdx.x >> 6] = acc;
-        __syncthreads();
-        g = 0.0f;
-#pragma unroll
-        for (int w = 0; w < NW; ++w) g += part[buf][w];
-        buf ^= 1;
-    }
+    const float g = pipe_reduce<G>(acc, part, buf);
     float coef;
     const float m_new = coord_step<FORM>(g, cur.sn, cur.m_old, cur.ylab, a.k, &coef);
     a.model[cur.m] = m_new;  // every lane of the group stores the same value: no branch
@@ -364,8 +398,8 @@ __device__ __forceinline__ bool pipe_step(const EpochArgs& a, const SharedBuf<U>
 // ----------------------------------------------------------------------------------------
 // Epoch kernel, software-pipelined two coordinates deep, shared vector addressed as a raw
 // buffer.  G lanes per coordinate (4..64 in 256-thread workgroups, or G = 256: one
-// workgroup per coordinate, wave sums combined through LDS).  Every segment fits the
-// register slices (length <= G*R).  The loop body is unrolled twice so that the register
+// workgroup per coordinate, wave sums combined through LDS).  Segments of up to G*R entries
+// stay in registers; longer ones take pipe_long.  The loop body is unrolled twice so that the register
 // arrays of consecutive coordinates alternate instead of being copied (a copy would have to
 // wait for the loads that fill it).
 // ----------------------------------------------------------------------------------------

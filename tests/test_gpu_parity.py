@@ -284,10 +284,11 @@ def test_every_group_width_keeps_invariant(group, fresh_reads, pipeline):
     assert info["group_lanes"] == group
     held = group * {4: 4, 8: 6, 16: 10, 32: 5, 64: 4, 256: 16}[group]  # entries kept in registers
     if group == 256:
-        plain = "block"
+        assert info["kernel"] == ("pipelined" if pipeline else "block")
+    elif info["max_segment"] > 2 * held:
+        assert info["kernel"] == "mixed"
     else:
-        plain = "mixed" if info["max_segment"] > 2 * held else "group"
-    assert info["kernel"] == ("pipelined" if pipeline and info["max_segment"] <= held else plain)
+        assert info["kernel"] == ("pipelined" if pipeline else "group")
     s.epochs(1, 3)
     gm, gs, _ = s.get_state()
     assert rel_inf(f64(gs), fresh(p, f64(gm))) <= 1e-4
@@ -301,10 +302,15 @@ def test_epoch_kernel_selection():
     # every segment within the register slices -> pipelined kernel (fp32 or fp64 shared vector);
     # long segments -> the mixed kernel; window 1 -> ordered.
     expect = {"dense_ridge": "pipelined", "sparse_ridge_small": "pipelined", "text_svm_twin": "pipelined",
-              "click_svm_twin": "pipelined", "text_ridge_twin": "mixed"}
+              "click_svm_twin": "pipelined", "text_ridge_twin": "pipelined"}
     for key, kernel in expect.items():
         s = scd.solver_for(problem(key))
         assert s.info()["kernel"] == kernel, key
+        if key == "text_ridge_twin":  # skewed lengths, small window: one workgroup per coordinate
+            assert s.info()["group_lanes"] == 256
+            s.set_option("pipeline", 0)
+            assert s.info()["kernel"] == "mixed"
+            s.set_option("pipeline", 1)
         s.set_option("window", 1)  # ordered: the shared vector in LDS when it fits (160 KiB), else one workgroup
         p = problem(key)
         assert s.info()["kernel"] == ("ordered_lds" if p.L * 4 + 128 <= 160 * 1024 else "block"), key
@@ -314,6 +320,34 @@ def test_epoch_kernel_selection():
         s.set_option("pipeline", 0)
         assert s.info()["kernel"] != "pipelined", key
         s.close()
+
+
+@pytest.mark.parametrize("key,over,group", [
+    # every column 160-320 entries with 16-lane groups (10 slices each): all take the long path
+    ("sparse_ridge", dict(n_rows=2_000, n_cols=500, density=0.09), 16),
+    # one workgroup per column; the hottest columns exceed 256 x 16 entries
+    ("text_ridge_csc", dict(n_rows=6_000, n_cols=166_000, row_nnz=370), 0),
+])
+def test_pipelined_long_segments(key, over, group):
+    p = synth.make(key, **over)
+    E = 6
+    _, _, curve = _oracle_curve(p, 0, E)
+    s = scd.solver_for(p)
+    s.set_option("group", group)
+    info = s.info()
+    held = info["group_lanes"] * (16 if info["group_lanes"] == 256 else 10)
+    print(f"long segments {key}: kernel {info['kernel']} lanes {info['group_lanes']} max {info['max_segment']}",
+          flush=True)
+    assert info["kernel"] == "pipelined" and info["max_segment"] > held
+    P0, _ = s.objective()
+    for e in range(E):
+        s.epochs(0, 1)
+        gm, gs, _ = s.get_state()
+        assert rel_inf(f64(gs), fresh(p, f64(gm))) <= 1e-4, e
+        G, Gr = s.duality_gap(), curve[e][2]
+        if Gr > 1e-6 * abs(P0):
+            assert G <= 2.0 * Gr, (e, G, Gr)
+    s.close()
 
 
 @pytest.mark.parametrize("window", [2, 7, 64, 1000])
