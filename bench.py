@@ -93,6 +93,9 @@ def cpu_baseline(prob, budget_s: float, seed: int):
     el = 0.0
     curve = []
     ttg = None
+    # One core, pinned: the oracle is sequential by definition.
+    allowed = sorted(os.sched_getaffinity(0))
+    os.sched_setaffinity(0, {allowed[0]})
     while True:
         t0 = time.perf_counter()
         orc.epochs(prob.form, prob.n_rows, prob.n_cols, prob.ptr, prob.idx, prob.val, prob.y, prob.lam, seed, epochs,
@@ -106,9 +109,17 @@ def cpu_baseline(prob, budget_s: float, seed: int):
             ttg = (epochs, el)
         if el >= budget_s or epochs >= 1000:
             break
+    os.sched_setaffinity(0, set(allowed))
+    cpu = "unknown"
+    try:
+        with open("/proc/cpuinfo") as fh:
+            cpu = next((ln.split(":", 1)[1].strip() for ln in fh if ln.startswith("model name")), cpu)
+    except OSError:
+        pass
     return {"value": prob.nnz * epochs / el, "unit": "nnz/s", "cores": 1, "kind": "oracle",
             "sample": f"{epochs} sequential fp64 epochs of the same workload from the zero state "
-                      f"({el:.1f} s of epoch time on one host thread)",
+                      f"({el:.1f} s of epoch time on one host thread, pinned to core {allowed[0]})",
+            "cpu_model": cpu, "host_cores_visible": len(allowed),
             "epochs_per_s": epochs / el,
             "time_to_gap_1e-3_s": ttg[1] if ttg else None, "epochs_to_gap_1e-3": ttg[0] if ttg else None,
             "gap_curve": [float(f"{g:.3e}") for g in curve[:12]]}
@@ -126,6 +137,9 @@ def main():
     ap.add_argument("--max-gap-epochs", type=int, default=200)
     ap.add_argument("--gap-seconds", type=float, default=60.0,
                     help="stop the time-to-gap run once this much epoch time has been spent")
+    ap.add_argument("--ablation", action="store_true",
+                    help="before the timed steps, run the frozen gather-dot kernel (no scatter) three times, for "
+                         "attributing L2 counters: stream only (set-up norms), gathers only, full epoch")
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="after the timed steps, run a plain 1 GiB device-to-device copy twice (a kernel of known "
                          "traffic for scaling rocprofv3 FETCH_SIZE/WRITE_SIZE counters)")
@@ -178,6 +192,12 @@ def main():
                 hits[thr] = (e + 1, t_epochs)
         if 1e-6 in hits or t_epochs >= args.gap_seconds:
             break
+
+    if args.ablation:
+        _, shared_now, _ = solver.get_state()
+        for _ in range(3):
+            solver.gather_dots(shared_now)
+        torch.cuda.synchronize()
 
     # --- timed steps ------------------------------------------------------------------------
     reset()
@@ -240,6 +260,13 @@ def main():
     }
     solver.close()
     ceil = device_ceilings(prob.L)
+    if traffic is not None:
+        # Measured HBM bytes (rocprofv3 counters, copy-calibrated) over the live epoch time.
+        tg = traffic / epoch_avg / 1e9
+        out["roofline"]["traffic_GBps"] = tg
+        out["roofline"]["traffic_frac_of_peak"] = tg / HBM_PEAK_GBS
+        if ceil["copy_bytes_per_s"]:
+            out["roofline"]["traffic_frac_of_copy"] = tg * 1e9 / ceil["copy_bytes_per_s"]
     if ceil["atomic_adds_per_s"]:
         # The scatter issues one device-scope atomic per stored entry.
         rate = prob.nnz / epoch_avg
