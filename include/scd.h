@@ -110,8 +110,10 @@ typedef struct {
     int32_t kernel;       /* epoch kernel the next scd_epochs launches: 0 lane groups,
                              1 one workgroup per coordinate, 2 ordered with the shared
                              vector in LDS, 3 lane groups with long segments handed to the
-                             workgroup, 4 software-pipelined                                 */
-    int32_t reserved;
+                             workgroup, 4 software-pipelined, 5 hot set in LDS (one
+                             workgroup, at most 8 coordinates in flight)               */
+    int32_t hot_entries;  /* shared-vector entries the hot-set kernel keeps in LDS
+                             (0 until it is first needed)                               */
 } scd_info_t;
 
 /* Create a solver for min P / max D of the chosen formulation (Sec. II; Sec. III-C).
@@ -188,6 +190,12 @@ int scd_set_state(scd_handle_t h, const float *model_dev, const float *shared_de
  *   "pipeline"    1 (default) = use the software-pipelined epoch kernel where it applies
  *                 (shared vector below 2 GiB; with skewed segment lengths only when each
  *                 in-flight coordinate can have a workgroup of its own), 0 = the plain kernels.
+ *   "hot"         1 (default) = with at most 8 coordinates in flight, segments of at most 64
+ *                 entries and "group" 0, run the epoch in one workgroup that keeps the most-updated
+ *                 shared-vector entries in LDS (their gathers and adds never leave the CU) and
+ *                 reads the others ahead of their coordinates; 0 = never.  The hot set is chosen
+ *                 (a pass over the matrix, synchronising) when this first applies: at create, or
+ *                 when "window" or "hot" is set.
  *   "shared_fp64" 1 = store the shared vector in fp64 (fp64 atomic adds), 0 = fp32.  Chosen at
  *                 create: fp64 when some entry receives more than 28,000 atomic adds per epoch,
  *                 where fp32 accumulation would drift by more than about 1e-5 of its magnitude.

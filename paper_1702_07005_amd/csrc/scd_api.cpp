@@ -3,13 +3,14 @@
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
-#include <cmath>
 #include <climits>
+#include <cmath>
 #include <cstdarg>
 #include <cstdio>
 #include <cstring>
 #include <new>
 #include <string>
+#include <vector>
 
 #include "scd.h"
 #include "scd_kernels.h"
@@ -73,6 +74,11 @@ constexpr int kProbes = 8;                // Hutchinson probes of the coupling e
 constexpr uint32_t kWideHits = 28000;
 // The pipelined kernel addresses the shared vector as a raw buffer (byte offsets below 2^31).
 constexpr int64_t kPipeMaxBytes = (int64_t(1) << 31) - 8;
+// Hot-set kernel: hot entries kept in LDS (sized for an fp64 shared vector next to the largest
+// batch buffers), minimum share of stored entries they must cover, and the bound on its waits
+// (sleeps of about 64 cycles each: about half a second).
+constexpr double kHotMinCover = 0.1;
+constexpr uint32_t kHotSpinLimit = 1u << 24;
 
 }  // namespace
 
@@ -113,6 +119,15 @@ struct scd_solver {
     int64_t fresh = 0;
     int64_t pipeline = 1;
     double* sink = nullptr;  // pipelined kernel, fp64 shared vector: slots inactive lanes add 0 to
+    // Hot-set kernel (windows of at most kHotMaxWindow): built on first need.
+    int64_t hot = 1;              // option
+    int hot_built = 0;
+    uint16_t* slot_of = nullptr;  // [L]
+    int32_t* hot_ids = nullptr;   // [n_hot]
+    uint32_t n_hot = 0;
+    double hot_cover = 0.0;       // fraction of stored entries that point at a hot entry
+    int* hot_err = nullptr;       // device flag set by a timed-out wait in the hot-set kernel
+    int* err_host = nullptr;      // pinned copies of hot_err: one per gap slot + one for reduce_state
 };
 
 namespace {
@@ -126,6 +141,37 @@ int auto_group(const scd_solver* h) {
 }
 
 int64_t shared_bytes(const scd_solver* h) { return h->L * (int64_t)(h->wide ? sizeof(double) : sizeof(float)); }
+
+// Batch geometry of the hot-set kernel for window W.
+struct HotGeom {
+    uint32_t W, B, Smax, hot_bytes;
+    size_t lds;
+};
+
+bool hot_geometry(const scd_solver* h, int64_t W, HotGeom* g) {
+    if (W < 2 || W > kHotMaxWindow || h->max_seg > kHotMaxSegment || h->C < 1) return false;
+    g->W = (uint32_t)W;
+    g->Smax = (uint32_t)std::max<int64_t>(8, (h->max_seg + 7) / 8 * 8);
+    const uint32_t cap = std::min<uint32_t>(64, 64u * kHotEntriesPerLane / g->Smax);
+    g->B = cap / g->W * g->W;
+    if (g->B < g->W) return false;
+    g->hot_bytes = (uint32_t)(((size_t)h->n_hot * (h->wide ? sizeof(double) : sizeof(float)) + 15) / 16 * 16);
+    g->lds = hot_lds_bytes(g->hot_bytes, g->B, g->Smax);
+    return true;
+}
+
+// Largest hot set that fits LDS next to the largest batch buffers (64 coordinates x 24 entries) as
+// fp64 entries, so that it stays valid at both widths of the shared vector.
+uint32_t hot_capacity(const scd_solver* h) {
+    const size_t worst = hot_lds_bytes(0, 64, kHotEntriesPerLane);
+    if (h->max_lds <= worst + 16) return 0;
+    return (uint32_t)std::min<size_t>((h->max_lds - worst - 16) / sizeof(double), kHotCold - 1);
+}
+
+bool hot_plan(const scd_solver* h, int64_t window, HotGeom* g) {
+    return h->hot && h->group == 0 && h->hot_built && h->n_hot > 0 && h->hot_cover >= kHotMinCover &&
+           hot_geometry(h, window, g) && g->lds <= h->max_lds;
+}
 
 int plan_epoch(const scd_solver* h, LaunchPlan* lp, uint32_t* n_groups) {
     memset(lp, 0, sizeof *lp);
@@ -149,6 +195,15 @@ int plan_epoch(const scd_solver* h, LaunchPlan* lp, uint32_t* n_groups) {
         lp->fresh = 1;
         lp->blocks = 1;
         *n_groups = 1;
+        return SCD_OK;
+    }
+    HotGeom hg;
+    if (hot_plan(h, window, &hg)) {
+        lp->kind = PLAN_HOT;
+        lp->group = 8;
+        lp->blocks = 1;
+        lp->lds_bytes = hg.lds;
+        *n_groups = hg.W;
         return SCD_OK;
     }
     const int64_t cap_blocks = (int64_t)h->cus * kBlocksPerCU;
@@ -198,6 +253,102 @@ int plan_epoch(const scd_solver* h, LaunchPlan* lp, uint32_t* n_groups) {
     return SCD_OK;
 }
 
+// Number of entries with at least T hits, and the sum of their hits (synchronises).
+int hot_count(scd_solver* h, const unsigned* hits, unsigned T, unsigned long long* dev2, hipStream_t s,
+              unsigned long long* count, unsigned long long* sum) {
+    unsigned long long host2[2] = {0, 0};
+    HIP_TRY(hipMemsetAsync(dev2, 0, 2 * sizeof(unsigned long long), s));
+    HIP_TRY(launch_hot_count_ge(hits, h->L, T, dev2, s));
+    HIP_TRY(hipMemcpyAsync(host2, dev2, sizeof host2, hipMemcpyDeviceToHost, s));
+    HIP_TRY(hipStreamSynchronize(s));
+    *count = host2[0];
+    *sum = host2[1];
+    return SCD_OK;
+}
+
+// Hot set of the hot-set kernel: the entries with at least T stored entries pointing at them (T
+// the smallest threshold that keeps the set within LDS capacity), slots in index order, so the
+// set is a deterministic function of the matrix.  Built once, on first need; synchronises.
+int build_hot_tables(scd_solver* h, hipStream_t s) {
+    if (h->hot_built) return SCD_OK;
+    h->hot_built = 1;  // a set that cannot help (n_hot = 0) is not retried
+    const uint32_t cap = hot_capacity(h);
+    if (cap == 0 || h->nnz == 0 || h->max_seg > kHotMaxSegment || h->max_hits == 0) return SCD_OK;
+    unsigned* hits = nullptr;
+    unsigned long long* dev2 = nullptr;
+    unsigned* blocks = nullptr;
+    const int64_t nblk = (h->L + kHotAssignBlock - 1) / kHotAssignBlock;
+    int rc = SCD_OK;
+    auto hip = [&](hipError_t e, const char* what) {
+        if (rc == SCD_OK && e != hipSuccess)
+            rc = fail(e == hipErrorOutOfMemory ? SCD_ERR_OOM : SCD_ERR_HIP, "%s: %s", what, hipGetErrorString(e));
+        return rc == SCD_OK;
+    };
+    hip(hipMalloc(&hits, sizeof(unsigned) * (size_t)h->L), "hipMalloc(hits)");
+    hip(hipMalloc(&dev2, 2 * sizeof(unsigned long long)), "hipMalloc(counts)");
+    hip(hipMalloc(&blocks, sizeof(unsigned) * (size_t)nblk), "hipMalloc(block counts)");
+    if (rc == SCD_OK) {
+        hip(hipMemsetAsync(hits, 0, sizeof(unsigned) * (size_t)h->L, s), "zero hits");
+        hip(launch_count_hits(h->idx, h->nnz, hits, s), "count hits");
+    }
+    // Smallest T in [1, max_hits + 1] with count(hits >= T) <= cap (count at max_hits + 1 is 0).
+    unsigned lo = 1, hi = h->max_hits + 1;
+    unsigned long long cnt = 0, sum = 0;
+    while (rc == SCD_OK && lo < hi) {
+        const unsigned mid = lo + (hi - lo) / 2;
+        if (int r = hot_count(h, hits, mid, dev2, s, &cnt, &sum)) rc = r;
+        else if (cnt <= cap) hi = mid;
+        else lo = mid + 1;
+    }
+    if (rc == SCD_OK && (rc = hot_count(h, hits, lo, dev2, s, &cnt, &sum)) == SCD_OK && cnt > 0) {
+        std::vector<unsigned> base((size_t)nblk);
+        hip(launch_hot_block_count(hits, h->L, lo, blocks, s), "hot block counts");
+        hip(hipMemcpyAsync(base.data(), blocks, sizeof(unsigned) * (size_t)nblk, hipMemcpyDeviceToHost, s),
+            "copy block counts");
+        hip(hipStreamSynchronize(s), "synchronize");
+        unsigned run = 0;
+        for (auto& b : base) {
+            const unsigned c = b;
+            b = run;
+            run += c;
+        }
+        hip(hipMemcpyAsync(blocks, base.data(), sizeof(unsigned) * (size_t)nblk, hipMemcpyHostToDevice, s),
+            "copy block bases");
+        hip(hipMalloc(&h->slot_of, sizeof(uint16_t) * (size_t)h->L), "hipMalloc(slot_of)");
+        hip(hipMalloc(&h->hot_ids, sizeof(int32_t) * (size_t)cnt), "hipMalloc(hot_ids)");
+        hip(launch_hot_assign(hits, h->L, lo, blocks, h->slot_of, h->hot_ids, s), "hot slots");
+        hip(hipStreamSynchronize(s), "synchronize");
+        if (rc == SCD_OK) {
+            h->n_hot = (uint32_t)cnt;
+            h->hot_cover = (double)sum / (double)h->nnz;
+        }
+    }
+    (void)hipFree(hits);
+    (void)hipFree(dev2);
+    (void)hipFree(blocks);
+    if (rc != SCD_OK) {
+        (void)hipFree(h->slot_of);
+        (void)hipFree(h->hot_ids);
+        h->slot_of = nullptr;
+        h->hot_ids = nullptr;
+        h->n_hot = 0;
+    }
+    return rc;
+}
+
+// Builds the hot set when the current options would use the hot-set kernel.
+int hot_if_needed(scd_solver* h, hipStream_t s) {
+    const int64_t window = h->window ? h->window : h->auto_window;
+    HotGeom g;
+    if (!h->hot || h->group != 0 || h->hot_built || !hot_geometry(h, window, &g)) return SCD_OK;
+    return build_hot_tables(h, s);
+}
+
+int check_hot_err(scd_solver* h, int v) {
+    if (v) return fail(SCD_ERR_HIP, "hot-set epoch kernel: a wait between its waves timed out; the state is invalid");
+    return SCD_OK;
+}
+
 int obj_group(const scd_solver* h) {
     const int G = h->group ? (int)h->group : auto_group(h);
     return G > 64 ? 64 : G;
@@ -234,6 +385,10 @@ void release(scd_solver* h) {
     (void)hipFree(h->partials);
     (void)hipFree(h->sums);
     (void)hipFree(h->sink);
+    (void)hipFree(h->slot_of);
+    (void)hipFree(h->hot_ids);
+    (void)hipFree(h->hot_err);
+    (void)hipHostFree(h->err_host);
     if (h->host_sums) (void)hipHostFree(h->host_sums);
     if (h->slot_sums) (void)hipHostFree(h->slot_sums);
     for (hipEvent_t& e : h->slot_event)
@@ -266,8 +421,9 @@ int enqueue_sums(scd_solver* h, hipStream_t s, double* host) {
 // The same, waiting for the result in h->host_sums.
 int reduce_state(scd_solver* h, hipStream_t s) {
     if (int r = enqueue_sums(h, s, h->host_sums)) return r;
+    HIP_TRY(hipMemcpyAsync(h->err_host + kGapSlots, h->hot_err, sizeof(int), hipMemcpyDeviceToHost, s));
     HIP_TRY(hipStreamSynchronize(s));
-    return SCD_OK;
+    return check_hot_err(h, h->err_host[kGapSlots]);
 }
 
 void objectives_from_sums(const scd_solver* h, const double* t, double* P, double* D) {
@@ -367,6 +523,10 @@ int scd_create(const scd_matrix_t* A, const float* y, double lambda, int32_t for
     }
     hip(hipMalloc(&h->partials, sizeof(double) * (size_t)kObjBlocksMax * 5), "hipMalloc(partials)");
     hip(hipMalloc(&h->sums, sizeof(double) * 8), "hipMalloc(sums)");
+    hip(hipMalloc(&h->hot_err, sizeof(int)), "hipMalloc(hot_err)");
+    hip(hipMemsetAsync(h->hot_err, 0, sizeof(int), s), "zero hot_err");
+    hip(hipHostMalloc(&h->err_host, sizeof(int) * (kGapSlots + 1), hipHostMallocDefault), "hipHostMalloc(err)");
+    if (rc == SCD_OK) memset(h->err_host, 0, sizeof(int) * (kGapSlots + 1));
     if (rc == SCD_OK) {
         const size_t sink_bytes = sizeof(double) * 256 * (size_t)h->cus * kBlocksPerCU;
         hip(hipMalloc(&h->sink, sink_bytes), "hipMalloc(sink)");
@@ -456,6 +616,7 @@ int scd_create(const scd_matrix_t* A, const float* y, double lambda, int32_t for
             if (h->coupling > 1e-6) w = std::min<int64_t>(w, std::max<int64_t>(1, h->C / 16));
             h->auto_window = std::max<int64_t>(1, std::min<int64_t>(w, h->C));
         }
+        if (rc == SCD_OK) step(hot_if_needed(h, s));
         hip(hipMemsetAsync(h->model, 0, sizeof(float) * (size_t)h->C, s), "zero model");
         hip(hipMemsetAsync(h->u, 0, (h->wide ? sizeof(double) : sizeof(float)) * (size_t)h->L, s), "zero shared");
         hip(hipStreamSynchronize(s), "synchronize");
@@ -489,6 +650,11 @@ int scd_epochs(scd_handle_t h, uint64_t seed, int32_t n_epochs, void* stream) {
     uint32_t n_groups = 1;
     if (int r = plan_epoch(h, &lp, &n_groups)) return r;
     if (lp.kind == PLAN_ORDERED_LDS) HIP_TRY(ordered_lds_prepare(h->form, lp.wide != 0, lp.lds_bytes));
+    HotGeom hg{};
+    if (lp.kind == PLAN_HOT) {
+        hot_plan(h, n_groups, &hg);
+        HIP_TRY(hot_prepare(h->form, h->wide != 0, hg.lds));
+    }
     EpochArgs a{};
     a.ptr = h->ptr;
     a.idx = h->idx;
@@ -507,7 +673,22 @@ int scd_epochs(scd_handle_t h, uint64_t seed, int32_t n_epochs, void* stream) {
     hipStream_t s = (hipStream_t)stream;
     for (int32_t e = 0; e < n_epochs; ++e) {
         a.perm = make_perm(seed, (uint64_t)h->epoch, (uint32_t)h->C);
-        HIP_TRY(launch_epoch(h->form, a, lp, s));
+        if (lp.kind == PLAN_HOT) {
+            HotArgs ha{};
+            ha.e = a;
+            ha.slot_of = h->slot_of;
+            ha.hot_ids = h->hot_ids;
+            ha.n_hot = h->n_hot;
+            ha.W = hg.W;
+            ha.B = hg.B;
+            ha.Smax = hg.Smax;
+            ha.hot_bytes = hg.hot_bytes;
+            ha.spin_limit = kHotSpinLimit;
+            ha.err = h->hot_err;
+            HIP_TRY(launch_epoch_hot(h->form, h->wide != 0, ha, hg.lds, s));
+        } else {
+            HIP_TRY(launch_epoch(h->form, a, lp, s));
+        }
         ++h->epoch;
     }
     return SCD_OK;
@@ -540,6 +721,7 @@ int scd_duality_gap_async(scd_handle_t h, void* stream, int32_t slot) {
     if (int r = set_device(h)) return r;
     hipStream_t s = (hipStream_t)stream;
     if (int r = enqueue_sums(h, s, h->slot_sums + 5 * slot)) return r;
+    HIP_TRY(hipMemcpyAsync(h->err_host + slot, h->hot_err, sizeof(int), hipMemcpyDeviceToHost, s));
     HIP_TRY(hipEventRecord(h->slot_event[slot], s));
     h->slot_pending[slot] = 1;
     return SCD_OK;
@@ -551,6 +733,7 @@ int scd_duality_gap_wait(scd_handle_t h, int32_t slot, double* gap, double* prim
     if (!h->slot_pending[slot]) return fail(SCD_ERR_INVALID, "slot %d holds no evaluation", slot);
     h->slot_pending[slot] = 0;
     HIP_TRY(hipEventSynchronize(h->slot_event[slot]));
+    if (int r = check_hot_err(h, h->err_host[slot])) return r;
     double P, D;
     objectives_from_sums(h, h->slot_sums + 5 * slot, &P, &D);
     if (!std::isfinite(P) || !std::isfinite(D)) return fail(SCD_ERR_NUMERIC, "non-finite objective (P=%g, D=%g)", P, D);
@@ -580,6 +763,7 @@ int scd_set_state(scd_handle_t h, const float* model, const float* shared, int64
     if (epoch < 0) return fail(SCD_ERR_INVALID, "epoch must be >= 0");
     if (int r = set_device(h)) return r;
     hipStream_t s = (hipStream_t)stream;
+    HIP_TRY(hipMemsetAsync(h->hot_err, 0, sizeof(int), s));  // a written state replaces an invalid one
     if (model) HIP_TRY(hipMemcpyAsync(h->model, model, sizeof(float) * (size_t)h->C, hipMemcpyDeviceToDevice, s));
     if (shared) {
         if (h->wide)
@@ -597,11 +781,20 @@ int scd_set_option(scd_handle_t h, const char* key, int64_t value) {
     if (!strcmp(key, "window")) {
         if (value < 0 || value > 2147483647LL) return fail(SCD_ERR_INVALID, "window must be in [0, 2^31)");
         h->window = value;
+        if (int r = set_device(h)) return r;
+        if (int r = hot_if_needed(h, nullptr)) return r;
+    } else if (!strcmp(key, "hot")) {
+        if (value != 0 && value != 1) return fail(SCD_ERR_INVALID, "hot must be 0 or 1");
+        h->hot = value;
+        if (int r = set_device(h)) return r;
+        if (int r = hot_if_needed(h, nullptr)) return r;
     } else if (!strcmp(key, "group")) {
         if (!(value == 0 || value == 4 || value == 8 || value == 16 || value == 32 || value == 64 ||
               value == kBlockThreads))
             return fail(SCD_ERR_INVALID, "group must be 0, 4, 8, 16, 32, 64 or 256");
         h->group = value;
+        if (int r = set_device(h)) return r;
+        if (int r = hot_if_needed(h, nullptr)) return r;
     } else if (!strcmp(key, "fresh_reads")) {
         if (value != 0 && value != 1) return fail(SCD_ERR_INVALID, "fresh_reads must be 0 or 1");
         h->fresh = value;
@@ -640,6 +833,7 @@ int scd_get_option(scd_handle_t h, const char* key, int64_t* value) {
     else if (!strcmp(key, "group")) *value = h->group;
     else if (!strcmp(key, "fresh_reads")) *value = h->fresh;
     else if (!strcmp(key, "pipeline")) *value = h->pipeline;
+    else if (!strcmp(key, "hot")) *value = h->hot;
     else if (!strcmp(key, "shared_fp64")) *value = h->wide;
     else return fail(SCD_ERR_UNSUPPORTED, "unknown option '%s'", key);
     return SCD_OK;
@@ -652,10 +846,11 @@ int scd_get_info(scd_handle_t h, scd_info_t* info) {
     uint32_t n_groups = 1;
     plan_epoch(h, &lp, &n_groups);
     info->formulation = h->form;
-    info->group_lanes = (lp.kind == PLAN_GROUP || lp.kind == PLAN_MIXED || lp.kind == PLAN_PIPE) ? lp.group
+    info->group_lanes = (lp.kind == PLAN_GROUP || lp.kind == PLAN_MIXED || lp.kind == PLAN_PIPE || lp.kind == PLAN_HOT)
+                            ? lp.group
                         : lp.kind == PLAN_BLOCK && !lp.ordered ? kBlockThreads : 1024;
     info->kernel = lp.kind;
-    info->reserved = 0;
+    info->hot_entries = (int32_t)h->n_hot;
     info->long_len = lp.kind == PLAN_MIXED ? lp.long_len : 0;
     info->shared_fp64 = h->wide;
     info->max_hits = h->max_hits;

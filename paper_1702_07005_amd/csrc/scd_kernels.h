@@ -45,7 +45,7 @@ struct EpochArgs {
                          // inactive lanes add 0 to
 };
 
-enum { PLAN_GROUP = 0, PLAN_BLOCK = 1, PLAN_ORDERED_LDS = 2, PLAN_MIXED = 3, PLAN_PIPE = 4 };
+enum { PLAN_GROUP = 0, PLAN_BLOCK = 1, PLAN_ORDERED_LDS = 2, PLAN_MIXED = 3, PLAN_PIPE = 4, PLAN_HOT = 5 };
 
 struct LaunchPlan {
     int kind;        // PLAN_*
@@ -75,11 +75,43 @@ struct ObjArgs {
     double lam;
 };
 
+// Hot-set epoch (one workgroup): the n_hot most-updated shared-vector entries live in LDS for the
+// epoch; one consumer wave runs the W in-flight coordinates from LDS only, kHotProducers waves stream
+// the next batches (segment, hot slot or cold value) into LDS buffers.
+constexpr int kHotProducers = 4;
+constexpr int kHotEntriesPerLane = 24;  // producer lanes x this >= batch entries (64 x 24 = 1536)
+constexpr int kHotMaxWindow = 8;         // consumer wave: W groups of 8 lanes
+constexpr int kHotMaxSegment = 64;
+constexpr uint16_t kHotCold = 0xFFFF;    // slot_of value of an entry that is not hot
+
+struct HotArgs {
+    EpochArgs e;
+    const uint16_t* slot_of;  // [L]: LDS slot of a hot shared-vector entry, kHotCold otherwise
+    const int32_t* hot_ids;   // [n_hot]: shared-vector index of each slot
+    uint32_t n_hot;
+    uint32_t W;               // coordinates in flight (<= kHotMaxWindow)
+    uint32_t B;               // coordinates per batch (multiple of W)
+    uint32_t Smax;            // entries per coordinate reserved in a batch buffer (multiple of 8)
+    uint32_t hot_bytes;       // LDS bytes of the hot array (16-byte aligned)
+    uint32_t spin_limit;      // bounded waits: after this many sleeps a wave gives up and sets *err
+    int* err;
+};
+
+size_t hot_lds_bytes(uint32_t hot_bytes, uint32_t B, uint32_t Smax);
+hipError_t hot_prepare(int form, bool wide, size_t lds_bytes);
+hipError_t launch_epoch_hot(int form, bool wide, const HotArgs& h, size_t lds_bytes, hipStream_t s);
+hipError_t launch_hot_count_ge(const unsigned* hits, int64_t L, unsigned T, unsigned long long* out2, hipStream_t s);
+hipError_t launch_hot_block_count(const unsigned* hits, int64_t L, unsigned T, unsigned* block_counts, hipStream_t s);
+hipError_t launch_hot_assign(const unsigned* hits, int64_t L, unsigned T, const unsigned* block_base, uint16_t* slot_of,
+                             int32_t* hot_ids, hipStream_t s);
+constexpr int kHotAssignBlock = 1024;  // shared-vector indices per workgroup in the slot assignment
+
 hipError_t launch_epoch(int form, const EpochArgs& a, const LaunchPlan& lp, hipStream_t s);
 hipError_t ordered_lds_prepare(int form, bool wide, size_t lds_bytes);
 hipError_t launch_convert_f32_to_f64(const float* in, int64_t n, double* out, hipStream_t s);
 hipError_t launch_convert_f64_to_f32(const double* in, int64_t n, float* out, hipStream_t s);
 hipError_t launch_max_hits(const int32_t* idx, int64_t nnz, int64_t L, unsigned* hits, unsigned* out, hipStream_t s);
+hipError_t launch_count_hits(const int32_t* idx, int64_t nnz, unsigned* hits, hipStream_t s);
 hipError_t launch_perm_fill(const PermKeys& p, int32_t* out, hipStream_t s);
 hipError_t launch_gather_dots(const int64_t* ptr, const int32_t* idx, const float* val, const float* u, uint32_t C,
                               int G, int blocks, float* out, hipStream_t s);

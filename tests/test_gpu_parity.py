@@ -302,7 +302,7 @@ def test_epoch_kernel_selection():
     # every segment within the register slices -> pipelined kernel (fp32 or fp64 shared vector);
     # long segments -> the mixed kernel; window 1 -> ordered.
     expect = {"dense_ridge": "pipelined", "sparse_ridge_small": "pipelined", "text_svm_twin": "pipelined",
-              "click_svm_twin": "pipelined", "text_ridge_twin": "pipelined"}
+              "click_svm_twin": "hot_lds", "text_ridge_twin": "pipelined"}
     for key, kernel in expect.items():
         s = scd.solver_for(problem(key))
         assert s.info()["kernel"] == kernel, key
@@ -317,8 +317,10 @@ def test_epoch_kernel_selection():
         s.set_option("window", 0)
         s.set_option("shared_fp64", 1)
         assert s.info()["kernel"] == kernel, key
+        s.set_option("hot", 0)
+        assert s.info()["kernel"] == "pipelined", key
         s.set_option("pipeline", 0)
-        assert s.info()["kernel"] != "pipelined", key
+        assert s.info()["kernel"] not in ("pipelined", "hot_lds"), key
         s.close()
 
 
@@ -347,6 +349,78 @@ def test_pipelined_long_segments(key, over, group):
         G, Gr = s.duality_gap(), curve[e][2]
         if Gr > 1e-6 * abs(P0):
             assert G <= 2.0 * Gr, (e, G, Gr)
+    s.close()
+
+
+# ---------------------------------------------------------------------------------- hot-set kernel
+
+HOT_CASES = {
+    # one-hot click rows: the most frequent field values are the hot set
+    "click": ("click_svm_twin", None, 0),
+    "click_fp64": ("click_svm_twin", None, 1),
+    # short columns, uniform rows: every row index fits LDS (the whole shared vector is hot)
+    "ridge_small": ("sparse_ridge", dict(n_rows=2_000, n_cols=5_000, density=0.01), 0),
+    "ridge_dual": ("click_svm_twin", "dual", 0),
+}
+
+
+def _hot_problem(case):
+    key, over, _ = HOT_CASES[case]
+    if over == "dual":
+        return synth.as_ridge_dual(problem(key))
+    return synth.make(key, **over) if over else problem(key)
+
+
+@pytest.mark.parametrize("case", sorted(HOT_CASES))
+def test_hot_set_kernel_parity(case):
+    p = _hot_problem(case)
+    E = 6
+    _, _, curve = _oracle_curve(p, 0, E)
+    s = scd.solver_for(p)
+    s.set_option("shared_fp64", HOT_CASES[case][2])
+    if s.info()["window"] > 8 or s.info()["window"] < 2:
+        s.set_option("window", 4)
+    info = s.info()
+    print(f"hot {case}: kernel {info['kernel']} window {info['window']} hot entries {info['hot_entries']} "
+          f"max segment {info['max_segment']}", flush=True)
+    assert info["kernel"] == "hot_lds" and info["hot_entries"] > 0
+    P0, _ = s.objective()
+    for e in range(E):
+        s.epochs(0, 1)
+        gm, gs, _ = s.get_state()
+        model = f64(gm)
+        assert rel_inf(f64(gs), fresh(p, model)) <= 1e-4, e
+        if p.form == "svm_dual":
+            assert model.min() >= 0.0 and model.max() <= 1.0
+        G, Gr = s.duality_gap(), curve[e][2]
+        if Gr > 1e-6 * abs(P0):
+            assert G <= 2.0 * Gr, (e, G, Gr)
+    s.close()
+
+
+def test_hot_set_selection_rules():
+    p = problem("click_svm_twin")
+    s = scd.solver_for(p)
+    n_hot = s.info()["hot_entries"]
+    assert n_hot > 0 and s.info()["kernel"] == "hot_lds"
+    t = scd.solver_for(p)  # the hot set is a deterministic function of the matrix
+    assert t.info()["hot_entries"] == n_hot
+    t.close()
+    for w, kernel in ((2, "hot_lds"), (8, "hot_lds"), (9, "pipelined"), (1, "ordered_lds"), (0, "hot_lds")):
+        s.set_option("window", w)
+        assert s.info()["kernel"] == kernel or (w == 1 and s.info()["kernel"] == "block"), w
+    s.set_option("group", 8)
+    assert s.info()["kernel"] == "pipelined"
+    s.set_option("group", 0)
+    s.set_option("hot", 0)
+    assert s.info()["kernel"] == "pipelined" and s.get_option("hot") == 0
+    s.set_option("hot", 1)
+    assert s.info()["kernel"] == "hot_lds"
+    # long segments never take it
+    q = scd.solver_for(problem("sparse_ridge_small"))
+    q.set_option("window", 4)
+    assert q.info()["kernel"] != "hot_lds"
+    q.close()
     s.close()
 
 
