@@ -1182,79 +1182,89 @@ __device__ __forceinline__ bool hot_wait(uint32_t* flag, uint32_t want, uint32_t
     }
 }
 
-template <int FORM, typename U>
+// One step's worth of a batch buffer for a consumer lane: coordinate metadata and the lane's SL
+// entries (key, value, cold value).
+template <int SL>
+struct HotStep {
+    uint32_t m, len;
+    float m_old, sn, ylab;
+    int32_t kk[SL];
+    float vv[SL], xv[SL];
+};
+
+template <int SL>
+__device__ __forceinline__ void hot_load_step(HotStep<SL>& t, const uint32_t* mb, const int32_t* key, const float* val,
+                                              const float* cold, uint32_t B, uint32_t c, uint32_t e0, bool act) {
+    t.m = mb[c];
+    t.len = act ? mb[B + c] : 0u;
+    t.m_old = __uint_as_float(mb[2u * B + c]);
+    t.sn = __uint_as_float(mb[3u * B + c]);
+    t.ylab = __uint_as_float(mb[4u * B + c]);
+#pragma unroll
+    for (int r = 0; r < SL; ++r) {
+        t.kk[r] = key[e0 + 8 * r];
+        t.vv[r] = val[e0 + 8 * r];
+        t.xv[r] = cold[e0 + 8 * r];
+    }
+}
+
+// The consumer for coordinates of at most 8 * SL entries.  Per step: read the hot values the
+// current keys point at, read the next step's metadata and entries (always, the last step
+// re-reads its own, so that the number of LDS operations is fixed and the wait for the hot values
+// never covers the prefetch), then reduce, step and scatter.  Hot entries are updated in LDS; the
+// new model value and each cold entry's update go back into the batch buffer, and the producer
+// that owns it issues the global stores and atomics before refilling it, so this wave never
+// waits on global memory.
+template <int FORM, typename U, int SL>
 __device__ __forceinline__ void hot_consumer(const HotArgs& h, U* hot, uint32_t* ready, uint32_t* freed,
                                              uint32_t* abort_flag, uint32_t* bufs, uint32_t nb, int lane) {
     const EpochArgs& a = h.e;
-    const uint32_t B = h.B, Smax = h.Smax, W = h.W, buf_words = 5u * B + 3u * B * Smax;
-    const uint32_t SL = Smax / 8;  // entries per lane (<= 8), uniform
+    const uint32_t B = h.B, Smax = h.Smax, W = h.W, buf_words = 5u * B + 3u * B * Smax, S = B / W;
     const uint32_t g = (uint32_t)lane >> 3, sub = (uint32_t)lane & 7u;
     const bool act = g < W;
     for (uint32_t b = 0; b < nb; ++b) {
         const uint32_t p = b % kHotProducers, n = b / kHotProducers;
         if (!hot_wait(ready + p, n + 1, abort_flag, h.spin_limit, h.err)) return;
-        uint32_t* const mbw = bufs + p * buf_words;
-        const uint32_t* mb = mbw;
+        uint32_t* const mb = bufs + p * buf_words;
         const int32_t* key = reinterpret_cast<const int32_t*>(mb + 5u * B);
         const float* val = reinterpret_cast<const float*>(key + B * Smax);
         float* const coldw = const_cast<float*>(val + B * Smax);
-        const float* cold = coldw;
-        for (uint32_t st = 0; st < B / W; ++st) {
-            const uint32_t c = st * W + (act ? g : 0u);
-            const uint32_t m = mb[c];  // 0xFFFFFFFF past the last position of the epoch
-            const uint32_t len = act ? mb[B + c] : 0u;
-            const float m_old = __uint_as_float(mb[2u * B + c]);
-            const float sn = __uint_as_float(mb[3u * B + c]);
-            const float ylab = __uint_as_float(mb[4u * B + c]);
+        HotStep<SL> cur;
+        uint32_t c = act ? g : 0u;
+        hot_load_step<SL>(cur, mb, key, val, coldw, B, c, c * Smax + sub, act);
+        for (uint32_t st = 0; st < S; ++st) {
             const uint32_t e0 = c * Smax + sub;
-            // All eight slices at once, with no branch around any read: a slice beyond the SL
-            // reserved for this lane re-reads slice 0 (its entries are masked out below, since
-            // sub + 8r >= Smax >= len there).  Keys, values and cold values first, then the hot
-            // values the keys point at (slot 0 stands in for a cold entry), merged by bit mask so
-            // that the compiler cannot sink a read into a per-lane branch and serialise it.
-            int32_t kk[8];
-            float vv[8], xv[8];
+            U hv[SL];
 #pragma unroll
-            for (uint32_t r = 0; r < 8; ++r) {
-                const uint32_t o = e0 + (r < SL ? 8 * r : 0u);
-                kk[r] = key[o];
-                vv[r] = val[o];
-                xv[r] = cold[o];
-            }
-            __builtin_amdgcn_sched_barrier(0);  // all reads of the step issue before any is consumed
-            U hv[8];
-#pragma unroll
-            for (uint32_t r = 0; r < 8; ++r) hv[r] = hot[kk[r] >= 0 ? kk[r] : 0];
+            for (int r = 0; r < SL; ++r) hv[r] = hot[cur.kk[r] >= 0 ? cur.kk[r] : 0];
             __builtin_amdgcn_sched_barrier(0);
-#pragma unroll
-            for (uint32_t r = 0; r < 8; ++r) {
-                const uint32_t msk = kk[r] >= 0 ? 0xFFFFFFFFu : 0u;
-                xv[r] = __uint_as_float((__float_as_uint((float)hv[r]) & msk) | (__float_as_uint(xv[r]) & ~msk));
-            }
+            const uint32_t cn = st + 1 < S ? (st + 1) * W + (act ? g : 0u) : c;
+            HotStep<SL> nxt;
+            hot_load_step<SL>(nxt, mb, key, val, coldw, B, cn, cn * Smax + sub, act);
+            __builtin_amdgcn_sched_barrier(0);
             float acc = 0.0f;
 #pragma unroll
-            for (uint32_t r = 0; r < 8; ++r)
-                if (sub + 8 * r < len) acc = fmaf(vv[r], xv[r], acc);
+            for (int r = 0; r < SL; ++r) {
+                const uint32_t msk = cur.kk[r] >= 0 ? 0xFFFFFFFFu : 0u;
+                const float x = __uint_as_float((__float_as_uint((float)hv[r]) & msk) | (__float_as_uint(cur.xv[r]) & ~msk));
+                if (sub + 8u * r < cur.len) acc = fmaf(cur.vv[r], x, acc);
+            }
             const float gsum = group_sum<8>(acc);
             float coef;
-            const float m_new = coord_step<FORM>(gsum, sn, m_old, ylab, a.k, &coef);
-            // Hot entries are updated here, in LDS.  The new model value and each cold entry's
-            // update go back into the batch buffer; the producer that owns it issues the global
-            // stores and atomics before refilling it, so this wave never waits on global memory.
-            if (act && m != 0xFFFFFFFFu) {
-                if (sub == 0) mbw[2u * B + c] = __float_as_uint(m_new);
+            const float m_new = coord_step<FORM>(gsum, cur.sn, cur.m_old, cur.ylab, a.k, &coef);
+            if (act && cur.m != 0xFFFFFFFFu) {
+                if (sub == 0) mb[2u * B + c] = __float_as_uint(m_new);
 #pragma unroll
-                for (uint32_t r = 0; r < 8; ++r) {
-                    if (sub + 8 * r < len) {
-                        const float d = coef * vv[r];
-                        if (kk[r] >= 0) {
-                            if (coef != 0.0f) atomicAdd(&hot[kk[r]], (U)d);
-                        } else {
-                            coldw[e0 + 8 * r] = d;
-                        }
+                for (int r = 0; r < SL; ++r) {
+                    if (sub + 8u * r < cur.len) {
+                        const float d = coef * cur.vv[r];
+                        coldw[e0 + 8 * r] = d;  // read back only for cold entries
+                        if (cur.kk[r] >= 0 && coef != 0.0f) atomicAdd(&hot[cur.kk[r]], (U)d);
                     }
                 }
             }
+            cur = nxt;
+            c = cn;
         }
         __hip_atomic_store(freed + p, n + 1, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_WORKGROUP);
     }
@@ -1370,9 +1380,18 @@ __global__ __launch_bounds__(64 * (1 + kHotProducers)) void k_epoch_hot(HotArgs 
     if (tid < 2 * kHotProducers + 1) ready[tid] = 0u;  // ready, freed and abort are contiguous
     __syncthreads();
     const uint32_t nb = (a.perm.n + h.B - 1) / h.B;
-    if (wave == 0)
-        hot_consumer<FORM, U>(h, hot, ready, freed, abort_flag, bufs, nb, lane);
-    else
+    if (wave == 0) {
+        switch (h.Smax / 8) {  // entries per consumer lane
+            case 1: hot_consumer<FORM, U, 1>(h, hot, ready, freed, abort_flag, bufs, nb, lane); break;
+            case 2: hot_consumer<FORM, U, 2>(h, hot, ready, freed, abort_flag, bufs, nb, lane); break;
+            case 3: hot_consumer<FORM, U, 3>(h, hot, ready, freed, abort_flag, bufs, nb, lane); break;
+            case 4: hot_consumer<FORM, U, 4>(h, hot, ready, freed, abort_flag, bufs, nb, lane); break;
+            case 5: hot_consumer<FORM, U, 5>(h, hot, ready, freed, abort_flag, bufs, nb, lane); break;
+            case 6: hot_consumer<FORM, U, 6>(h, hot, ready, freed, abort_flag, bufs, nb, lane); break;
+            case 7: hot_consumer<FORM, U, 7>(h, hot, ready, freed, abort_flag, bufs, nb, lane); break;
+            default: hot_consumer<FORM, U, 8>(h, hot, ready, freed, abort_flag, bufs, nb, lane); break;
+        }
+    } else
         hot_producer<U>(h, ready, freed, abort_flag, bufs, nb, wave - 1, lane);
     __syncthreads();
     for (uint32_t i = tid; i < h.n_hot; i += blockDim.x) uu[h.hot_ids[i]] = hot[i];
