@@ -29,6 +29,7 @@ HIPCC_FLAGS = [
     # No packed fp32 (v_pk_*_f32) in device code.
     "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
     "-Wall",
+    "-Wextra",
 ]
 
 

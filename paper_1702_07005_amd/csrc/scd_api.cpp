@@ -344,7 +344,7 @@ int hot_if_needed(scd_solver* h, hipStream_t s) {
     return build_hot_tables(h, s);
 }
 
-int check_hot_err(scd_solver* h, int v) {
+int check_hot_err(int v) {
     if (v) return fail(SCD_ERR_HIP, "hot-set epoch kernel: a wait between its waves timed out; the state is invalid");
     return SCD_OK;
 }
@@ -423,7 +423,7 @@ int reduce_state(scd_solver* h, hipStream_t s) {
     if (int r = enqueue_sums(h, s, h->host_sums)) return r;
     HIP_TRY(hipMemcpyAsync(h->err_host + kGapSlots, h->hot_err, sizeof(int), hipMemcpyDeviceToHost, s));
     HIP_TRY(hipStreamSynchronize(s));
-    return check_hot_err(h, h->err_host[kGapSlots]);
+    return check_hot_err(h->err_host[kGapSlots]);
 }
 
 void objectives_from_sums(const scd_solver* h, const double* t, double* P, double* D) {
@@ -576,7 +576,9 @@ int scd_create(const scd_matrix_t* A, const float* y, double lambda, int32_t for
         // Coupling of the coordinates (sets the default window), using h->u as the probe vector.
         const float mu = formulation == SCD_SVM_DUAL ? 0.0f : (float)(lambda * (double)h->n_rows);
         const float* sign = formulation == SCD_SVM_DUAL ? h->y : nullptr;
-        double fro2 = 0.0, coh2 = 0.0, diag2 = 0.0, diag1 = 0.0, cn = 0.0;
+        // Probe 0 (all-ones): sum of G's entries, sum of its diagonal, non-empty coordinates.
+        // Probes 1..kProbes (Rademacher): per-coordinate squared off-diagonal row mass into K = h->model.
+        double coh2 = 0.0, diag1 = 0.0, cn = 0.0;
         hip(hipMemsetAsync(h->model, 0, sizeof(float) * (size_t)h->C, s), "zero probe sums");  // K[c]
         for (uint32_t probe = 0; probe <= (uint32_t)kProbes && rc == SCD_OK; ++probe) {
             hip(launch_probe(h->ptr, h->idx, h->val, h->norms, sign, (uint32_t)h->C, h->L, mu, probe, G,
@@ -587,16 +589,13 @@ int scd_create(const scd_matrix_t* A, const float* y, double lambda, int32_t for
             if (rc != SCD_OK) break;
             if (probe == 0) {
                 coh2 = h->host_sums[0];
-                diag2 = h->host_sums[1];
                 diag1 = h->host_sums[2];
                 cn = h->host_sums[3];
-            } else {
-                fro2 += h->host_sums[0] / kProbes;  // estimate of sum_c kappa_c
             }
         }
         unsigned kmax_bits = 0;
         hip(hipMemsetAsync(h->flags, 0, sizeof(unsigned), s), "zero kappa");
-        hip(launch_kappa_max(h->model, h->norms, (uint32_t)h->C, mu, kProbes, obj_blocks(h, G),
+        hip(launch_kappa_max(h->model, h->norms, (uint32_t)h->C, kProbes, obj_blocks(h, G),
                              reinterpret_cast<unsigned*>(h->flags), s),
             "kappa max");
         hip(hipMemcpyAsync(&kmax_bits, h->flags, sizeof(unsigned), hipMemcpyDeviceToHost, s), "copy kappa");
@@ -608,8 +607,6 @@ int scd_create(const scd_matrix_t* A, const float* y, double lambda, int32_t for
             h->coherence = pairs > 0.0 ? (coh2 - diag1) / pairs : 0.0;
             // Worst coordinate's mean squared coupling to one other coordinate.
             h->coupling = cn > 1.0 ? (double)kmax / (cn - 1.0) : 0.0;
-            (void)fro2;
-            (void)diag2;
             const double budget = formulation == SCD_SVM_DUAL ? kCouplingBudgetSvm : kCouplingBudgetRidge;
             int64_t w = INT64_MAX;
             if (h->coupling > 0.0) w = 1 + (int64_t)std::min(9.0e18, std::floor(budget / h->coupling));
@@ -733,7 +730,7 @@ int scd_duality_gap_wait(scd_handle_t h, int32_t slot, double* gap, double* prim
     if (!h->slot_pending[slot]) return fail(SCD_ERR_INVALID, "slot %d holds no evaluation", slot);
     h->slot_pending[slot] = 0;
     HIP_TRY(hipEventSynchronize(h->slot_event[slot]));
-    if (int r = check_hot_err(h, h->err_host[slot])) return r;
+    if (int r = check_hot_err(h->err_host[slot])) return r;
     double P, D;
     objectives_from_sums(h, h->slot_sums + 5 * slot, &P, &D);
     if (!std::isfinite(P) || !std::isfinite(D)) return fail(SCD_ERR_NUMERIC, "non-finite objective (P=%g, D=%g)", P, D);

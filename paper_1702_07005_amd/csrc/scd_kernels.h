@@ -122,8 +122,8 @@ hipError_t launch_validate(const int64_t* ptr, uint32_t S, const int32_t* idx, c
 hipError_t launch_probe(const int64_t* ptr, const int32_t* idx, const float* val, const float* norms,
                         const float* sign, uint32_t C, int64_t L, float mu, uint32_t probe, int G, int blocks,
                         float* T, float* K, double* partials, double* out, hipStream_t s);
-hipError_t launch_kappa_max(const float* K, const float* norms, uint32_t C, float mu, int probes, int blocks,
-                            unsigned* out, hipStream_t s);
+hipError_t launch_kappa_max(const float* K, const float* norms, uint32_t C, int probes, int blocks, unsigned* out,
+                            hipStream_t s);
 hipError_t launch_objective(int form, const ObjArgs& o, int G, int blocks, double* partials, double* sums,
                             hipStream_t s);
 

@@ -834,7 +834,7 @@ __global__ __launch_bounds__(256) void k_probe_gather(const int64_t* __restrict_
 // Largest per-coordinate off-diagonal row mass kappa_c = sum_{j != c} G_cj^2, from the probe
 // sums K[c] over `probes` Rademacher probes.  Non-negative floats order like their bit patterns.
 __global__ __launch_bounds__(256) void k_kappa_max(const float* __restrict__ K, const float* __restrict__ norms,
-                                                   uint32_t C, float mu, float inv_probes, unsigned* __restrict__ out) {
+                                                   uint32_t C, float inv_probes, unsigned* __restrict__ out) {
     float best = 0.0f;
     for (uint32_t c = blockIdx.x * 256u + threadIdx.x; c < C; c += gridDim.x * 256u) {
         const float sc = norms[c];
@@ -1091,9 +1091,9 @@ hipError_t launch_probe(const int64_t* ptr, const int32_t* idx, const float* val
     return hipGetLastError();
 }
 
-hipError_t launch_kappa_max(const float* K, const float* norms, uint32_t C, float mu, int probes, int blocks,
-                            unsigned* out, hipStream_t s) {
-    hipLaunchKernelGGL(k_kappa_max, dim3(blocks), dim3(256), 0, s, K, norms, C, mu, 1.0f / (float)probes, out);
+hipError_t launch_kappa_max(const float* K, const float* norms, uint32_t C, int probes, int blocks, unsigned* out,
+                            hipStream_t s) {
+    hipLaunchKernelGGL(k_kappa_max, dim3(blocks), dim3(256), 0, s, K, norms, C, 1.0f / (float)probes, out);
     return hipGetLastError();
 }
 
