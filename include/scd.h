@@ -95,7 +95,8 @@ typedef struct {
     int64_t nnz;
     int64_t epoch;        /* global epoch counter (epochs run so far)                  */
     int64_t max_segment;  /* longest coordinate segment                                */
-    int64_t window;       /* coordinates in flight at most (persistent groups)         */
+    int64_t window;       /* coordinates in flight at most (whose updates other
+                             coordinates may not see yet)                               */
     double lambda;
     double coupling;      /* largest over coordinates c of sum_{j != c} G_cj^2 / (C - 1), G the
                              step-normalised Gram matrix of the coordinates (estimated at
@@ -196,6 +197,10 @@ int scd_set_state(scd_handle_t h, const float *model_dev, const float *shared_de
  *                 reads the others ahead of their coordinates; 0 = never.  The hot set is chosen
  *                 (a pass over the matrix, synchronising) when this first applies: at create, or
  *                 when "window" or "hot" is set.
+ *   "hot_wait_limit"  test hook: sleeps (about 64 cycles each) one wait between the waves of the
+ *                 hot-set kernel may take before the waves give up; the next synchronising call
+ *                 then returns SCD_ERR_HIP and the state stays invalid until scd_set_state.
+ *                 0 (default) = 2^24.
  *   "shared_fp64" 1 = store the shared vector in fp64 (fp64 atomic adds), 0 = fp32.  Chosen at
  *                 create: fp64 when some entry receives more than 28,000 atomic adds per epoch,
  *                 where fp32 accumulation would drift by more than about 1e-5 of its magnitude.

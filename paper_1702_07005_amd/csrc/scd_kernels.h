@@ -43,6 +43,8 @@ struct EpochArgs {
     uint32_t u_bytes;    // byte size of the shared vector when below 2^31 (raw-buffer range), else 0
     double* sink;        // pipelined kernel, fp64 shared vector: 256 slots per workgroup that
                          // inactive lanes add 0 to
+    uint32_t drain;      // pipelined kernel: wait for the group's own atomics before its next gathers
+    uint32_t pad2_;
 };
 
 enum { PLAN_GROUP = 0, PLAN_BLOCK = 1, PLAN_ORDERED_LDS = 2, PLAN_MIXED = 3, PLAN_PIPE = 4, PLAN_HOT = 5 };
@@ -56,6 +58,7 @@ struct LaunchPlan {
     uint32_t L;      // shared-vector length (PLAN_ORDERED_LDS)
     uint32_t long_len;  // PLAN_MIXED: segments longer than this go to the whole workgroup
     int tail;           // PLAN_GROUP: some segment is longer than the register slices
+    int drain;          // PLAN_PIPE: the window binds, so each group lets its scatter land before it gathers again
     int wide;           // shared vector stored as double
     size_t lds_bytes;
 };

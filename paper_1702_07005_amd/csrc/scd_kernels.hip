@@ -313,9 +313,12 @@ __device__ __forceinline__ void buf_atomic_add(const SharedBuf<U>& b, uint32_t i
 // and `nxt` the next one's metadata (both loaded one step earlier).  Issue order:
 //   gathers(cur), segment(nxt) -> ni/nv, metadata two positions ahead -> nn,
 //   [wait for the gathers] reduce + step + model store, atomics(cur).
-// The loads consumed by the next step are all issued before this step's atomics, and the
-// gathers of the next step are issued right after them, so a group's critical path per
-// coordinate is one gather round trip (the scatter's completion overlaps it).
+// The loads consumed by the next step are all issued before this step's atomics.  Without
+// `drain`, the next gathers follow the atomics at once: one gather round trip per coordinate,
+// but a group then has two coordinates in flight (the previous one's scatter may not have
+// landed).  With `drain` (the window binds) the group waits for its atomics first: two round
+// trips per coordinate, against three for the plain kernels, whose segment and metadata
+// loads are not prefetched.
 template <int G>
 __device__ __forceinline__ float pipe_reduce(float acc, float (*part)[G > 64 ? G / 64 : 1], int& buf) {
     if constexpr (G <= 64) {
@@ -363,6 +366,9 @@ __device__ __forceinline__ bool pipe_step(const EpochArgs& a, const SharedBuf<U>
                                           const CoordMeta& cur, const int (&ci)[R], const float (&cv)[R],
                                           const CoordMeta& nxt, int (&ni)[R], float (&nv)[R], CoordMeta& nn,
                                           float (*part)[G > 64 ? G / 64 : 1], int& buf) {
+    // When the window binds, the previous coordinate's atomics (the wave's latest operations) must
+    // land before this coordinate gathers, so that a group never has two coordinates in flight.
+    if (a.drain) __builtin_amdgcn_s_waitcnt(0x0F70);  // vmcnt(0)
     const int64_t len = cur.s1 - cur.s0;
     if (len > (int64_t)G * R) {
         pipe_long<FORM, G, R, FRESH, U>(a, ub, lane, j, cur, nxt, ni, nv, nn, part, buf);

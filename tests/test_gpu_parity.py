@@ -424,6 +424,47 @@ def test_hot_set_selection_rules():
     s.close()
 
 
+def test_hot_set_wait_timeout_is_reported_and_recoverable():
+    # A one-sleep limit makes the consumer give up at its first wait (the producers need global
+    # loads before the first batch is ready); every wave still leaves the kernel normally.
+    p = problem("click_svm_twin")
+    s = scd.solver_for(p)
+    assert s.info()["kernel"] == "hot_lds"
+    s.set_option("hot_wait_limit", 1)
+    s.epochs(0, 1)
+    with pytest.raises(scd.ScdError, match="timed out"):
+        s.duality_gap()
+    s.duality_gap_async(0)
+    with pytest.raises(scd.ScdError, match="timed out"):
+        s.duality_gap_wait(0)
+    # A written state replaces the invalid one; with the default limit the epochs run normally.
+    s.set_option("hot_wait_limit", 0)
+    s.set_state(torch.zeros(p.C, device=DEV), torch.zeros(p.L, device=DEV), 0)
+    s.epochs(0, 2)
+    gm, gs, _ = s.get_state()
+    assert rel_inf(f64(gs), fresh(p, f64(gm))) <= 1e-4
+    assert s.duality_gap() > 0.0
+    s.close()
+
+
+def test_two_solvers_on_two_streams():
+    pa, pb = problem("sparse_ridge_small"), problem("click_svm_twin")
+    a = scd.solver_for(pa)
+    b = scd.solver_for(pb)
+    torch.cuda.synchronize()
+    sa, sb = torch.cuda.Stream(), torch.cuda.Stream()  # default priority
+    for _ in range(3):
+        a.epochs(0, 1, stream=sa)
+        b.epochs(0, 1, stream=sb)
+    torch.cuda.synchronize()
+    for s, p, st in ((a, pa, sa), (b, pb, sb)):
+        gm, gs, ep = s.get_state(stream=st)
+        st.synchronize()
+        assert ep == 3
+        assert rel_inf(f64(gs), fresh(p, f64(gm))) <= 1e-4
+        s.close()
+
+
 @pytest.mark.parametrize("window", [2, 7, 64, 1000])
 def test_windowed_epochs(window):
     p = problem("sparse_ridge_small")
