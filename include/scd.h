@@ -112,7 +112,9 @@ typedef struct {
                              1 one workgroup per coordinate, 2 ordered with the shared
                              vector in LDS, 3 lane groups with long segments handed to the
                              workgroup, 4 software-pipelined, 5 hot set in LDS (one
-                             workgroup, at most 8 coordinates in flight)               */
+                             workgroup, at most 8 coordinates in flight), 6 one workgroup
+                             per coordinate taking positions from a queue (skewed
+                             segment lengths)                                           */
     int32_t hot_entries;  /* shared-vector entries the hot-set kernel keeps in LDS
                              (0 until it is first needed)                               */
 } scd_info_t;
@@ -190,7 +192,12 @@ int scd_set_state(scd_handle_t h, const float *model_dev, const float *shared_de
  *                 caches), 0 = plain loads.
  *   "pipeline"    1 (default) = use the software-pipelined epoch kernel where it applies
  *                 (shared vector below 2 GiB; with skewed segment lengths only when each
- *                 in-flight coordinate can have a workgroup of its own), 0 = the plain kernels.
+ *                 in-flight coordinate can have a workgroup of its own, then with workgroups
+ *                 taking positions from a queue), 0 = the plain kernels.
+ *   "queue_chunk" consecutive permutation positions each workgroup of the queued kernel claims
+ *                 at a time: 0 (default) = 1 per 64 coordinates in flight (at least 1), else
+ *                 1..64.  Larger chunks lower the claim rate on the queue's counter and let
+ *                 coordinates start further from their permutation positions.
  *   "hot"         1 (default) = with at most 8 coordinates in flight, segments of at most 64
  *                 entries and "group" 0, run the epoch in one workgroup that keeps the most-updated
  *                 shared-vector entries in LDS (their gathers and adds never leave the CU) and

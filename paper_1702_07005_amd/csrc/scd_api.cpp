@@ -118,7 +118,9 @@ struct scd_solver {
     int64_t group = 0;
     int64_t fresh = 0;
     int64_t pipeline = 1;
+    int64_t queue_chunk = 0;  // option: positions per queue claim, 0 = by window
     double* sink = nullptr;  // pipelined kernel, fp64 shared vector: slots inactive lanes add 0 to
+    uint32_t* queue = nullptr;  // queued kernel: next position, workgroups finished (zero between launches)
     // Hot-set kernel (windows of at most kHotMaxWindow): built on first need.
     int64_t hot = 1;              // option
     int hot_built = 0;
@@ -240,18 +242,28 @@ int plan_epoch(const scd_solver* h, LaunchPlan* lp, uint32_t* n_groups) {
     const bool skewed = h->max_seg > long_len;
     if (pipe_ok && skewed && h->group == 0 && groups <= cap_blocks) {
         // Few coordinates in flight and skewed lengths: each in-flight coordinate gets a workgroup
-        // of its own, so a long segment is streamed by 256 lanes without holding up others.  Only
-        // half the window is kept in flight (half the groups, each draining): the long (hot)
-        // segments couple strongly with each other, and with a full window of them in flight the
-        // per-epoch gap exceeded twice the sequential algorithm's in one run in ten on the scaled
-        // text-ridge workload (half: never in 30).  The plain kernel for this case serialises long
+        // of its own, so a long segment is streamed by 256 lanes without holding up others, and
+        // the workgroups take positions from a queue, so that those that draw long segments do
+        // not fall behind the permutation order.  The plain kernel for this case serialises long
         // segments inside a workgroup instead.
-        const int64_t half = std::max<int64_t>(1, groups / 2);
-        lp->kind = PLAN_PIPE;
+        // A segment beyond the register slices is streamed in blocks and stays between its
+        // gather and its scatter for several block round trips, not one: such coordinates (the
+        // densest columns, which couple most strongly with each other) overlap more of the
+        // others.  With every column fitting the slices the default window kept the per-epoch gap
+        // within 1.06x of the sequential algorithm's (30 runs, text-ridge 3,500 x 166,000); at
+        // full size (columns of up to 350,000 entries) the same rule went past 2x in 5 runs of 12,
+        // half of it in none.
+        if (h->window == 0 && h->max_seg > (int64_t)kBlockThreads * kQueueSlices)
+            groups = std::max<int64_t>(1, groups / 2);
+        lp->kind = PLAN_QUEUE;
         lp->drain = 1;
+        // One counter serves about 8e7 claims per second; a workgroup claims about once per
+        // 2-4 us, so every 64 workgroups share one claim per step.
+        lp->chunk = (int)(h->queue_chunk ? h->queue_chunk
+                                         : std::min<int64_t>(kQueueChunkMax, std::max<int64_t>(1, groups / 64)));
         lp->group = kBlockThreads;
-        lp->blocks = (int)half;
-        *n_groups = (uint32_t)half;
+        lp->blocks = (int)groups;
+        *n_groups = (uint32_t)groups;
         return SCD_OK;
     }
     lp->kind = skewed ? PLAN_MIXED : PLAN_GROUP;
@@ -404,6 +416,7 @@ void release(scd_solver* h) {
     (void)hipFree(h->partials);
     (void)hipFree(h->sums);
     (void)hipFree(h->sink);
+    (void)hipFree(h->queue);
     (void)hipFree(h->slot_of);
     (void)hipFree(h->hot_ids);
     (void)hipFree(h->hot_err);
@@ -550,6 +563,8 @@ int scd_create(const scd_matrix_t* A, const float* y, double lambda, int32_t for
         const size_t sink_bytes = sizeof(double) * 256 * (size_t)h->cus * kBlocksPerCU;
         hip(hipMalloc(&h->sink, sink_bytes), "hipMalloc(sink)");
         hip(hipMemsetAsync(h->sink, 0, sink_bytes, s), "zero sink");
+        hip(hipMalloc(&h->queue, 2 * sizeof(uint32_t)), "hipMalloc(queue)");
+        hip(hipMemsetAsync(h->queue, 0, 2 * sizeof(uint32_t), s), "zero queue");
     }
     hip(hipHostMalloc(&h->host_sums, sizeof(double) * 8, hipHostMallocDefault), "hipHostMalloc");
     hip(hipHostMalloc(&h->slot_sums, sizeof(double) * 5 * kGapSlots, hipHostMallocDefault), "hipHostMalloc(slots)");
@@ -687,6 +702,8 @@ int scd_epochs(scd_handle_t h, uint64_t seed, int32_t n_epochs, void* stream) {
     a.u_bytes = shared_bytes(h) <= kPipeMaxBytes ? (uint32_t)shared_bytes(h) : 0u;
     a.sink = h->sink;
     a.drain = (uint32_t)lp.drain;
+    a.queue = h->queue;
+    a.chunk = (uint32_t)std::max(1, lp.chunk);
     hipStream_t s = (hipStream_t)stream;
     for (int32_t e = 0; e < n_epochs; ++e) {
         a.perm = make_perm(seed, (uint64_t)h->epoch, (uint32_t)h->C);
@@ -821,6 +838,9 @@ int scd_set_option(scd_handle_t h, const char* key, int64_t value) {
     } else if (!strcmp(key, "pipeline")) {
         if (value != 0 && value != 1) return fail(SCD_ERR_INVALID, "pipeline must be 0 or 1");
         h->pipeline = value;
+    } else if (!strcmp(key, "queue_chunk")) {
+        if (value < 0 || value > (int64_t)kQueueChunkMax) return fail(SCD_ERR_INVALID, "queue_chunk must be in [0, 64]");
+        h->queue_chunk = value;
     } else if (!strcmp(key, "shared_fp64")) {
         if (value != 0 && value != 1) return fail(SCD_ERR_INVALID, "shared_fp64 must be 0 or 1");
         if (value == h->wide) return SCD_OK;
@@ -853,6 +873,7 @@ int scd_get_option(scd_handle_t h, const char* key, int64_t* value) {
     else if (!strcmp(key, "group")) *value = h->group;
     else if (!strcmp(key, "fresh_reads")) *value = h->fresh;
     else if (!strcmp(key, "pipeline")) *value = h->pipeline;
+    else if (!strcmp(key, "queue_chunk")) *value = h->queue_chunk;
     else if (!strcmp(key, "hot")) *value = h->hot;
     else if (!strcmp(key, "hot_wait_limit")) *value = h->hot_wait_limit;
     else if (!strcmp(key, "shared_fp64")) *value = h->wide;
@@ -867,7 +888,8 @@ int scd_get_info(scd_handle_t h, scd_info_t* info) {
     uint32_t n_groups = 1;
     plan_epoch(h, &lp, &n_groups);
     info->formulation = h->form;
-    info->group_lanes = (lp.kind == PLAN_GROUP || lp.kind == PLAN_MIXED || lp.kind == PLAN_PIPE || lp.kind == PLAN_HOT)
+    info->group_lanes = (lp.kind == PLAN_GROUP || lp.kind == PLAN_MIXED || lp.kind == PLAN_PIPE || lp.kind == PLAN_HOT ||
+                         lp.kind == PLAN_QUEUE)
                             ? lp.group
                         : lp.kind == PLAN_BLOCK && !lp.ordered ? kBlockThreads : 1024;
     info->kernel = lp.kind;

@@ -44,10 +44,15 @@ struct EpochArgs {
     double* sink;        // pipelined kernel, fp64 shared vector: 256 slots per workgroup that
                          // inactive lanes add 0 to
     uint32_t drain;      // pipelined kernel: wait for the group's own atomics before its next gathers
-    uint32_t pad2_;
+    uint32_t chunk;      // queued kernel: consecutive positions per claim (1..kQueueChunkMax)
+    uint32_t* queue;     // queued kernel: [0] next permutation position, [1] workgroups finished (both 0
+                         // between launches)
 };
 
-enum { PLAN_GROUP = 0, PLAN_BLOCK = 1, PLAN_ORDERED_LDS = 2, PLAN_MIXED = 3, PLAN_PIPE = 4, PLAN_HOT = 5 };
+constexpr uint32_t kQueueChunkMax = 64;
+constexpr int kQueueSlices = 16;  // register slices per lane of the queued kernel (256 x 16 entries held)
+
+enum { PLAN_GROUP = 0, PLAN_BLOCK = 1, PLAN_ORDERED_LDS = 2, PLAN_MIXED = 3, PLAN_PIPE = 4, PLAN_HOT = 5, PLAN_QUEUE = 6 };
 
 struct LaunchPlan {
     int kind;        // PLAN_*
@@ -59,6 +64,7 @@ struct LaunchPlan {
     uint32_t long_len;  // PLAN_MIXED: segments longer than this go to the whole workgroup
     int tail;           // PLAN_GROUP: some segment is longer than the register slices
     int drain;          // PLAN_PIPE: the window binds, so each group lets its scatter land before it gathers again
+    int chunk;          // PLAN_QUEUE: consecutive permutation positions per claim
     int wide;           // shared vector stored as double
     size_t lds_bytes;
 };

@@ -309,6 +309,59 @@ __device__ __forceinline__ void buf_atomic_add(const SharedBuf<U>& b, uint32_t i
     }
 }
 
+// A segment longer than the register slices, streamed in blocks of G * kLongBlock entries:
+// each lane loads kLongBlock indices and values, then issues kLongBlock gathers (or atomics),
+// so a block costs one or two memory round trips instead of one per entry.  Segments that
+// cover most of the shared vector otherwise stay between their gather and their scatter for
+// milliseconds, long enough to overlap others they couple strongly with.  Lanes past the end
+// re-read entry s0 and are masked by an out-of-range shared-vector offset.
+constexpr int kLongBlock = 16;
+
+template <int G, bool FRESH, typename U>
+__device__ __forceinline__ float long_dot(const EpochArgs& a, const SharedBuf<U>& ub, int lane, int64_t s0,
+                                          int64_t s1) {
+    float acc = 0.0f;
+    for (int64_t b = s0; b < s1; b += (int64_t)G * kLongBlock) {
+        int ix[kLongBlock];
+        float vx[kLongBlock];
+        bool in[kLongBlock];
+#pragma unroll
+        for (int r = 0; r < kLongBlock; ++r) {
+            const int64_t k = b + lane + (int64_t)r * G;
+            in[r] = k < s1;
+            const int64_t kk = in[r] ? k : s0;
+            ix[r] = a.idx[kk];
+            vx[r] = a.val[kk];
+        }
+        float gv[kLongBlock];
+#pragma unroll
+        for (int r = 0; r < kLongBlock; ++r) gv[r] = buf_load<FRESH>(ub, (uint32_t)ix[r], in[r]);
+#pragma unroll
+        for (int r = 0; r < kLongBlock; ++r) acc = fmaf(vx[r], gv[r], acc);
+    }
+    return acc;
+}
+
+template <int G, typename U>
+__device__ __forceinline__ void long_scatter(const EpochArgs& a, const SharedBuf<U>& ub, int lane, int64_t s0,
+                                             int64_t s1, float coef) {
+    for (int64_t b = s0; b < s1; b += (int64_t)G * kLongBlock) {
+        int ix[kLongBlock];
+        float vx[kLongBlock];
+        bool in[kLongBlock];
+#pragma unroll
+        for (int r = 0; r < kLongBlock; ++r) {
+            const int64_t k = b + lane + (int64_t)r * G;
+            in[r] = k < s1;
+            const int64_t kk = in[r] ? k : s0;
+            ix[r] = a.idx[kk];
+            vx[r] = a.val[kk];
+        }
+#pragma unroll
+        for (int r = 0; r < kLongBlock; ++r) buf_atomic_add(ub, (uint32_t)ix[r], in[r], coef * vx[r]);
+    }
+}
+
 // One coordinate of k_epoch_pipe.  On entry `ci/cv` hold the current coordinate's segment
 // and `nxt` the next one's metadata (both loaded one step earlier).  Issue order:
 //   gathers(cur), segment(nxt) -> ni/nv, metadata two positions ahead -> nn,
@@ -337,7 +390,7 @@ __device__ __forceinline__ float pipe_reduce(float acc, float (*part)[G > 64 ? G
 }
 
 // A segment longer than the register slices (rare; skewed lengths): stream it twice, gather
-// then scatter, with ordinary waits.  It ends by issuing the same operations, in the same
+// then scatter, in blocks (long_dot, long_scatter) with ordinary waits.  It ends by issuing the same operations, in the same
 // order, as the end of the pipelined step (next segment, metadata two ahead, then 1 + R
 // operations standing in for the model store and the atomics), so that the compiler's wait
 // counts after the step stay exact on both paths.
@@ -345,14 +398,11 @@ template <int FORM, int G, int R, bool FRESH, typename U>
 __device__ __forceinline__ void pipe_long(const EpochArgs& a, const SharedBuf<U>& ub, int lane, uint32_t j,
                                        const CoordMeta& cur, const CoordMeta& nxt, int (&ni)[R], float (&nv)[R],
                                        CoordMeta& nn, float (*part)[G > 64 ? G / 64 : 1], int& buf) {
-    float acc = 0.0f;
-    for (int64_t k = cur.s0 + lane; k < cur.s1; k += G) acc = fmaf(a.val[k], buf_load<FRESH>(ub, (uint32_t)a.idx[k], true), acc);
-    const float g = pipe_reduce<G>(acc, part, buf);
+    const float g = pipe_reduce<G>(long_dot<G, FRESH>(a, ub, lane, cur.s0, cur.s1), part, buf);
     float coef;
     const float m_new = coord_step<FORM>(g, cur.sn, cur.m_old, cur.ylab, a.k, &coef);
     a.model[cur.m] = m_new;
-    if (coef != 0.0f)
-        for (int64_t k = cur.s0 + lane; k < cur.s1; k += G) buf_atomic_add(ub, (uint32_t)a.idx[k], true, coef * a.val[k]);
+    if (coef != 0.0f) long_scatter<G>(a, ub, lane, cur.s0, cur.s1, coef);
     const uint64_t P = a.n_groups, n = a.perm.n;
     load_seg_raw<G, R>(a, nxt, lane, ni, nv);
     const uint64_t j2 = (uint64_t)j + 2 * P;
@@ -438,6 +488,157 @@ __global__ __launch_bounds__(256) void k_epoch_pipe(EpochArgs a) {
         j += P;
         cA = cA2;
         cB = cB2;
+    }
+}
+
+// ----------------------------------------------------------------------------------------
+// Epoch kernel with a position queue: one workgroup per coordinate, draining, and positions
+// claimed in permutation order from a counter (queue[0]) instead of taken at a fixed stride.
+// With a fixed stride, a workgroup that draws long segments falls behind the others; on
+// skewed lengths the processing order then drifts by thousands of positions from the
+// permutation, and the iterates follow a different sequence than the sequential algorithm
+// on the same permutation (by as much as a different permutation would).  With the queue a
+// coordinate starts within a few windows of its position.
+//
+// A claim takes `chunk` consecutive positions (one atomic add of `chunk`): one counter
+// serves about 8e7 returning atomics per second, so wide windows claim several positions at
+// a time.  Chunk c of a workgroup covers its steps [c*chunk, (c+1)*chunk); it is claimed in
+// step c*chunk - kQueueLead with one returning atomic issued with the prefetch loads.  Every
+// step issues that atomic through a raw buffer whose range holds only queue[0]: lane 0 at
+// offset 0 when the step claims, every other lane (and lane 0 in other steps) out of range,
+// which makes no access.  There is no branch, so the compiler's count of the operations issued
+// after the gathers stays exact.  The claim lands by the next step's drain; lane 0 writes it to
+// an LDS ring before that step's reduction barrier, and every wave reads it after the barrier,
+// when it loads the metadata of the chunk's first coordinate two steps ahead.  No wait or
+// barrier is added.  Each workgroup counts itself out in queue[1]; the last one resets both
+// words for the next launch.
+// ----------------------------------------------------------------------------------------
+constexpr int kQueueRing = 4;  // chunk bases held in LDS (chunk number mod 4)
+constexpr int kQueueLead = 4;  // steps between a claim and the first step of its chunk
+
+// Position of step `k` of this workgroup (>= n once the queue is exhausted).
+__device__ __forceinline__ uint32_t queue_pos(const uint32_t* ring, uint32_t k, uint32_t chunk) {
+    return ring[(k / chunk) % kQueueRing] + k % chunk;
+}
+
+// One coordinate of k_epoch_queue (step k of this workgroup).  `cur` and its segment `ci/cv`,
+// and `nxt`'s metadata were loaded one step earlier.  Loads `nxt`'s segment into `ni/nv` and
+// the metadata of the coordinate two steps ahead into `nn`; returns that coordinate's position
+// (>= n when the queue is exhausted; `nn` then describes a valid stand-in coordinate).
+template <int FORM, int R, bool FRESH, typename U>
+__device__ __forceinline__ uint32_t queue_step(const EpochArgs& a, const SharedBuf<U>& ub,
+                                               const __amdgpu_buffer_rsrc_t& qr, int lane, uint32_t k,
+                                               const CoordMeta& cur, const int (&ci)[R], const float (&cv)[R],
+                                               const CoordMeta& nxt, int (&ni)[R], float (&nv)[R], CoordMeta& nn,
+                                               uint32_t* ring, uint32_t& claim, float (*part)[4], int& buf) {
+    constexpr int G = 256;
+    const uint32_t K = a.chunk;
+    __builtin_amdgcn_s_waitcnt(0x0F70);  // vmcnt(0): this workgroup's atomics and its last claim have landed
+    // The previous step claimed chunk (k - 1 + kQueueLead) / K if it began one.
+    if (lane == 0 && k > 0 && (k - 1 + kQueueLead) % K == 0) ring[((k - 1 + kQueueLead) / K) % kQueueRing] = claim;
+    const uint32_t n = a.perm.n;
+    const uint32_t p2 = queue_pos(ring, k + 2, K);  // its chunk was published before the previous barrier
+    const uint32_t m2 = p2 < n ? perm_at(p2, a.perm) : cur.m;
+    const int qoff = lane == 0 && (k + kQueueLead) % K == 0 ? 0 : 4;
+    const int64_t len = cur.s1 - cur.s0;
+    if (len > (int64_t)G * R) {
+        // Longer than the register slices: stream the segment twice (gather, then scatter).
+        const float g = pipe_reduce<G>(long_dot<G, FRESH>(a, ub, lane, cur.s0, cur.s1), part, buf);
+        float coef;
+        const float m_new = coord_step<FORM>(g, cur.sn, cur.m_old, cur.ylab, a.k, &coef);
+        a.model[cur.m] = m_new;
+        if (coef != 0.0f) long_scatter<G>(a, ub, lane, cur.s0, cur.s1, coef);
+        load_seg_raw<G, R>(a, nxt, lane, ni, nv);
+        nn = load_meta_of(a, m2);
+        claim = (uint32_t)__builtin_amdgcn_raw_ptr_buffer_atomic_add_i32((int)K, qr, qoff, 0, 0);
+    } else {
+        float gv[R];
+#pragma unroll
+        for (int r = 0; r < R; ++r) gv[r] = buf_load<FRESH>(ub, (uint32_t)ci[r], (int64_t)(lane + r * G) < len);
+        __builtin_amdgcn_sched_barrier(0);
+        load_seg_raw<G, R>(a, nxt, lane, ni, nv);
+        nn = load_meta_of(a, m2);
+        claim = (uint32_t)__builtin_amdgcn_raw_ptr_buffer_atomic_add_i32((int)K, qr, qoff, 0, 0);
+        __builtin_amdgcn_sched_barrier(0);
+        float acc = 0.0f;
+#pragma unroll
+        for (int r = 0; r < R; ++r) acc = fmaf(cv[r], gv[r], acc);
+        const float g = pipe_reduce<G>(acc, part, buf);
+        float coef;
+        const float m_new = coord_step<FORM>(g, cur.sn, cur.m_old, cur.ylab, a.k, &coef);
+        a.model[cur.m] = m_new;  // every lane stores the same value
+        const bool moves = coef != 0.0f;
+#pragma unroll
+        for (int r = 0; r < R; ++r)
+            buf_atomic_add(ub, (uint32_t)ci[r], moves && (int64_t)(lane + r * G) < len, coef * cv[r]);
+    }
+    return p2;
+}
+
+template <int FORM, int R, bool FRESH, typename U>
+__global__ __launch_bounds__(256) void k_epoch_queue(EpochArgs a) {
+    constexpr int G = 256;
+    __shared__ float part[2][G / 64];
+    __shared__ uint32_t ring[kQueueRing];
+    const int lane = threadIdx.x;
+    const uint32_t n = a.perm.n;
+    const uint32_t K = a.chunk;
+    // word 3 = 0x00020000: 32-bit data format, the gfx9-family raw-buffer setting.
+    const __amdgpu_buffer_rsrc_t qr = __builtin_amdgcn_make_buffer_rsrc(a.queue, (short)0, 4, 0x00020000);
+    // The chunks that cover steps [0, kQueueLead): the steps' own claims start with the next one.
+    const uint32_t first = (kQueueLead + K - 1) / K;  // 1..kQueueLead
+    uint32_t c[kQueueLead];
+#pragma unroll
+    for (int i = 0; i < kQueueLead; ++i)
+        c[i] = (uint32_t)__builtin_amdgcn_raw_ptr_buffer_atomic_add_i32((int)K, qr, lane == 0 && (uint32_t)i < first ? 0 : 4,
+                                                                         0, 0);
+    if (lane == 0) {
+        // Claims of one lane on one address are performed in order; sort anyway.
+#pragma unroll
+        for (int i = 1; i < kQueueLead; ++i)
+#pragma unroll
+            for (int t = kQueueLead - 1; t >= i; --t)
+                if ((uint32_t)t < first && c[t] < c[t - 1]) {
+                    const uint32_t x = c[t];
+                    c[t] = c[t - 1];
+                    c[t - 1] = x;
+                }
+#pragma unroll
+        for (int i = 0; i < kQueueLead; ++i)
+            if ((uint32_t)i < first) ring[i % kQueueRing] = c[i];
+    }
+    __syncthreads();
+    uint32_t pA = queue_pos(ring, 0, K), pB = queue_pos(ring, 1, K);
+    if (pA < n) {
+        const SharedBuf<U> ub =
+            shared_buf<U>(a.u, a.u_bytes, reinterpret_cast<U*>(a.sink) + (size_t)blockIdx.x * 256 + threadIdx.x);
+        int buf = 0;
+        uint32_t claim = 0, k = 0;
+        CoordMeta cA = load_meta_of(a, perm_at(pA, a.perm));
+        int ciA[R], ciB[R];
+        float cvA[R], cvB[R];
+        load_seg_raw<G, R>(a, cA, lane, ciA, cvA);
+        CoordMeta cB = load_meta_of(a, pB < n ? perm_at(pB, a.perm) : cA.m);
+        for (;;) {
+            CoordMeta cA2, cB2;
+            const uint32_t pA2 = queue_step<FORM, R, FRESH>(a, ub, qr, lane, k++, cA, ciA, cvA, cB, ciB, cvB, cA2,
+                                                            ring, claim, part, buf);
+            if (pB >= n) break;
+            const uint32_t pB2 = queue_step<FORM, R, FRESH>(a, ub, qr, lane, k++, cB, ciB, cvB, cA2, ciA, cvA, cB2,
+                                                            ring, claim, part, buf);
+            if (pA2 >= n) break;
+            cA = cA2;
+            cB = cB2;
+            pB = pB2;
+        }
+    }
+    if (lane == 0) {
+        __builtin_amdgcn_s_waitcnt(0x0F70);  // every claim of this workgroup has been performed
+        const uint32_t done = __hip_atomic_fetch_add(a.queue + 1, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        if (done == gridDim.x - 1) {  // the others have finished claiming: reset for the next launch
+            __hip_atomic_store(a.queue, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            __hip_atomic_store(a.queue + 1, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        }
     }
 }
 
@@ -898,6 +1099,12 @@ static hipError_t launch_pipe(const EpochArgs& a, int blocks, hipStream_t s) {
     return hipGetLastError();
 }
 
+template <int FORM, bool FRESH, typename U>
+static hipError_t launch_queue(const EpochArgs& a, int blocks, hipStream_t s) {
+    hipLaunchKernelGGL((k_epoch_queue<FORM, kQueueSlices, FRESH, U>), dim3(blocks), dim3(256), 0, s, a);
+    return hipGetLastError();
+}
+
 template <int FORM, int G, bool FRESH, typename U>
 static hipError_t launch_mixed(const EpochArgs& a, int blocks, uint32_t long_len, hipStream_t s) {
     constexpr int R = slice_depth(G);
@@ -945,6 +1152,8 @@ static hipError_t launch_epoch_typed(const EpochArgs& a, const LaunchPlan& lp, h
     }
     if (lp.kind == PLAN_PIPE)
         return lp.fresh ? launch_pipe_by_width<FORM, true, U>(a, lp, s) : launch_pipe_by_width<FORM, false, U>(a, lp, s);
+    if (lp.kind == PLAN_QUEUE)
+        return lp.fresh ? launch_queue<FORM, true, U>(a, lp.blocks, s) : launch_queue<FORM, false, U>(a, lp.blocks, s);
     if (lp.kind == PLAN_BLOCK) {
         if (lp.ordered)
             hipLaunchKernelGGL((k_epoch_block<FORM, 256, 16, true, true, U>), dim3(lp.blocks), dim3(256), 0, s, a);

@@ -300,9 +300,9 @@ def test_every_group_width_keeps_invariant(group, fresh_reads, pipeline):
 
 def test_epoch_kernel_selection():
     # every segment within the register slices -> pipelined kernel (fp32 or fp64 shared vector);
-    # long segments -> the mixed kernel; window 1 -> ordered.
+    # skewed lengths, small window -> queued (mixed without pipelining); window 1 -> ordered.
     expect = {"dense_ridge": "pipelined", "sparse_ridge_small": "pipelined", "text_svm_twin": "pipelined",
-              "click_svm_twin": "hot_lds", "text_ridge_twin": "pipelined"}
+              "click_svm_twin": "hot_lds", "text_ridge_twin": "queued"}
     for key, kernel in expect.items():
         s = scd.solver_for(problem(key))
         assert s.info()["kernel"] == kernel, key
@@ -318,19 +318,19 @@ def test_epoch_kernel_selection():
         s.set_option("shared_fp64", 1)
         assert s.info()["kernel"] == kernel, key
         s.set_option("hot", 0)
-        assert s.info()["kernel"] == "pipelined", key
+        assert s.info()["kernel"] == ("queued" if kernel == "queued" else "pipelined"), key
         s.set_option("pipeline", 0)
-        assert s.info()["kernel"] not in ("pipelined", "hot_lds"), key
+        assert s.info()["kernel"] not in ("pipelined", "hot_lds", "queued"), key
         s.close()
 
 
-@pytest.mark.parametrize("key,over,group", [
+@pytest.mark.parametrize("key,over,group,kernel", [
     # every column 160-320 entries with 16-lane groups (10 slices each): all take the long path
-    ("sparse_ridge", dict(n_rows=2_000, n_cols=500, density=0.09), 16),
+    ("sparse_ridge", dict(n_rows=2_000, n_cols=500, density=0.09), 16, "pipelined"),
     # one workgroup per column; the hottest columns exceed 256 x 16 entries
-    ("text_ridge_csc", dict(n_rows=6_000, n_cols=166_000, row_nnz=370), 0),
+    ("text_ridge_csc", dict(n_rows=6_000, n_cols=166_000, row_nnz=370), 0, "queued"),
 ])
-def test_pipelined_long_segments(key, over, group):
+def test_pipelined_long_segments(key, over, group, kernel):
     p = synth.make(key, **over)
     E = 6
     _, _, curve = _oracle_curve(p, 0, E)
@@ -340,7 +340,7 @@ def test_pipelined_long_segments(key, over, group):
     held = info["group_lanes"] * (16 if info["group_lanes"] == 256 else 10)
     print(f"long segments {key}: kernel {info['kernel']} lanes {info['group_lanes']} max {info['max_segment']}",
           flush=True)
-    assert info["kernel"] == "pipelined" and info["max_segment"] > held
+    assert info["kernel"] == kernel and info["max_segment"] > held
     P0, _ = s.objective()
     for e in range(E):
         s.epochs(0, 1)
@@ -349,6 +349,88 @@ def test_pipelined_long_segments(key, over, group):
         G, Gr = s.duality_gap(), curve[e][2]
         if Gr > 1e-6 * abs(P0):
             assert G <= 2.0 * Gr, (e, G, Gr)
+    s.close()
+
+
+# ---------------------------------------------------------------------------------- queued kernel
+
+QUEUE_CASES = {
+    # (problem, size overrides, window, shared_fp64, positions per claim)
+    # skewed column lengths (Zipf features), default window
+    "text_ridge": ("text_ridge_twin", None, 0, 0, 0),
+    "text_ridge_fp64": ("text_ridge_twin", None, 0, 1, 0),
+    "text_ridge_chunk3": ("text_ridge_twin", None, 0, 0, 3),
+    # few workgroups, each holding four claimed positions
+    "text_ridge_w3": ("text_ridge_twin", None, 3, 0, 0),
+    # weak coupling (lambda N >> |a_c|^2): 300 workgroups claim 4 positions each at the start,
+    # more than the 1,000 coordinates
+    "small_first_claims": ("text_ridge_csc", dict(n_rows=2_000, n_cols=1_000, row_nnz=60, lam=1.0), 300, 0, 4),
+    # chunks longer than the window
+    "small_w2_chunk5": ("text_ridge_csc", dict(n_rows=2_000, n_cols=1_000, row_nnz=60), 2, 0, 5),
+}
+
+
+def _queue_problem(case):
+    key, over = QUEUE_CASES[case][:2]
+    return synth.make(key, **over) if over else problem(key)
+
+
+@pytest.mark.parametrize("case", sorted(QUEUE_CASES))
+def test_queued_kernel_parity(case):
+    p = _queue_problem(case)
+    _, _, window, wide, chunk = QUEUE_CASES[case]
+    E = 6
+    _, _, curve = _oracle_curve(p, 0, E)
+    s = scd.solver_for(p)
+    s.set_option("shared_fp64", wide)
+    s.set_option("window", window)
+    s.set_option("queue_chunk", chunk)
+    info = s.info()
+    print(f"queued {case}: kernel {info['kernel']} window {info['window']} max segment {info['max_segment']}",
+          flush=True)
+    assert info["kernel"] == "queued" and info["group_lanes"] == 256
+    assert info["window"] == (window or info["auto_window"])
+    P0, _ = s.objective()
+    nonempty = np.diff(p.ptr) > 0
+    prev = np.zeros(p.C)
+    for e in range(E):
+        s.epochs(0, 1)
+        gm, gs, _ = s.get_state()
+        model = f64(gm)
+        assert rel_inf(f64(gs), fresh(p, model)) <= 1e-4, e
+        if e < 2:  # every launch walks the whole permutation (the queue starts from 0 each time)
+            assert np.mean(model[nonempty] != prev[nonempty]) > 0.99, e
+        prev = model
+        G, Gr = s.duality_gap(), curve[e][2]
+        if Gr > 1e-6 * abs(P0):
+            assert G <= 2.0 * Gr, (e, G, Gr)
+    s.close()
+
+
+def test_queued_window_with_long_segments():
+    # columns beyond the register slices (256 x 16 entries): the default keeps half the window in
+    # flight; an explicit window is taken as given
+    p = synth.make("text_ridge_csc", n_rows=6_000, n_cols=166_000, row_nnz=370)
+    s = scd.solver_for(p)
+    info = s.info()
+    assert info["max_segment"] > 256 * 16 and info["kernel"] == "queued"
+    assert info["window"] == max(1, info["auto_window"] // 2)
+    s.set_option("window", 40)
+    assert s.info()["window"] == 40
+    s.close()
+    t = scd.solver_for(problem("text_ridge_twin"))  # every column within the slices: the whole window
+    assert t.info()["max_segment"] <= 256 * 16 and t.info()["window"] == t.info()["auto_window"]
+    t.close()
+
+
+def test_queue_chunk_option():
+    s = scd.solver_for(problem("text_ridge_twin"))
+    assert s.get_option("queue_chunk") == 0
+    for bad in (-1, 65):
+        with pytest.raises(scd.ScdError):
+            s.set_option("queue_chunk", bad)
+    s.set_option("queue_chunk", 64)
+    assert s.get_option("queue_chunk") == 64 and s.info()["kernel"] == "queued"
     s.close()
 
 
