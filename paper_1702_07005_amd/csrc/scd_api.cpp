@@ -124,7 +124,7 @@ struct scd_solver {
     // Hot-set kernel (windows of at most kHotMaxWindow): built on first need.
     int64_t hot = 1;              // option
     int hot_built = 0;
-    uint16_t* slot_of = nullptr;  // [L]
+    uint16_t* slot_entry = nullptr;  // [nnz]: hot slot of each stored entry's index (kHotCold: not hot)
     int32_t* hot_ids = nullptr;   // [n_hot]
     uint32_t n_hot = 0;
     double hot_cover = 0.0;       // fraction of stored entries that point at a hot entry
@@ -308,6 +308,8 @@ int build_hot_tables(scd_solver* h, hipStream_t s) {
     unsigned* hits = nullptr;
     unsigned long long* dev2 = nullptr;
     unsigned* blocks = nullptr;
+    uint16_t* slot_of = nullptr;  // [L]: slot of each shared-vector entry, kHotCold when not hot
+    bool skip = false;
     const int64_t nblk = (h->L + kHotAssignBlock - 1) / kHotAssignBlock;
     int rc = SCD_OK;
     auto hip = [&](hipError_t e, const char* what) {
@@ -345,11 +347,24 @@ int build_hot_tables(scd_solver* h, hipStream_t s) {
         }
         hip(hipMemcpyAsync(blocks, base.data(), sizeof(unsigned) * (size_t)nblk, hipMemcpyHostToDevice, s),
             "copy block bases");
-        hip(hipMalloc(&h->slot_of, sizeof(uint16_t) * (size_t)h->L), "hipMalloc(slot_of)");
+        hip(hipMalloc(&slot_of, sizeof(uint16_t) * (size_t)h->L), "hipMalloc(slot_of)");
         hip(hipMalloc(&h->hot_ids, sizeof(int32_t) * (size_t)cnt), "hipMalloc(hot_ids)");
-        hip(launch_hot_assign(hits, h->L, lo, blocks, h->slot_of, h->hot_ids, s), "hot slots");
-        hip(hipStreamSynchronize(s), "synchronize");
+        hip(launch_hot_assign(hits, h->L, lo, blocks, slot_of, h->hot_ids, s), "hot slots");
+        // Each stored entry's slot, read by the producers beside idx (2 bytes per entry).  Without
+        // the memory for it the hot-set kernel is not used.
         if (rc == SCD_OK) {
+            const hipError_t e = hipMalloc(&h->slot_entry, sizeof(uint16_t) * (size_t)h->nnz);
+            if (e == hipErrorOutOfMemory) {
+                (void)hipGetLastError();
+                h->slot_entry = nullptr;
+                skip = true;
+            } else {
+                hip(e, "hipMalloc(slot_entry)");
+            }
+        }
+        if (rc == SCD_OK && !skip) hip(launch_hot_entry_slots(h->idx, h->nnz, slot_of, h->slot_entry, s), "entry slots");
+        hip(hipStreamSynchronize(s), "synchronize");
+        if (rc == SCD_OK && !skip) {
             h->n_hot = (uint32_t)cnt;
             h->hot_cover = (double)sum / (double)h->nnz;
         }
@@ -357,10 +372,11 @@ int build_hot_tables(scd_solver* h, hipStream_t s) {
     (void)hipFree(hits);
     (void)hipFree(dev2);
     (void)hipFree(blocks);
-    if (rc != SCD_OK) {
-        (void)hipFree(h->slot_of);
+    (void)hipFree(slot_of);
+    if (rc != SCD_OK || skip) {
+        (void)hipFree(h->slot_entry);
         (void)hipFree(h->hot_ids);
-        h->slot_of = nullptr;
+        h->slot_entry = nullptr;
         h->hot_ids = nullptr;
         h->n_hot = 0;
     }
@@ -417,7 +433,7 @@ void release(scd_solver* h) {
     (void)hipFree(h->sums);
     (void)hipFree(h->sink);
     (void)hipFree(h->queue);
-    (void)hipFree(h->slot_of);
+    (void)hipFree(h->slot_entry);
     (void)hipFree(h->hot_ids);
     (void)hipFree(h->hot_err);
     (void)hipHostFree(h->err_host);
@@ -710,7 +726,7 @@ int scd_epochs(scd_handle_t h, uint64_t seed, int32_t n_epochs, void* stream) {
         if (lp.kind == PLAN_HOT) {
             HotArgs ha{};
             ha.e = a;
-            ha.slot_of = h->slot_of;
+            ha.slot_entry = h->slot_entry;
             ha.hot_ids = h->hot_ids;
             ha.n_hot = h->n_hot;
             ha.W = hg.W;

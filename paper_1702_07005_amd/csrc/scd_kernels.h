@@ -95,7 +95,8 @@ constexpr uint16_t kHotCold = 0xFFFF;    // slot_of value of an entry that is no
 
 struct HotArgs {
     EpochArgs e;
-    const uint16_t* slot_of;  // [L]: LDS slot of a hot shared-vector entry, kHotCold otherwise
+    const uint16_t* slot_entry;  // [nnz]: LDS slot of each stored entry's shared-vector index, kHotCold
+                                 // when that entry is not hot (read with idx, so no random lookup)
     const int32_t* hot_ids;   // [n_hot]: shared-vector index of each slot
     uint32_t n_hot;
     uint32_t W;               // coordinates in flight (<= kHotMaxWindow)
@@ -121,6 +122,8 @@ hipError_t launch_convert_f32_to_f64(const float* in, int64_t n, double* out, hi
 hipError_t launch_convert_f64_to_f32(const double* in, int64_t n, float* out, hipStream_t s);
 hipError_t launch_max_hits(const int32_t* idx, int64_t nnz, int64_t L, unsigned* hits, unsigned* out, hipStream_t s);
 hipError_t launch_count_hits(const int32_t* idx, int64_t nnz, unsigned* hits, hipStream_t s);
+hipError_t launch_hot_entry_slots(const int32_t* idx, int64_t nnz, const uint16_t* slot_of, uint16_t* slot_entry,
+                                  hipStream_t s);
 hipError_t launch_perm_fill(const PermKeys& p, int32_t* out, hipStream_t s);
 hipError_t launch_gather_dots(const int64_t* ptr, const int32_t* idx, const float* val, const float* u, uint32_t C,
                               int G, int blocks, float* out, hipStream_t s);

@@ -1539,10 +1539,11 @@ __device__ __forceinline__ void hot_producer(const HotArgs& h, uint32_t* ready, 
             mb[3u * B + lane] = __float_as_uint(sn);
             mb[4u * B + lane] = __float_as_uint(ylab);
         }
-        // Entries, three stages of unconditional loads (entry 0 stands in for unused slots):
-        // index and value, hot slot, current value of the shared vector.
+        // Entries, two stages of unconditional loads (entry 0 stands in for unused slots): index,
+        // value and hot slot, then the current value of the shared vector.
         int32_t ix[NE];
         float vv[NE];
+        uint32_t sl[NE];
         bool in[NE];
         uint32_t c = c0, k = k0;
 #pragma unroll
@@ -1554,6 +1555,7 @@ __device__ __forceinline__ void hot_producer(const HotArgs& h, uint32_t* ready, 
             const int64_t kk = in[t] ? sc + k : 0;
             ix[t] = a.idx[kk];
             vv[t] = a.val[kk];
+            sl[t] = h.slot_entry[kk];
             c += dc;
             k += dk;
             if (k >= Smax) {
@@ -1561,9 +1563,6 @@ __device__ __forceinline__ void hot_producer(const HotArgs& h, uint32_t* ready, 
                 ++c;
             }
         }
-        uint32_t sl[NE];
-#pragma unroll
-        for (int t = 0; t < NE; ++t) sl[t] = h.slot_of[ix[t]];
         float cv[NE];
 #pragma unroll
         for (int t = 0; t < NE; ++t) cv[t] = (float)uu[ix[t]];
@@ -1731,6 +1730,21 @@ hipError_t launch_hot_count_ge(const unsigned* hits, int64_t L, unsigned T, unsi
 hipError_t launch_hot_block_count(const unsigned* hits, int64_t L, unsigned T, unsigned* block_counts, hipStream_t s) {
     const int64_t nb = (L + kHotAssignBlock - 1) / kHotAssignBlock;
     hipLaunchKernelGGL(k_hot_block_count, dim3((unsigned)nb), dim3(256), 0, s, hits, L, T, block_counts);
+    return hipGetLastError();
+}
+
+__global__ __launch_bounds__(256) void k_hot_entry_slots(const int32_t* __restrict__ idx, int64_t nnz,
+                                                         const uint16_t* __restrict__ slot_of,
+                                                         uint16_t* __restrict__ slot_entry) {
+    for (int64_t k = (int64_t)blockIdx.x * 256 + threadIdx.x; k < nnz; k += (int64_t)gridDim.x * 256)
+        slot_entry[k] = slot_of[idx[k]];
+}
+
+hipError_t launch_hot_entry_slots(const int32_t* idx, int64_t nnz, const uint16_t* slot_of, uint16_t* slot_entry,
+                                  hipStream_t s) {
+    const int64_t want = (nnz + 255) / 256;
+    const unsigned blocks = (unsigned)(want < 1 ? 1 : want > 65536 ? 65536 : want);
+    hipLaunchKernelGGL(k_hot_entry_slots, dim3(blocks), dim3(256), 0, s, idx, nnz, slot_of, slot_entry);
     return hipGetLastError();
 }
 
