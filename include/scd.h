@@ -167,9 +167,12 @@ int scd_duality_gap_wait(scd_handle_t h, int32_t slot, double *gap, double *prim
 /* Copy the state out (device buffers, may be NULL to skip), exactly as the solver holds it:
  *   model_dev:  float32[n_coords]   (beta, or alpha)
  *   shared_dev: float32[shared_len] (w = A beta, or w(alpha), or wbar = A^T alpha)
- *   epoch:      host int64 (may be NULL).  Enqueues only.  A state copied out and written
- *   back with scd_set_state resumes bit-exactly when the shared vector is stored in fp32
- *   (option "shared_fp64" = 0); an fp64 shared vector is exchanged rounded to fp32. */
+ *   epoch:      host int64 (may be NULL).  Enqueues only, so it reports no error of the
+ *   epochs before it: a hot-set epoch whose waits timed out (see "hot_wait_limit") leaves a
+ *   partial state that this call copies as is; the next synchronising call returns the error.
+ *   A state copied out and written back with scd_set_state resumes bit-exactly when the shared
+ *   vector is stored in fp32 (option "shared_fp64" = 0); an fp64 shared vector is exchanged
+ *   rounded to fp32. */
 int scd_get_state(scd_handle_t h, float *model_dev, float *shared_dev, int64_t *epoch, void *stream);
 
 /* Overwrite the state (resume from a checkpoint).  model_dev/shared_dev in the layout of
