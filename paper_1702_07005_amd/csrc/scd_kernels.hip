@@ -1062,21 +1062,34 @@ __global__ __launch_bounds__(256) void k_sumsq(const float* __restrict__ T, int6
 }
 
 // Sum `nparts` rows of `width` doubles in index order (one workgroup; deterministic).
+// Sums `width` (at most kSumWidthMax) columns of `partials` [nparts][width] in one workgroup, in an
+// order fixed by nparts alone (so the result does not depend on timing): thread t adds rows t,
+// t + 256, ... in turn, each wave combines its lanes by an xor butterfly, and thread 0 adds the
+// four wave sums in wave order.
+constexpr int kSumWidthMax = 8;
+
 __global__ __launch_bounds__(256) void k_sum_partials(const double* __restrict__ partials, int nparts, int width,
                                                       double* __restrict__ out) {
-    __shared__ double sh[256];
-    for (int w = 0; w < width; ++w) {
-        double x = 0.0;
-        for (int p = threadIdx.x; p < nparts; p += 256) x += partials[(size_t)p * width + w];
-        sh[threadIdx.x] = x;
-        __syncthreads();
-        for (int s = 128; s > 0; s >>= 1) {
-            if ((int)threadIdx.x < s) sh[threadIdx.x] += sh[threadIdx.x + s];
-            __syncthreads();
-        }
-        if (threadIdx.x == 0) out[w] = sh[0];
-        __syncthreads();
+    __shared__ double sh[4][kSumWidthMax];
+    double x[kSumWidthMax];
+#pragma unroll
+    for (int w = 0; w < kSumWidthMax; ++w) x[w] = 0.0;
+    for (int p = threadIdx.x; p < nparts; p += 256) {
+#pragma unroll
+        for (int w = 0; w < kSumWidthMax; ++w)
+            if (w < width) x[w] += partials[(size_t)p * width + w];
     }
+#pragma unroll
+    for (int w = 0; w < kSumWidthMax; ++w)
+        for (int o = 32; o > 0; o >>= 1) x[w] += __shfl_xor(x[w], o, 64);
+    const int wave = threadIdx.x >> 6;
+    if ((threadIdx.x & 63) == 0) {
+#pragma unroll
+        for (int w = 0; w < kSumWidthMax; ++w) sh[wave][w] = x[w];
+    }
+    __syncthreads();
+    if (threadIdx.x == 0)
+        for (int w = 0; w < width; ++w) out[w] = ((sh[0][w] + sh[1][w]) + sh[2][w]) + sh[3][w];
 }
 
 // ----------------------------------------------------------------------------------------
