@@ -178,6 +178,17 @@ int pipe_drain(const scd_solver* h, int64_t window, int64_t groups) {
     return window > 0 && window < h->C && 2 * groups > window ? 1 : 0;
 }
 
+// The coupling budget was set with the plain kernels, whose coordinates spend part of each step
+// outside the gather-to-scatter interval.  A draining pipelined group keeps its coordinate in that
+// interval for nearly the whole step, so at the same window more coordinates are really between
+// gather and scatter.  With the automatic window such plans keep 4/5 of it in flight: at full
+// text-SVM size (41 -> 32) the worst per-epoch gap ratio to the sequential algorithm over 24 runs
+// fell from 2.06 to 1.81.
+int64_t pipe_groups(const scd_solver* h, int64_t window, int64_t groups) {
+    if (h->window != 0 || !pipe_drain(h, window, groups)) return groups;
+    return std::max<int64_t>(1, groups * 4 / 5);
+}
+
 bool hot_plan(const scd_solver* h, int64_t window, HotGeom* g) {
     return h->hot && h->group == 0 && h->hot_built && h->n_hot > 0 && h->hot_cover >= kHotMinCover &&
            hot_geometry(h, window, g) && g->lds <= h->max_lds;
@@ -224,6 +235,7 @@ int plan_epoch(const scd_solver* h, LaunchPlan* lp, uint32_t* n_groups) {
         if (window > 0 && window < groups) groups = window;
         if (groups > h->C) groups = h->C;
         if (groups < 1) groups = 1;
+        if (pipe_ok) groups = pipe_groups(h, window, groups);
         lp->kind = pipe_ok ? PLAN_PIPE : PLAN_BLOCK;
         lp->drain = pipe_ok ? pipe_drain(h, window, groups) : 0;
         lp->group = kBlockThreads;
@@ -270,6 +282,7 @@ int plan_epoch(const scd_solver* h, LaunchPlan* lp, uint32_t* n_groups) {
     lp->long_len = (uint32_t)long_len;
     lp->tail = h->max_seg > (int64_t)G * slice_depth(G);
     if (!skewed && pipe_ok) {
+        groups = pipe_groups(h, window, groups);
         lp->kind = PLAN_PIPE;  // segments beyond the slices take its long path
         lp->drain = pipe_drain(h, window, groups);
     }
