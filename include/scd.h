@@ -37,6 +37,9 @@
  *   - Streams: `stream` is a hipStream_t (NULL = the null stream).  Calls that only
  *     enqueue work return immediately; calls that return values to the host synchronise
  *     the stream.  A handle is not thread-safe; separate handles on separate streams are.
+ *     The work of one handle must be ordered: enqueue it on one stream, or order the streams
+ *     with events.  Its epochs share scratch (the queued kernel's position counter, the gap
+ *     evaluation slots), so two epochs of one handle running at once process coordinates twice.
  *   - Faults inside kernels surface as SCD_ERR_HIP at the next synchronising call.
  */
 #ifndef SCD_H
