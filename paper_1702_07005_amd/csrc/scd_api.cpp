@@ -1,5 +1,6 @@
 // scd_api.cpp -- the C ABI of include/scd.h: handle lifecycle, validation, launch planning,
-// objectives and state.  All compute runs in the HIP kernels of scd_kernels.hip.
+// objectives and state.  All compute runs in the HIP kernels of scd_epoch.hip, scd_hot.hip and
+// scd_setup.hip.
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
