@@ -431,6 +431,25 @@ def test_queued_kernel_parity(case):
     s.close()
 
 
+def test_queued_kernel_fresh_reads():
+    # device-scope gathers (option fresh_reads) in the queued kernel
+    p = problem("text_ridge_twin")
+    E = 4
+    _, _, curve = _oracle_curve(p, 0, E)
+    s = scd.solver_for(p)
+    s.set_option("fresh_reads", 1)
+    assert s.info()["kernel"] == "queued"
+    P0, _ = s.objective()
+    for e in range(E):
+        s.epochs(0, 1)
+        gm, gs, _ = s.get_state()
+        assert rel_inf(f64(gs), fresh(p, f64(gm))) <= 1e-4, e
+        G, Gr = s.duality_gap(), curve[e][2]
+        if Gr > 1e-6 * abs(P0):
+            assert G <= 2.0 * Gr, (e, G, Gr)
+    s.close()
+
+
 def test_queued_window_with_long_segments():
     # columns beyond the register slices (256 x 16 entries): the default keeps half the window in
     # flight; an explicit window is taken as given
@@ -467,6 +486,8 @@ HOT_CASES = {
     # short columns, uniform rows: every row index fits LDS (the whole shared vector is hot)
     "ridge_small": ("sparse_ridge", dict(n_rows=2_000, n_cols=5_000, density=0.01), 0),
     "ridge_dual": ("click_svm_twin", "dual", 0),
+    # one case per consumer specialisation (entries per consumer lane = row length / 8, rounded up)
+    **{f"width_{n}": ("click_svm", dict(n_rows=20_000, n_cols=30_000, row_nnz=n), 0) for n in (5, 12, 30, 45, 52, 60)},
 }
 
 
