@@ -26,7 +26,8 @@ namespace scd {
 // (spin_limit sleeps), after which the wave sets *err and all waves leave.
 // ----------------------------------------------------------------------------------------
 size_t hot_lds_bytes(uint32_t hot_bytes, uint32_t B, uint32_t Smax) {
-    return (size_t)hot_bytes + 64 + (size_t)kHotProducers * (5u * B + 3u * B * Smax) * sizeof(uint32_t);
+    return (size_t)hot_bytes + kHotFlagBytes + kHotScratchBytes +
+           (size_t)kHotProducers * (5u * B + 3u * B * Smax) * sizeof(uint32_t);
 }
 
 __device__ __forceinline__ bool hot_wait(uint32_t* flag, uint32_t want, uint32_t* abort_flag, uint32_t limit,
@@ -70,20 +71,61 @@ __device__ __forceinline__ void hot_load_step(HotStep<SL>& t, const uint32_t* mb
     }
 }
 
-// The consumer for coordinates of at most 8 * SL entries.  Per step: read the hot values the
-// current keys point at, read the next step's metadata and entries (always, the last step
-// re-reads its own, so that the number of LDS operations is fixed and the wait for the hot values
-// never covers the prefetch), then reduce, step and scatter.  Hot entries are updated in LDS; the
-// new model value and each cold entry's update go back into the batch buffer, and the producer
-// that owns it issues the global stores and atomics before refilling it, so this wave never
-// waits on global memory.
+// One step of the consumer: W coordinates, 8 lanes each.  Reads the hot values the keys of `cur`
+// point at, then the metadata and entries of the next step into `nxt` (the last step of a batch
+// re-reads its own), then reduces, steps and scatters.  The plain LDS writes are issued by every
+// lane (an inactive group writes into its own slots of `scr`), so only the hot-entry atomics sit
+// behind a branch: a coordinate whose step is zero (in the SVM dual, most of them once their alpha
+// sits at a bound) issues none.
+template <int FORM, typename U, int SL>
+__device__ __forceinline__ void hot_step(const EpochArgs& a, U* hot, uint32_t* mb, const int32_t* key,
+                                         const float* val, float* coldw, float* scr, uint32_t B,
+                                         uint32_t Smax, uint32_t cn, bool act, uint32_t sub, int lane,
+                                         const HotStep<SL>& cur, uint32_t c, HotStep<SL>& nxt) {
+    U hv[SL];
+#pragma unroll
+    for (int r = 0; r < SL; ++r) hv[r] = hot[cur.kk[r] >= 0 ? cur.kk[r] : 0];
+    __builtin_amdgcn_sched_barrier(0);
+    hot_load_step<SL>(nxt, mb, key, val, coldw, B, cn, cn * Smax + sub, act);
+    __builtin_amdgcn_sched_barrier(0);
+    float acc = 0.0f;
+#pragma unroll
+    for (int r = 0; r < SL; ++r) {
+        // Padding entries have value 0; a cold entry's value came with it.
+        const float x = cur.kk[r] >= 0 ? (float)hv[r] : cur.xv[r];
+        acc = fmaf(cur.vv[r], x, acc);
+    }
+    const float gsum = group_sum<8>(acc);
+    float coef;
+    const float m_new = coord_step<FORM>(gsum, cur.sn, cur.m_old, cur.ylab, a.k, &coef);
+    // The model value and the updates go into this coordinate's batch slots (an empty position at
+    // the end of the epoch has m = EMPTY and zero values, which the flush skips).
+    const uint32_t e0 = c * Smax + sub;
+    uint32_t* const mw = act ? mb + 2u * B + c : reinterpret_cast<uint32_t*>(scr + lane);
+    *mw = __float_as_uint(m_new);
+#pragma unroll
+    for (int r = 0; r < SL; ++r) {
+        const float d = coef * cur.vv[r];
+        float* const cw = act ? coldw + e0 + 8 * r : scr + lane;
+        *cw = d;  // read back only for cold entries
+        if (act && cur.kk[r] >= 0 && sub + 8u * r < cur.len && coef != 0.0f) atomicAdd(hot + cur.kk[r], (U)d);
+    }
+}
+
+// The consumer for coordinates of at most 8 * SL entries: the steps of each batch, unrolled twice
+// so that the two step records alternate instead of being copied (a copy would wait for the
+// prefetch).  Hot entries are updated in LDS; the new model value and each cold entry's update go
+// back into the batch buffer, and the producer that owns it issues the global stores and atomics
+// before refilling it, so this wave never waits on global memory.
 template <int FORM, typename U, int SL>
 __device__ __forceinline__ void hot_consumer(const HotArgs& h, U* hot, uint32_t* ready, uint32_t* freed,
-                                             uint32_t* abort_flag, uint32_t* bufs, uint32_t nb, int lane) {
+                                             uint32_t* abort_flag, uint32_t* bufs, float* scr, uint32_t nb,
+                                             int lane) {
     const EpochArgs& a = h.e;
     const uint32_t B = h.B, Smax = h.Smax, W = h.W, buf_words = 5u * B + 3u * B * Smax, S = B / W;
     const uint32_t g = (uint32_t)lane >> 3, sub = (uint32_t)lane & 7u;
     const bool act = g < W;
+    const uint32_t g0 = act ? g : 0u;  // inactive lanes read coordinate 0 of each step and write nothing
     for (uint32_t b = 0; b < nb; ++b) {
         const uint32_t p = b % kHotProducers, n = b / kHotProducers;
         if (!hot_wait(ready + p, n + 1, abort_flag, h.spin_limit, h.err)) return;
@@ -91,42 +133,18 @@ __device__ __forceinline__ void hot_consumer(const HotArgs& h, U* hot, uint32_t*
         const int32_t* key = reinterpret_cast<const int32_t*>(mb + 5u * B);
         const float* val = reinterpret_cast<const float*>(key + B * Smax);
         float* const coldw = const_cast<float*>(val + B * Smax);
-        HotStep<SL> cur;
-        uint32_t c = act ? g : 0u;
-        hot_load_step<SL>(cur, mb, key, val, coldw, B, c, c * Smax + sub, act);
-        for (uint32_t st = 0; st < S; ++st) {
-            const uint32_t e0 = c * Smax + sub;
-            U hv[SL];
-#pragma unroll
-            for (int r = 0; r < SL; ++r) hv[r] = hot[cur.kk[r] >= 0 ? cur.kk[r] : 0];
-            __builtin_amdgcn_sched_barrier(0);
-            const uint32_t cn = st + 1 < S ? (st + 1) * W + (act ? g : 0u) : c;
-            HotStep<SL> nxt;
-            hot_load_step<SL>(nxt, mb, key, val, coldw, B, cn, cn * Smax + sub, act);
-            __builtin_amdgcn_sched_barrier(0);
-            float acc = 0.0f;
-#pragma unroll
-            for (int r = 0; r < SL; ++r) {
-                const uint32_t msk = cur.kk[r] >= 0 ? 0xFFFFFFFFu : 0u;
-                const float x = __uint_as_float((__float_as_uint((float)hv[r]) & msk) | (__float_as_uint(cur.xv[r]) & ~msk));
-                if (sub + 8u * r < cur.len) acc = fmaf(cur.vv[r], x, acc);
-            }
-            const float gsum = group_sum<8>(acc);
-            float coef;
-            const float m_new = coord_step<FORM>(gsum, cur.sn, cur.m_old, cur.ylab, a.k, &coef);
-            if (act && cur.m != 0xFFFFFFFFu) {
-                if (sub == 0) mb[2u * B + c] = __float_as_uint(m_new);
-#pragma unroll
-                for (int r = 0; r < SL; ++r) {
-                    if (sub + 8u * r < cur.len) {
-                        const float d = coef * cur.vv[r];
-                        coldw[e0 + 8 * r] = d;  // read back only for cold entries
-                        if (cur.kk[r] >= 0 && coef != 0.0f) atomicAdd(&hot[cur.kk[r]], (U)d);
-                    }
-                }
-            }
-            cur = nxt;
-            c = cn;
+        HotStep<SL> sa, sb;
+        hot_load_step<SL>(sa, mb, key, val, coldw, B, g0, g0 * Smax + sub, act);
+        uint32_t st = 0;
+        for (; st + 1 < S; st += 2) {
+            const uint32_t c0 = st * W + g0, c1 = c0 + W;
+            const uint32_t c2 = st + 2 < S ? c1 + W : c1;
+            hot_step<FORM, U, SL>(a, hot, mb, key, val, coldw, scr, B, Smax, c1, act, sub, lane, sa, c0, sb);
+            hot_step<FORM, U, SL>(a, hot, mb, key, val, coldw, scr, B, Smax, c2, act, sub, lane, sb, c1, sa);
+        }
+        if (st < S) {
+            const uint32_t c0 = st * W + g0;
+            hot_step<FORM, U, SL>(a, hot, mb, key, val, coldw, scr, B, Smax, c0, act, sub, lane, sa, c0, sb);
         }
         __hip_atomic_store(freed + p, n + 1, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_WORKGROUP);
     }
@@ -234,7 +252,9 @@ __global__ __launch_bounds__(64 * (1 + kHotProducers)) void k_epoch_hot(HotArgs 
     uint32_t* const ready = reinterpret_cast<uint32_t*>(hot_lds + h.hot_bytes);
     uint32_t* const freed = ready + kHotProducers;
     uint32_t* const abort_flag = freed + kHotProducers;
-    uint32_t* const bufs = reinterpret_cast<uint32_t*>(hot_lds + h.hot_bytes + 64);
+    float* const scr = reinterpret_cast<float*>(hot_lds + h.hot_bytes + kHotFlagBytes);  // 64 floats
+    uint32_t* const bufs = reinterpret_cast<uint32_t*>(hot_lds + h.hot_bytes + kHotFlagBytes + kHotScratchBytes);
+    static_assert((2 * kHotProducers + 1) * sizeof(uint32_t) <= kHotFlagBytes, "handover words exceed their area");
     U* const uu = static_cast<U*>(a.u);
     const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
     for (uint32_t i = tid; i < h.n_hot; i += blockDim.x) hot[i] = uu[h.hot_ids[i]];
@@ -243,14 +263,14 @@ __global__ __launch_bounds__(64 * (1 + kHotProducers)) void k_epoch_hot(HotArgs 
     const uint32_t nb = (a.perm.n + h.B - 1) / h.B;
     if (wave == 0) {
         switch (h.Smax / 8) {  // entries per consumer lane
-            case 1: hot_consumer<FORM, U, 1>(h, hot, ready, freed, abort_flag, bufs, nb, lane); break;
-            case 2: hot_consumer<FORM, U, 2>(h, hot, ready, freed, abort_flag, bufs, nb, lane); break;
-            case 3: hot_consumer<FORM, U, 3>(h, hot, ready, freed, abort_flag, bufs, nb, lane); break;
-            case 4: hot_consumer<FORM, U, 4>(h, hot, ready, freed, abort_flag, bufs, nb, lane); break;
-            case 5: hot_consumer<FORM, U, 5>(h, hot, ready, freed, abort_flag, bufs, nb, lane); break;
-            case 6: hot_consumer<FORM, U, 6>(h, hot, ready, freed, abort_flag, bufs, nb, lane); break;
-            case 7: hot_consumer<FORM, U, 7>(h, hot, ready, freed, abort_flag, bufs, nb, lane); break;
-            default: hot_consumer<FORM, U, 8>(h, hot, ready, freed, abort_flag, bufs, nb, lane); break;
+            case 1: hot_consumer<FORM, U, 1>(h, hot, ready, freed, abort_flag, bufs, scr, nb, lane); break;
+            case 2: hot_consumer<FORM, U, 2>(h, hot, ready, freed, abort_flag, bufs, scr, nb, lane); break;
+            case 3: hot_consumer<FORM, U, 3>(h, hot, ready, freed, abort_flag, bufs, scr, nb, lane); break;
+            case 4: hot_consumer<FORM, U, 4>(h, hot, ready, freed, abort_flag, bufs, scr, nb, lane); break;
+            case 5: hot_consumer<FORM, U, 5>(h, hot, ready, freed, abort_flag, bufs, scr, nb, lane); break;
+            case 6: hot_consumer<FORM, U, 6>(h, hot, ready, freed, abort_flag, bufs, scr, nb, lane); break;
+            case 7: hot_consumer<FORM, U, 7>(h, hot, ready, freed, abort_flag, bufs, scr, nb, lane); break;
+            default: hot_consumer<FORM, U, 8>(h, hot, ready, freed, abort_flag, bufs, scr, nb, lane); break;
         }
     } else
         hot_producer<U>(h, ready, freed, abort_flag, bufs, nb, wave - 1, lane);

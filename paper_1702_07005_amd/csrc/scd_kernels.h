@@ -87,8 +87,10 @@ struct ObjArgs {
 // Hot-set epoch (one workgroup): the n_hot most-updated shared-vector entries live in LDS for the
 // epoch; one consumer wave runs the W in-flight coordinates from LDS only, kHotProducers waves stream
 // the next batches (segment, hot slot or cold value) into LDS buffers.
-constexpr int kHotProducers = 4;
-constexpr int kHotEntriesPerLane = 24;  // producer lanes x this >= batch entries (64 x 24 = 1536)
+constexpr int kHotProducers = 8;
+constexpr int kHotEntriesPerLane = 12;  // producer lanes x this >= batch entries (64 x 12 = 768)
+constexpr int kHotFlagBytes = 128;      // LDS handover words: ready[producer], freed[producer], abort
+constexpr int kHotScratchBytes = 64 * 4;  // write targets of the consumer's inactive lanes
 constexpr int kHotMaxWindow = 8;         // consumer wave: W groups of 8 lanes
 constexpr int kHotMaxSegment = 64;
 constexpr uint16_t kHotCold = 0xFFFF;    // slot_of value of an entry that is not hot
