@@ -191,8 +191,9 @@ int64_t pipe_groups(const scd_solver* h, int64_t window, int64_t groups) {
 }
 
 bool hot_plan(const scd_solver* h, int64_t window, HotGeom* g) {
+    // Its producers read cold values through a raw buffer over the shared vector (below 2 GiB).
     return h->hot && h->group == 0 && h->hot_built && h->n_hot > 0 && h->hot_cover >= kHotMinCover &&
-           hot_geometry(h, window, g) && g->lds <= h->max_lds;
+           shared_bytes(h) <= kPipeMaxBytes && hot_geometry(h, window, g) && g->lds <= h->max_lds;
 }
 
 int plan_epoch(const scd_solver* h, LaunchPlan* lp, uint32_t* n_groups) {

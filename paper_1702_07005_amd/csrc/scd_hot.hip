@@ -27,7 +27,7 @@ namespace scd {
 // ----------------------------------------------------------------------------------------
 size_t hot_lds_bytes(uint32_t hot_bytes, uint32_t B, uint32_t Smax) {
     return (size_t)hot_bytes + kHotFlagBytes + kHotScratchBytes +
-           (size_t)kHotProducers * (5u * B + 3u * B * Smax) * sizeof(uint32_t);
+           (size_t)kHotProducers * hot_buf_words(B, Smax) * sizeof(uint32_t);
 }
 
 __device__ __forceinline__ bool hot_wait(uint32_t* flag, uint32_t want, uint32_t* abort_flag, uint32_t limit,
@@ -45,70 +45,112 @@ __device__ __forceinline__ bool hot_wait(uint32_t* flag, uint32_t want, uint32_t
     }
 }
 
-// One step's worth of a batch buffer for a consumer lane: coordinate metadata and the lane's SL
-// entries (key, value, cold value).
+// One batch buffer in LDS (B coordinates, Smax entry slots each; 32-bit words, 16-byte aligned).
+struct HotBuf {
+    float4* rec;    // [B]: model value, step scale, label or <y, a_m>, new model value (the consumer's)
+    int2* kv;       // [B * Smax]: key and value bits of each entry slot.  Key: the hot slot (>= 0), or
+                    // ~index for a cold entry; padding slots are cold with value 0.
+    float* cold;    // [B * Smax]: a cold entry's shared-vector value, then every slot's update
+    uint32_t* mid;  // [B]: coordinate index, or kHotEmpty for positions past the end of the epoch
+};
+
+__device__ __forceinline__ HotBuf hot_buf(uint32_t* base, uint32_t B, uint32_t Smax) {
+    HotBuf b;
+    b.rec = reinterpret_cast<float4*>(base);
+    b.kv = reinterpret_cast<int2*>(base + 4u * B);
+    b.cold = reinterpret_cast<float*>(base + 4u * B + 2u * B * Smax);
+    b.mid = base + 4u * B + 3u * B * Smax;
+    return b;
+}
+
+constexpr uint32_t kHotEmpty = 0xFFFFFFFFu;
+
+// The closed-form steps of coord_step with each coordinate's divisor folded into a scale that the
+// producer computes (so the consumer's step has no division):
+//   ridge primal  sc = 1 / (|a_m|^2 + lambda N)      d = (<y, a_m> - g - lambda N beta_m) sc
+//   SVM dual      sc = lambda N / |x_i|^2, -1 if 0    alpha_i <- clip(alpha_i + sc (1 - y_i g), 0, 1)
+//   ridge dual    sc = 1 / (lambda N + |abar_n|^2)   d = (lambda y_n - g - lambda N alpha_n) sc
+template <int FORM>
+__device__ __forceinline__ float hot_step_scale(float s, const StepConsts& k) {
+    if constexpr (FORM == FORM_SVM_DUAL)
+        return s > 0.0f ? k.lamN / s : -1.0f;
+    else
+        return 1.0f / (s + k.lamN);
+}
+
+template <int FORM>
+__device__ __forceinline__ float hot_coord_step(float g, float m_old, float sc, float ylab, const StepConsts& k,
+                                                float* coef) {
+    if constexpr (FORM == FORM_RIDGE_PRIMAL) {
+        const float d = ((ylab - g) - k.lamN * m_old) * sc;
+        *coef = d;
+        return m_old + d;
+    } else if constexpr (FORM == FORM_SVM_DUAL) {
+        // An empty row (sc < 0): the dual is linear in alpha_i with positive slope, so alpha_i = 1.
+        const float a = sc < 0.0f ? 1.0f : fminf(fmaxf(m_old + sc * (1.0f - ylab * g), 0.0f), 1.0f);
+        *coef = (a - m_old) * ylab * k.inv_lamN;
+        return a;
+    } else {
+        const float d = (k.lam * ylab - g - k.lamN * m_old) * sc;
+        *coef = d;
+        return m_old + d;
+    }
+}
+
+// One step's worth of a batch buffer for a consumer lane: the coordinate's record and the lane's SL
+// entry slots (key, value, cold value).
 template <int SL>
 struct HotStep {
-    uint32_t m, len;
-    float m_old, sn, ylab;
+    float4 r;
     int32_t kk[SL];
     float vv[SL], xv[SL];
 };
 
 template <int SL>
-__device__ __forceinline__ void hot_load_step(HotStep<SL>& t, const uint32_t* mb, const int32_t* key, const float* val,
-                                              const float* cold, uint32_t B, uint32_t c, uint32_t e0, bool act) {
-    t.m = mb[c];
-    t.len = act ? mb[B + c] : 0u;
-    t.m_old = __uint_as_float(mb[2u * B + c]);
-    t.sn = __uint_as_float(mb[3u * B + c]);
-    t.ylab = __uint_as_float(mb[4u * B + c]);
+__device__ __forceinline__ void hot_load_step(HotStep<SL>& t, const HotBuf& hb, uint32_t c, uint32_t e0) {
+    t.r = hb.rec[c];
 #pragma unroll
     for (int r = 0; r < SL; ++r) {
-        t.kk[r] = key[e0 + 8 * r];
-        t.vv[r] = val[e0 + 8 * r];
-        t.xv[r] = cold[e0 + 8 * r];
+        const int2 p = hb.kv[e0 + 8 * r];
+        t.kk[r] = p.x;
+        t.vv[r] = __int_as_float(p.y);
+        t.xv[r] = hb.cold[e0 + 8 * r];
     }
 }
 
 // One step of the consumer: W coordinates, 8 lanes each.  Reads the hot values the keys of `cur`
-// point at, then the metadata and entries of the next step into `nxt` (the last step of a batch
-// re-reads its own), then reduces, steps and scatters.  The plain LDS writes are issued by every
-// lane (an inactive group writes into its own slots of `scr`), so only the hot-entry atomics sit
-// behind a branch: a coordinate whose step is zero (in the SVM dual, most of them once their alpha
-// sits at a bound) issues none.
+// point at, then the record and entries of the next step into `nxt` (the last step of a batch
+// re-reads its own), then reduces, steps and scatters.  Every lane issues the plain LDS writes (an
+// inactive group writes into its own cells of `scr`).  The LDS atomics sit behind one branch per
+// step, taken by the groups whose step is nonzero (in the SVM dual, once their alpha sits at a bound,
+// most coordinates do not move); there every slot is added, a cold or padding slot into the lane's
+// cell of `dummy`.
 template <int FORM, typename U, int SL>
-__device__ __forceinline__ void hot_step(const EpochArgs& a, U* hot, uint32_t* mb, const int32_t* key,
-                                         const float* val, float* coldw, float* scr, uint32_t B,
+__device__ __forceinline__ void hot_step(const StepConsts& k, U* hot, U* dummy, const HotBuf& hb, float* scr,
                                          uint32_t Smax, uint32_t cn, bool act, uint32_t sub, int lane,
                                          const HotStep<SL>& cur, uint32_t c, HotStep<SL>& nxt) {
     U hv[SL];
 #pragma unroll
     for (int r = 0; r < SL; ++r) hv[r] = hot[cur.kk[r] >= 0 ? cur.kk[r] : 0];
     __builtin_amdgcn_sched_barrier(0);
-    hot_load_step<SL>(nxt, mb, key, val, coldw, B, cn, cn * Smax + sub, act);
+    hot_load_step<SL>(nxt, hb, cn, cn * Smax + sub);
     __builtin_amdgcn_sched_barrier(0);
     float acc = 0.0f;
 #pragma unroll
-    for (int r = 0; r < SL; ++r) {
-        // Padding entries have value 0; a cold entry's value came with it.
-        const float x = cur.kk[r] >= 0 ? (float)hv[r] : cur.xv[r];
-        acc = fmaf(cur.vv[r], x, acc);
-    }
+    for (int r = 0; r < SL; ++r) acc = fmaf(cur.vv[r], cur.kk[r] >= 0 ? (float)hv[r] : cur.xv[r], acc);
     const float gsum = group_sum<8>(acc);
     float coef;
-    const float m_new = coord_step<FORM>(gsum, cur.sn, cur.m_old, cur.ylab, a.k, &coef);
-    // The model value and the updates go into this coordinate's batch slots (an empty position at
-    // the end of the epoch has m = EMPTY and zero values, which the flush skips).
-    const uint32_t e0 = c * Smax + sub;
-    uint32_t* const mw = act ? mb + 2u * B + c : reinterpret_cast<uint32_t*>(scr + lane);
-    *mw = __float_as_uint(m_new);
+    const float m_new = hot_coord_step<FORM>(gsum, cur.r.x, cur.r.y, cur.r.z, k, &coef);
+    if (!act) coef = 0.0f;
+    // The new model value and every slot's update go into this coordinate's batch slots (an empty
+    // position at the end of the epoch has kHotEmpty as its index, which the flush skips).
+    *(act ? &hb.rec[c].w : scr + lane) = m_new;
+    float* const cw = act ? hb.cold + c * Smax + sub : scr + lane;
 #pragma unroll
-    for (int r = 0; r < SL; ++r) {
-        const float d = coef * cur.vv[r];
-        float* const cw = act ? coldw + e0 + 8 * r : scr + lane;
-        *cw = d;  // read back only for cold entries
-        if (act && cur.kk[r] >= 0 && sub + 8u * r < cur.len && coef != 0.0f) atomicAdd(hot + cur.kk[r], (U)d);
+    for (int r = 0; r < SL; ++r) cw[8 * r] = coef * cur.vv[r];  // read back only for cold entries
+    if (coef != 0.0f) {
+#pragma unroll
+        for (int r = 0; r < SL; ++r) atomicAdd(cur.kk[r] >= 0 ? hot + cur.kk[r] : dummy + lane, (U)(coef * cur.vv[r]));
     }
 }
 
@@ -118,129 +160,179 @@ __device__ __forceinline__ void hot_step(const EpochArgs& a, U* hot, uint32_t* m
 // back into the batch buffer, and the producer that owns it issues the global stores and atomics
 // before refilling it, so this wave never waits on global memory.
 template <int FORM, typename U, int SL>
-__device__ __forceinline__ void hot_consumer(const HotArgs& h, U* hot, uint32_t* ready, uint32_t* freed,
+__device__ __forceinline__ void hot_consumer(const HotArgs& h, U* hot, U* dummy, uint32_t* ready, uint32_t* freed,
                                              uint32_t* abort_flag, uint32_t* bufs, float* scr, uint32_t nb,
                                              int lane) {
-    const EpochArgs& a = h.e;
-    const uint32_t B = h.B, Smax = h.Smax, W = h.W, buf_words = 5u * B + 3u * B * Smax, S = B / W;
+    const StepConsts k = h.e.k;
+    const uint32_t B = h.B, Smax = h.Smax, W = h.W, bw = hot_buf_words(B, Smax), S = B / W;
     const uint32_t g = (uint32_t)lane >> 3, sub = (uint32_t)lane & 7u;
     const bool act = g < W;
     const uint32_t g0 = act ? g : 0u;  // inactive lanes read coordinate 0 of each step and write nothing
     for (uint32_t b = 0; b < nb; ++b) {
         const uint32_t p = b % kHotProducers, n = b / kHotProducers;
         if (!hot_wait(ready + p, n + 1, abort_flag, h.spin_limit, h.err)) return;
-        uint32_t* const mb = bufs + p * buf_words;
-        const int32_t* key = reinterpret_cast<const int32_t*>(mb + 5u * B);
-        const float* val = reinterpret_cast<const float*>(key + B * Smax);
-        float* const coldw = const_cast<float*>(val + B * Smax);
+        const HotBuf hb = hot_buf(bufs + p * bw, B, Smax);
         HotStep<SL> sa, sb;
-        hot_load_step<SL>(sa, mb, key, val, coldw, B, g0, g0 * Smax + sub, act);
+        hot_load_step<SL>(sa, hb, g0, g0 * Smax + sub);
         uint32_t st = 0;
         for (; st + 1 < S; st += 2) {
             const uint32_t c0 = st * W + g0, c1 = c0 + W;
             const uint32_t c2 = st + 2 < S ? c1 + W : c1;
-            hot_step<FORM, U, SL>(a, hot, mb, key, val, coldw, scr, B, Smax, c1, act, sub, lane, sa, c0, sb);
-            hot_step<FORM, U, SL>(a, hot, mb, key, val, coldw, scr, B, Smax, c2, act, sub, lane, sb, c1, sa);
+            hot_step<FORM, U, SL>(k, hot, dummy, hb, scr, Smax, c1, act, sub, lane, sa, c0, sb);
+            hot_step<FORM, U, SL>(k, hot, dummy, hb, scr, Smax, c2, act, sub, lane, sb, c1, sa);
         }
         if (st < S) {
             const uint32_t c0 = st * W + g0;
-            hot_step<FORM, U, SL>(a, hot, mb, key, val, coldw, scr, B, Smax, c0, act, sub, lane, sa, c0, sb);
+            hot_step<FORM, U, SL>(k, hot, dummy, hb, scr, Smax, c0, act, sub, lane, sa, c0, sb);
         }
         __hip_atomic_store(freed + p, n + 1, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_WORKGROUP);
     }
 }
 
-// Writes out a consumed batch buffer: new model values, and the updates of cold entries as
-// device-scope atomics (fire and forget).
-template <typename U>
-__device__ __forceinline__ void hot_flush(const EpochArgs& a, const uint32_t* mb, const int32_t* key, const float* valb,
-                                          const float* coldb, uint32_t B, uint32_t NB, int lane) {
-    U* const uu = static_cast<U*>(a.u);
-    if ((uint32_t)lane < B) {
-        const uint32_t m = mb[lane];
-        if (m != 0xFFFFFFFFu) a.model[m] = __uint_as_float(mb[2u * B + lane]);
-    }
-    for (uint32_t e = (uint32_t)lane; e < NB; e += 64) {
-        const int32_t kk = key[e];
-        const float d = coldb[e];
-        if (kk < 0 && valb[e] != 0.0f && d != 0.0f) atomic_add_u(uu + ~kk, d);
-    }
+
+// A producer's view of one batch: lane c < B loads coordinate c's metadata.  The coordinate index
+// is computed first (arithmetic only) and the loads are issued later, so that they can be issued
+// behind the previous batch's entry loads.
+struct HotMeta {
+    uint32_t m;  // coordinate, or kHotEmpty
+    int64_t s0, s1;
+    float m_old, sn, ylab;
+};
+
+__device__ __forceinline__ uint32_t hot_coord(const EpochArgs& a, uint32_t b, uint32_t B, uint32_t nb, int lane) {
+    const uint32_t j = b * B + (uint32_t)lane;
+    return b < nb && (uint32_t)lane < B && j < a.perm.n ? perm_at(j, a.perm) : kHotEmpty;
 }
 
+__device__ __forceinline__ void hot_meta_load(const EpochArgs& a, HotMeta& t) {
+    const uint32_t mm = t.m != kHotEmpty ? t.m : 0u;  // the loads always hit a valid coordinate
+    t.s0 = a.ptr[mm];
+    t.s1 = a.ptr[mm + 1];
+    t.m_old = a.model[mm];
+    t.sn = a.norms[mm];
+    t.ylab = a.y[mm];
+}
+
+// Raw-buffer load of a shared-vector entry, kept in its storage type; a lane with `in` false
+// reads at an out-of-range offset (0, no memory traffic).  Branch-free, so the compiler's count of
+// the memory operations behind an earlier load stays exact.
 template <typename U>
+__device__ __forceinline__ U hot_load_u(const SharedBuf<U>& b, uint32_t i, bool in) {
+    const uint32_t off = in ? i * (uint32_t)sizeof(U) : b.oob;
+    if constexpr (sizeof(U) == 4)
+        return __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(b.r, (int)off, 0, 0));
+    else
+        return __builtin_bit_cast(double, __builtin_amdgcn_raw_buffer_load_b64(b.r, (int)off, 0, 0));
+}
+
+// Producer wave q fills buffer q with batches q, q + kHotProducers, ...  It is software-pipelined:
+// the metadata of its next batch is loaded while this batch's entries are in flight, and the
+// consumed batch it replaces is read out of LDS before the new one is written in, and written out
+// to global memory (new model values, device-scope atomics for the cold entries' updates) after,
+// so that no wait for this batch's loads also waits for those stores and atomics.
+template <int FORM, typename U>
 __device__ __forceinline__ void hot_producer(const HotArgs& h, uint32_t* ready, uint32_t* freed, uint32_t* abort_flag,
                                              uint32_t* bufs, uint32_t nb, int q, int lane) {
     const EpochArgs& a = h.e;
-    const U* const uu = static_cast<const U*>(a.u);
-    const uint32_t B = h.B, Smax = h.Smax, C = a.perm.n, buf_words = 5u * B + 3u * B * Smax, NB = B * Smax;
-    uint32_t* const mb = bufs + q * buf_words;
-    int32_t* const key = reinterpret_cast<int32_t*>(mb + 5u * B);
-    float* const valb = reinterpret_cast<float*>(key + NB);
-    float* const coldb = valb + NB;
+    U* const uu = static_cast<U*>(a.u);
+    const SharedBuf<U> ub = shared_buf<U>(a.u, a.u_bytes, nullptr);
+    const uint32_t B = h.B, Smax = h.Smax, NB = B * Smax;
+    const HotBuf hb = hot_buf(bufs + q * hot_buf_words(B, Smax), B, Smax);
     constexpr int NE = kHotEntriesPerLane;
     // Buffer slot e = t * 64 + lane holds entry e % Smax of coordinate e / Smax of the batch; the
     // mapping is the same for every batch.
     const uint32_t c0 = (uint32_t)lane / Smax, k0 = (uint32_t)lane - c0 * Smax;
     const uint32_t dc = 64u / Smax, dk = 64u - dc * Smax;
+    HotMeta md;
+    md.m = hot_coord(a, (uint32_t)q, B, nb, lane);
+    hot_meta_load(a, md);
     for (uint32_t b = (uint32_t)q; b < nb + kHotProducers; b += kHotProducers) {
         const uint32_t n = b / kHotProducers;
-        if (n > 0 || b < nb) {  // the buffer's previous batch (if any) must have been consumed
-            if (!hot_wait(freed + q, n, abort_flag, h.spin_limit, h.err)) return;
-        }
-        if (n > 0) hot_flush<U>(a, mb, key, valb, coldb, B, NB, lane);
-        if (b >= nb) break;
-        // Metadata: lane c < B holds coordinate c of the batch.
-        const uint32_t j = b * B + (uint32_t)lane;
-        const bool live = (uint32_t)lane < B && j < C;
-        const uint32_t m = live ? perm_at(j, a.perm) : 0xFFFFFFFFu;
-        const uint32_t mm = live ? m : 0u;  // loads below always hit a valid coordinate
-        const int64_t s0 = a.ptr[mm], s1 = a.ptr[mm + 1];
-        const float m_old = a.model[mm], sn = a.norms[mm], ylab = a.y[mm];
-        const uint32_t len = live ? (uint32_t)(s1 - s0) : 0u;
-        if ((uint32_t)lane < B) {
-            mb[lane] = m;
-            mb[B + lane] = len;
-            mb[2u * B + lane] = __float_as_uint(m_old);
-            mb[3u * B + lane] = __float_as_uint(sn);
-            mb[4u * B + lane] = __float_as_uint(ylab);
-        }
-        // Entries, two stages of unconditional loads (entry 0 stands in for unused slots): index,
-        // value and hot slot, then the current value of the shared vector.
         int32_t ix[NE];
         float vv[NE];
         uint32_t sl[NE];
         bool in[NE];
-        uint32_t c = c0, k = k0;
+        U cv[NE];
+        HotMeta nx;
+        nx.m = hot_coord(a, b + kHotProducers, B, nb, lane);
+        if (b < nb) {
+            // Entries (entry 0 stands in for unused slots): index, value and hot slot.
+            const uint32_t len = md.m != kHotEmpty ? (uint32_t)(md.s1 - md.s0) : 0u;
+            uint32_t c = c0, k = k0;
 #pragma unroll
-        for (int t = 0; t < NE; ++t) {
-            const uint32_t cc = c < B ? c : 0u;
-            const int64_t sc = __shfl(s0, (int)cc);
-            const uint32_t lc = (uint32_t)__shfl((int)len, (int)cc);
-            in[t] = c < B && k < lc;
-            const int64_t kk = in[t] ? sc + k : 0;
-            ix[t] = a.idx[kk];
-            vv[t] = a.val[kk];
-            sl[t] = h.slot_entry[kk];
-            c += dc;
-            k += dk;
-            if (k >= Smax) {
-                k -= Smax;
-                ++c;
+            for (int t = 0; t < NE; ++t) {
+                const uint32_t cc = c < B ? c : 0u;
+                const int64_t sc = __shfl(md.s0, (int)cc);
+                const uint32_t lc = (uint32_t)__shfl((int)len, (int)cc);
+                in[t] = c < B && k < lc;
+                const int64_t kk = in[t] ? sc + k : 0;
+                ix[t] = a.idx[kk];
+                vv[t] = a.val[kk];
+                sl[t] = h.slot_entry[kk];
+                c += dc;
+                k += dk;
+                if (k >= Smax) {
+                    k -= Smax;
+                    ++c;
+                }
+            }
+            hot_meta_load(a, nx);
+            // Only cold entries need their shared-vector value: a hot entry's comes from LDS, and a
+            // padding slot's is not used.
+#pragma unroll
+            for (int t = 0; t < NE; ++t) cv[t] = hot_load_u<U>(ub, (uint32_t)ix[t], in[t] && sl[t] == kHotCold);
+        }
+        // The buffer's previous batch (if any) must have been consumed.
+        if (n > 0 || b < nb) {
+            if (!hot_wait(freed + q, n, abort_flag, h.spin_limit, h.err)) return;
+        }
+        // Read out the consumed batch: new model values, and each cold entry's update.
+        uint32_t old_m = kHotEmpty;
+        float old_model = 0.0f;
+        int32_t old_k[NE];
+        float old_d[NE];
+        if (n > 0) {
+            if ((uint32_t)lane < B) {
+                old_m = hb.mid[lane];
+                old_model = hb.rec[lane].w;
+            }
+#pragma unroll
+            for (int t = 0; t < NE; ++t) {
+                const uint32_t e = (uint32_t)t * 64u + (uint32_t)lane;
+                old_k[t] = 0;
+                old_d[t] = 0.0f;  // 0: nothing to write out (hot, padding, zero value or zero update)
+                if (e < NB) {
+                    const int2 p = hb.kv[e];
+                    old_k[t] = p.x;
+                    old_d[t] = p.x < 0 && p.y != 0 ? hb.cold[e] : 0.0f;
+                }
             }
         }
-        float cv[NE];
-#pragma unroll
-        for (int t = 0; t < NE; ++t) cv[t] = (float)uu[ix[t]];
-#pragma unroll
-        for (int t = 0; t < NE; ++t) {
-            const uint32_t e = (uint32_t)t * 64u + (uint32_t)lane;
-            if (e < NB) {
-                key[e] = !in[t] ? 0 : (sl[t] != kHotCold ? (int32_t)sl[t] : ~ix[t]);
-                valb[e] = in[t] ? vv[t] : 0.0f;
-                coldb[e] = cv[t];
+        if (b < nb) {
+            if ((uint32_t)lane < B) {
+                hb.mid[lane] = md.m;
+                hb.rec[lane] = make_float4(md.m_old, hot_step_scale<FORM>(md.sn, a.k), md.ylab, 0.0f);
             }
+#pragma unroll
+            for (int t = 0; t < NE; ++t) {
+                const uint32_t e = (uint32_t)t * 64u + (uint32_t)lane;
+                if (e < NB) {
+                    hb.kv[e] = make_int2(!in[t] ? -1 : (sl[t] != kHotCold ? (int32_t)sl[t] : ~ix[t]),
+                                         __float_as_int(in[t] ? vv[t] : 0.0f));
+                    hb.cold[e] = (float)cv[t];
+                }
+            }
+            __hip_atomic_store(ready + q, n + 1, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_WORKGROUP);
         }
-        __hip_atomic_store(ready + q, n + 1, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_WORKGROUP);
+        if (n > 0) {
+            // Fire and forget.
+            if (old_m != kHotEmpty) a.model[old_m] = old_model;
+#pragma unroll
+            for (int t = 0; t < NE; ++t)
+                if (old_d[t] != 0.0f) atomic_add_u(uu + ~old_k[t], old_d[t]);
+        }
+        if (b >= nb) break;
+        md = nx;
     }
 }
 
@@ -252,7 +344,11 @@ __global__ __launch_bounds__(64 * (1 + kHotProducers)) void k_epoch_hot(HotArgs 
     uint32_t* const ready = reinterpret_cast<uint32_t*>(hot_lds + h.hot_bytes);
     uint32_t* const freed = ready + kHotProducers;
     uint32_t* const abort_flag = freed + kHotProducers;
-    float* const scr = reinterpret_cast<float*>(hot_lds + h.hot_bytes + kHotFlagBytes);  // 64 floats
+    // Scratch: write targets of inactive consumer lanes (kHotWriteScratchBytes), then one atomic
+    // target per consumer lane for cold and padding slots.
+    float* const scr = reinterpret_cast<float*>(hot_lds + h.hot_bytes + kHotFlagBytes);
+    U* const dummy = reinterpret_cast<U*>(hot_lds + h.hot_bytes + kHotFlagBytes + kHotWriteScratchBytes);
+    static_assert(kHotWriteScratchBytes + 64 * sizeof(double) <= kHotScratchBytes, "scratch exceeds its area");
     uint32_t* const bufs = reinterpret_cast<uint32_t*>(hot_lds + h.hot_bytes + kHotFlagBytes + kHotScratchBytes);
     static_assert((2 * kHotProducers + 1) * sizeof(uint32_t) <= kHotFlagBytes, "handover words exceed their area");
     U* const uu = static_cast<U*>(a.u);
@@ -263,17 +359,17 @@ __global__ __launch_bounds__(64 * (1 + kHotProducers)) void k_epoch_hot(HotArgs 
     const uint32_t nb = (a.perm.n + h.B - 1) / h.B;
     if (wave == 0) {
         switch (h.Smax / 8) {  // entries per consumer lane
-            case 1: hot_consumer<FORM, U, 1>(h, hot, ready, freed, abort_flag, bufs, scr, nb, lane); break;
-            case 2: hot_consumer<FORM, U, 2>(h, hot, ready, freed, abort_flag, bufs, scr, nb, lane); break;
-            case 3: hot_consumer<FORM, U, 3>(h, hot, ready, freed, abort_flag, bufs, scr, nb, lane); break;
-            case 4: hot_consumer<FORM, U, 4>(h, hot, ready, freed, abort_flag, bufs, scr, nb, lane); break;
-            case 5: hot_consumer<FORM, U, 5>(h, hot, ready, freed, abort_flag, bufs, scr, nb, lane); break;
-            case 6: hot_consumer<FORM, U, 6>(h, hot, ready, freed, abort_flag, bufs, scr, nb, lane); break;
-            case 7: hot_consumer<FORM, U, 7>(h, hot, ready, freed, abort_flag, bufs, scr, nb, lane); break;
-            default: hot_consumer<FORM, U, 8>(h, hot, ready, freed, abort_flag, bufs, scr, nb, lane); break;
+            case 1: hot_consumer<FORM, U, 1>(h, hot, dummy, ready, freed, abort_flag, bufs, scr, nb, lane); break;
+            case 2: hot_consumer<FORM, U, 2>(h, hot, dummy, ready, freed, abort_flag, bufs, scr, nb, lane); break;
+            case 3: hot_consumer<FORM, U, 3>(h, hot, dummy, ready, freed, abort_flag, bufs, scr, nb, lane); break;
+            case 4: hot_consumer<FORM, U, 4>(h, hot, dummy, ready, freed, abort_flag, bufs, scr, nb, lane); break;
+            case 5: hot_consumer<FORM, U, 5>(h, hot, dummy, ready, freed, abort_flag, bufs, scr, nb, lane); break;
+            case 6: hot_consumer<FORM, U, 6>(h, hot, dummy, ready, freed, abort_flag, bufs, scr, nb, lane); break;
+            case 7: hot_consumer<FORM, U, 7>(h, hot, dummy, ready, freed, abort_flag, bufs, scr, nb, lane); break;
+            default: hot_consumer<FORM, U, 8>(h, hot, dummy, ready, freed, abort_flag, bufs, scr, nb, lane); break;
         }
     } else
-        hot_producer<U>(h, ready, freed, abort_flag, bufs, nb, wave - 1, lane);
+        hot_producer<FORM, U>(h, ready, freed, abort_flag, bufs, nb, wave - 1, lane);
     __syncthreads();
     for (uint32_t i = tid; i < h.n_hot; i += blockDim.x) uu[h.hot_ids[i]] = hot[i];
 }

@@ -90,10 +90,20 @@ struct ObjArgs {
 constexpr int kHotProducers = 8;
 constexpr int kHotEntriesPerLane = 12;  // producer lanes x this >= batch entries (64 x 12 = 768)
 constexpr int kHotFlagBytes = 128;      // LDS handover words: ready[producer], freed[producer], abort
-constexpr int kHotScratchBytes = 64 * 4;  // write targets of the consumer's inactive lanes
+// Write targets of the consumer's inactive lanes (a lane's cells at 32-byte strides, up to 8 slots),
+// then one fp64-sized atomic target per consumer lane.
+constexpr int kHotWriteScratchBytes = 512;
+constexpr int kHotScratchBytes = kHotWriteScratchBytes + 64 * 8;
 constexpr int kHotMaxWindow = 8;         // consumer wave: W groups of 8 lanes
 constexpr int kHotMaxSegment = 64;
 constexpr uint16_t kHotCold = 0xFFFF;    // slot_of value of an entry that is not hot
+
+// 32-bit words of one batch buffer (B coordinates, Smax entry slots each): a 4-word record per
+// coordinate, key and value per slot, cold value or update per slot, coordinate index; rounded up to
+// 16 bytes so that every buffer and its records stay aligned.
+__host__ __device__ constexpr uint32_t hot_buf_words(uint32_t B, uint32_t Smax) {
+    return (5u * B + 3u * B * Smax + 3u) & ~3u;
+}
 
 struct HotArgs {
     EpochArgs e;
