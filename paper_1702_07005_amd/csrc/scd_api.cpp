@@ -164,7 +164,7 @@ bool hot_geometry(const scd_solver* h, int64_t W, HotGeom* g) {
     return true;
 }
 
-// Largest hot set that fits LDS next to the largest batch buffers (64 coordinates x 12 entries) as
+// Largest hot set that fits LDS next to the largest batch buffers (64 x kHotEntriesPerLane slots) as
 // fp64 entries, so that it stays valid at both widths of the shared vector.
 uint32_t hot_capacity(const scd_solver* h) {
     const size_t worst = hot_lds_bytes(0, 64, kHotEntriesPerLane);

@@ -47,10 +47,11 @@ __device__ __forceinline__ bool hot_wait(uint32_t* flag, uint32_t want, uint32_t
 
 // One batch buffer in LDS (B coordinates, Smax entry slots each; 32-bit words, 16-byte aligned).
 struct HotBuf {
-    float4* rec;    // [B]: model value, step scale, label or <y, a_m>, new model value (the consumer's)
+    float4* rec;    // [B]: model value, step scale, label or <y, a_m>, unused; the consumer then
+                    // overwrites .z and .w with the new model value and the scatter coefficient
     int2* kv;       // [B * Smax]: key and value bits of each entry slot.  Key: the hot slot (>= 0), or
                     // ~index for a cold entry; padding slots are cold with value 0.
-    float* cold;    // [B * Smax]: a cold entry's shared-vector value, then every slot's update
+    float* cold;    // [B * Smax]: a cold entry's shared-vector value (0 for hot and padding slots)
     uint32_t* mid;  // [B]: coordinate index, or kHotEmpty for positions past the end of the epoch
 };
 
@@ -120,11 +121,13 @@ __device__ __forceinline__ void hot_load_step(HotStep<SL>& t, const HotBuf& hb, 
 
 // One step of the consumer: W coordinates, 8 lanes each.  Reads the hot values the keys of `cur`
 // point at, then the record and entries of the next step into `nxt` (the last step of a batch
-// re-reads its own), then reduces, steps and scatters.  Every lane issues the plain LDS writes (an
-// inactive group writes into its own cells of `scr`).  The LDS atomics sit behind one branch per
-// step, taken by the groups whose step is nonzero (in the SVM dual, once their alpha sits at a bound,
-// most coordinates do not move); there every slot is added, a cold or padding slot into the lane's
-// cell of `dummy`.
+// re-reads its own), then reduces, steps and scatters.  The new model value and the scatter
+// coefficient go back into the coordinate's record (one write, issued by every lane; an inactive
+// group writes into its own cells of `scr`); the producer forms the cold entries' updates from the
+// coefficient when it writes the batch out.  The LDS atomics sit behind one branch per step, taken
+// by the groups whose step is nonzero (in the SVM dual, once their alpha sits at a bound, most
+// coordinates do not move); there every slot is added, a cold or padding slot into the lane's cell
+// of `dummy`.
 template <int FORM, typename U, int SL>
 __device__ __forceinline__ void hot_step(const StepConsts& k, U* hot, U* dummy, const HotBuf& hb, float* scr,
                                          uint32_t Smax, uint32_t cn, bool act, uint32_t sub, int lane,
@@ -142,12 +145,8 @@ __device__ __forceinline__ void hot_step(const StepConsts& k, U* hot, U* dummy, 
     float coef;
     const float m_new = hot_coord_step<FORM>(gsum, cur.r.x, cur.r.y, cur.r.z, k, &coef);
     if (!act) coef = 0.0f;
-    // The new model value and every slot's update go into this coordinate's batch slots (an empty
-    // position at the end of the epoch has kHotEmpty as its index, which the flush skips).
-    *(act ? &hb.rec[c].w : scr + lane) = m_new;
-    float* const cw = act ? hb.cold + c * Smax + sub : scr + lane;
-#pragma unroll
-    for (int r = 0; r < SL; ++r) cw[8 * r] = coef * cur.vv[r];  // read back only for cold entries
+    // (An empty position at the end of the epoch has kHotEmpty as its index, which the flush skips.)
+    *reinterpret_cast<float2*>(act ? &hb.rec[c].z : scr + 2 * lane) = make_float2(m_new, coef);
     if (coef != 0.0f) {
 #pragma unroll
         for (int r = 0; r < SL; ++r) atomicAdd(cur.kk[r] >= 0 ? hot + cur.kk[r] : dummy + lane, (U)(coef * cur.vv[r]));
@@ -286,7 +285,9 @@ __device__ __forceinline__ void hot_producer(const HotArgs& h, uint32_t* ready, 
         if (n > 0 || b < nb) {
             if (!hot_wait(freed + q, n, abort_flag, h.spin_limit, h.err)) return;
         }
-        // Read out the consumed batch: new model values, and each cold entry's update.
+        // Read out the consumed batch: new model values, and each cold entry's update (the
+        // coordinate's coefficient times the entry's value, the product the consumer formed for
+        // its hot entries).
         uint32_t old_m = kHotEmpty;
         float old_model = 0.0f;
         int32_t old_k[NE];
@@ -294,8 +295,10 @@ __device__ __forceinline__ void hot_producer(const HotArgs& h, uint32_t* ready, 
         if (n > 0) {
             if ((uint32_t)lane < B) {
                 old_m = hb.mid[lane];
-                old_model = hb.rec[lane].w;
+                old_model = hb.rec[lane].z;
             }
+            uint32_t c = c0;
+            uint32_t k = k0;
 #pragma unroll
             for (int t = 0; t < NE; ++t) {
                 const uint32_t e = (uint32_t)t * 64u + (uint32_t)lane;
@@ -304,7 +307,13 @@ __device__ __forceinline__ void hot_producer(const HotArgs& h, uint32_t* ready, 
                 if (e < NB) {
                     const int2 p = hb.kv[e];
                     old_k[t] = p.x;
-                    old_d[t] = p.x < 0 && p.y != 0 ? hb.cold[e] : 0.0f;
+                    old_d[t] = p.x < 0 && p.y != 0 ? hb.rec[c].w * __int_as_float(p.y) : 0.0f;
+                }
+                c += dc;
+                k += dk;
+                if (k >= Smax) {
+                    k -= Smax;
+                    ++c;
                 }
             }
         }

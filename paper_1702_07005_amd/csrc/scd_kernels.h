@@ -88,10 +88,10 @@ struct ObjArgs {
 // epoch; one consumer wave runs the W in-flight coordinates from LDS only, kHotProducers waves stream
 // the next batches (segment, hot slot or cold value) into LDS buffers.
 constexpr int kHotProducers = 8;
-constexpr int kHotEntriesPerLane = 12;  // producer lanes x this >= batch entries (64 x 12 = 768)
+constexpr int kHotEntriesPerLane = 10;  // producer lanes x this >= batch entries (64 x 10 = 640)
 constexpr int kHotFlagBytes = 128;      // LDS handover words: ready[producer], freed[producer], abort
-// Write targets of the consumer's inactive lanes (a lane's cells at 32-byte strides, up to 8 slots),
-// then one fp64-sized atomic target per consumer lane.
+// Write targets of the consumer's inactive lanes (one 8-byte cell per lane), then one fp64-sized
+// atomic target per consumer lane.
 constexpr int kHotWriteScratchBytes = 512;
 constexpr int kHotScratchBytes = kHotWriteScratchBytes + 64 * 8;
 constexpr int kHotMaxWindow = 8;         // consumer wave: W groups of 8 lanes

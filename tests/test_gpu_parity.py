@@ -525,6 +525,28 @@ def test_hot_set_kernel_parity(case):
     s.close()
 
 
+def test_hot_set_cold_entry_at_index_zero():
+    # The hot-set kernel keys a cold entry by ~index, so shared-vector entry 0 has key -1, the key of
+    # padding slots too (those have value 0).  Move a column with 8 stored entries (far below the
+    # twin's hot threshold) to index 0: its updates must reach global memory like any other cold one.
+    base = problem("click_svm_twin")
+    hits = np.bincount(base.idx, minlength=base.L)
+    c = int(np.flatnonzero(hits == 8)[0])
+    idx = base.idx.copy()
+    at0, atc = idx == 0, idx == c
+    idx[at0], idx[atc] = c, 0
+    p = dataclasses.replace(base, idx=idx)
+    s = scd.solver_for(p)
+    assert s.info()["kernel"] == "hot_lds"
+    for e in range(2):
+        s.epochs(0, 1)
+        gm, gs, _ = s.get_state()
+        w, ref = f64(gs), fresh(p, f64(gm))
+        assert rel_inf(w, ref) <= 1e-4, e
+        assert ref[0] != 0.0 and abs(w[0] - ref[0]) <= 1e-4 * abs(ref[0]), (e, w[0], ref[0])
+    s.close()
+
+
 def test_hot_set_selection_rules():
     p = problem("click_svm_twin")
     s = scd.solver_for(p)
