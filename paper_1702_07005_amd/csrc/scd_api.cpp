@@ -159,7 +159,8 @@ bool hot_geometry(const scd_solver* h, int64_t W, HotGeom* g) {
     const uint32_t cap = std::min<uint32_t>(64, 64u * kHotEntriesPerLane / g->Smax);
     g->B = cap / g->W * g->W;
     if (g->B < g->W) return false;
-    g->hot_bytes = (uint32_t)(((size_t)h->n_hot * (h->wide ? sizeof(double) : sizeof(float)) + 15) / 16 * 16);
+    g->hot_bytes = (uint32_t)(((size_t)(h->n_hot + kHotZeroCells) * (h->wide ? sizeof(double) : sizeof(float)) + 15) /
+                              16 * 16);
     g->lds = hot_lds_bytes(g->hot_bytes, g->B, g->Smax);
     return true;
 }
@@ -169,7 +170,9 @@ bool hot_geometry(const scd_solver* h, int64_t W, HotGeom* g) {
 uint32_t hot_capacity(const scd_solver* h) {
     const size_t worst = hot_lds_bytes(0, 64, kHotEntriesPerLane);
     if (h->max_lds <= worst + 16) return 0;
-    return (uint32_t)std::min<size_t>((h->max_lds - worst - 16) / sizeof(double), kHotCold - 1);
+    const size_t cells = (h->max_lds - worst - 16) / sizeof(double);
+    if (cells <= (size_t)kHotZeroCells) return 0;
+    return (uint32_t)std::min<size_t>(cells - kHotZeroCells, kHotCold - 1);
 }
 
 // Without draining, a pipelined group can have two coordinates in flight (its previous scatter

@@ -47,11 +47,12 @@ __device__ __forceinline__ bool hot_wait(uint32_t* flag, uint32_t want, uint32_t
 
 // One batch buffer in LDS (B coordinates, Smax entry slots each; 32-bit words, 16-byte aligned).
 struct HotBuf {
-    float4* rec;    // [B]: model value, step scale, label or <y, a_m>, unused; the consumer then
-                    // overwrites .z and .w with the new model value and the scatter coefficient
-    int2* kv;       // [B * Smax]: key and value bits of each entry slot.  Key: the hot slot (>= 0), or
-                    // ~index for a cold entry; padding slots are cold with value 0.
-    float* cold;    // [B * Smax]: a cold entry's shared-vector value (0 for hot and padding slots)
+    float4* rec;    // [B]: model value, step scale, label or <y, a_m>, cold part of the gathered dot;
+                    // the consumer then overwrites .z and .w with the new model value and the
+                    // scatter coefficient
+    int2* kv;       // [B * Smax]: key and value bits of each entry slot.  A hot entry's key is its
+                    // slot in the hot array; a cold or padding slot has value 0 and the key of the
+                    // zero cell of the consumer lane that takes it (hot array slot n_hot + lane).
     uint32_t* mid;  // [B]: coordinate index, or kHotEmpty for positions past the end of the epoch
 };
 
@@ -59,8 +60,7 @@ __device__ __forceinline__ HotBuf hot_buf(uint32_t* base, uint32_t B, uint32_t S
     HotBuf b;
     b.rec = reinterpret_cast<float4*>(base);
     b.kv = reinterpret_cast<int2*>(base + 4u * B);
-    b.cold = reinterpret_cast<float*>(base + 4u * B + 2u * B * Smax);
-    b.mid = base + 4u * B + 3u * B * Smax;
+    b.mid = base + 4u * B + 2u * B * Smax;
     return b;
 }
 
@@ -99,12 +99,12 @@ __device__ __forceinline__ float hot_coord_step(float g, float m_old, float sc, 
 }
 
 // One step's worth of a batch buffer for a consumer lane: the coordinate's record and the lane's SL
-// entry slots (key, value, cold value).
+// entry slots (key, value).
 template <int SL>
 struct HotStep {
     float4 r;
     int32_t kk[SL];
-    float vv[SL], xv[SL];
+    float vv[SL];
 };
 
 template <int SL>
@@ -115,33 +115,32 @@ __device__ __forceinline__ void hot_load_step(HotStep<SL>& t, const HotBuf& hb, 
         const int2 p = hb.kv[e0 + 8 * r];
         t.kk[r] = p.x;
         t.vv[r] = __int_as_float(p.y);
-        t.xv[r] = hb.cold[e0 + 8 * r];
     }
 }
 
 // One step of the consumer: W coordinates, 8 lanes each.  Reads the hot values the keys of `cur`
 // point at, then the record and entries of the next step into `nxt` (the last step of a batch
-// re-reads its own), then reduces, steps and scatters.  The new model value and the scatter
-// coefficient go back into the coordinate's record (one write, issued by every lane; an inactive
-// group writes into its own cells of `scr`); the producer forms the cold entries' updates from the
-// coefficient when it writes the batch out.  The LDS atomics sit behind one branch per step, taken
-// by the groups whose step is nonzero (in the SVM dual, once their alpha sits at a bound, most
-// coordinates do not move); there every slot is added, a cold or padding slot into the lane's cell
-// of `dummy`.
+// re-reads its own), then reduces (hot part plus the producer's cold part), steps and scatters.
+// The new model value and the scatter coefficient go back into the coordinate's record (one write,
+// issued by every lane; an inactive group writes into its own cells of `scr`); the producer forms
+// the cold entries' updates from the coefficient when it writes the batch out.  The LDS atomics sit
+// behind one branch per step, taken by the groups whose step is nonzero (in the SVM dual, once their
+// alpha sits at a bound, most coordinates do not move).  A cold or padding slot reads its lane's
+// zero cell and adds coef * 0 to it, so no slot needs a select.
 template <int FORM, typename U, int SL>
-__device__ __forceinline__ void hot_step(const StepConsts& k, U* hot, U* dummy, const HotBuf& hb, float* scr,
-                                         uint32_t Smax, uint32_t cn, bool act, uint32_t sub, int lane,
-                                         const HotStep<SL>& cur, uint32_t c, HotStep<SL>& nxt) {
+__device__ __forceinline__ void hot_step(const StepConsts& k, U* hot, const HotBuf& hb, float* scr, uint32_t Smax,
+                                         uint32_t cn, bool act, uint32_t sub, int lane, const HotStep<SL>& cur,
+                                         uint32_t c, HotStep<SL>& nxt) {
     U hv[SL];
 #pragma unroll
-    for (int r = 0; r < SL; ++r) hv[r] = hot[cur.kk[r] >= 0 ? cur.kk[r] : 0];
+    for (int r = 0; r < SL; ++r) hv[r] = hot[cur.kk[r]];
     __builtin_amdgcn_sched_barrier(0);
     hot_load_step<SL>(nxt, hb, cn, cn * Smax + sub);
     __builtin_amdgcn_sched_barrier(0);
     float acc = 0.0f;
 #pragma unroll
-    for (int r = 0; r < SL; ++r) acc = fmaf(cur.vv[r], cur.kk[r] >= 0 ? (float)hv[r] : cur.xv[r], acc);
-    const float gsum = group_sum<8>(acc);
+    for (int r = 0; r < SL; ++r) acc = fmaf(cur.vv[r], (float)hv[r], acc);
+    const float gsum = group_sum<8>(acc) + cur.r.w;
     float coef;
     const float m_new = hot_coord_step<FORM>(gsum, cur.r.x, cur.r.y, cur.r.z, k, &coef);
     if (!act) coef = 0.0f;
@@ -149,17 +148,17 @@ __device__ __forceinline__ void hot_step(const StepConsts& k, U* hot, U* dummy, 
     *reinterpret_cast<float2*>(act ? &hb.rec[c].z : scr + 2 * lane) = make_float2(m_new, coef);
     if (coef != 0.0f) {
 #pragma unroll
-        for (int r = 0; r < SL; ++r) atomicAdd(cur.kk[r] >= 0 ? hot + cur.kk[r] : dummy + lane, (U)(coef * cur.vv[r]));
+        for (int r = 0; r < SL; ++r) atomicAdd(hot + cur.kk[r], (U)(coef * cur.vv[r]));
     }
 }
 
 // The consumer for coordinates of at most 8 * SL entries: the steps of each batch, unrolled twice
 // so that the two step records alternate instead of being copied (a copy would wait for the
-// prefetch).  Hot entries are updated in LDS; the new model value and each cold entry's update go
-// back into the batch buffer, and the producer that owns it issues the global stores and atomics
-// before refilling it, so this wave never waits on global memory.
+// prefetch).  Hot entries are updated in LDS; the new model value and the coefficient go back into
+// the batch buffer, and the producer that owns it issues the global stores and atomics before
+// refilling it, so this wave never waits on global memory.
 template <int FORM, typename U, int SL>
-__device__ __forceinline__ void hot_consumer(const HotArgs& h, U* hot, U* dummy, uint32_t* ready, uint32_t* freed,
+__device__ __forceinline__ void hot_consumer(const HotArgs& h, U* hot, uint32_t* ready, uint32_t* freed,
                                              uint32_t* abort_flag, uint32_t* bufs, float* scr, uint32_t nb,
                                              int lane) {
     const StepConsts k = h.e.k;
@@ -177,17 +176,16 @@ __device__ __forceinline__ void hot_consumer(const HotArgs& h, U* hot, U* dummy,
         for (; st + 1 < S; st += 2) {
             const uint32_t c0 = st * W + g0, c1 = c0 + W;
             const uint32_t c2 = st + 2 < S ? c1 + W : c1;
-            hot_step<FORM, U, SL>(k, hot, dummy, hb, scr, Smax, c1, act, sub, lane, sa, c0, sb);
-            hot_step<FORM, U, SL>(k, hot, dummy, hb, scr, Smax, c2, act, sub, lane, sb, c1, sa);
+            hot_step<FORM, U, SL>(k, hot, hb, scr, Smax, c1, act, sub, lane, sa, c0, sb);
+            hot_step<FORM, U, SL>(k, hot, hb, scr, Smax, c2, act, sub, lane, sb, c1, sa);
         }
         if (st < S) {
             const uint32_t c0 = st * W + g0;
-            hot_step<FORM, U, SL>(k, hot, dummy, hb, scr, Smax, c0, act, sub, lane, sa, c0, sb);
+            hot_step<FORM, U, SL>(k, hot, hb, scr, Smax, c0, act, sub, lane, sa, c0, sb);
         }
         __hip_atomic_store(freed + p, n + 1, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_WORKGROUP);
     }
 }
-
 
 // A producer's view of one batch: lane c < B loads coordinate c's metadata.  The coordinate index
 // is computed first (arithmetic only) and the loads are issued later, so that they can be issued
@@ -224,11 +222,17 @@ __device__ __forceinline__ U hot_load_u(const SharedBuf<U>& b, uint32_t i, bool 
         return __builtin_bit_cast(double, __builtin_amdgcn_raw_buffer_load_b64(b.r, (int)off, 0, 0));
 }
 
-// Producer wave q fills buffer q with batches q, q + kHotProducers, ...  It is software-pipelined:
-// the metadata of its next batch is loaded while this batch's entries are in flight, and the
-// consumed batch it replaces is read out of LDS before the new one is written in, and written out
-// to global memory (new model values, device-scope atomics for the cold entries' updates) after,
-// so that no wait for this batch's loads also waits for those stores and atomics.
+// Producer wave q fills buffer q with batches q, q + kHotProducers, ...  Slot e = t * 64 + lane of a
+// batch holds entry e % Smax of coordinate e / Smax; since Smax is a multiple of 8, each aligned
+// group of 8 lanes holds entries of one coordinate.  Per slot the producer loads the index, value and
+// hot slot, and a cold entry's shared-vector value; it writes the key and value of hot entries, and
+// adds each coordinate's cold part of the dot (value times shared-vector value over its cold
+// entries) into the coordinate's record.  It is software-pipelined: the metadata of its next batch
+// is loaded while this batch's entries are in flight, and the consumed batch it replaces is read out
+// of LDS before the new one is written in and written out to global memory (new model values,
+// device-scope atomics for the cold entries' updates) after, so that no wait for this batch's loads
+// also waits for those stores and atomics.  The cold entries' indices and values stay in registers
+// until that write-out.
 template <int FORM, typename U>
 __device__ __forceinline__ void hot_producer(const HotArgs& h, uint32_t* ready, uint32_t* freed, uint32_t* abort_flag,
                                              uint32_t* bufs, uint32_t nb, int q, int lane) {
@@ -238,20 +242,25 @@ __device__ __forceinline__ void hot_producer(const HotArgs& h, uint32_t* ready, 
     const uint32_t B = h.B, Smax = h.Smax, NB = B * Smax;
     const HotBuf hb = hot_buf(bufs + q * hot_buf_words(B, Smax), B, Smax);
     constexpr int NE = kHotEntriesPerLane;
-    // Buffer slot e = t * 64 + lane holds entry e % Smax of coordinate e / Smax of the batch; the
-    // mapping is the same for every batch.
     const uint32_t c0 = (uint32_t)lane / Smax, k0 = (uint32_t)lane - c0 * Smax;
     const uint32_t dc = 64u / Smax, dk = 64u - dc * Smax;
     HotMeta md;
     md.m = hot_coord(a, (uint32_t)q, B, nb, lane);
     hot_meta_load(a, md);
+    int32_t fl_ix[NE];  // the buffer's current batch: cold entries' indices and values (0: none)
+    float fl_v[NE];
+#pragma unroll
+    for (int t = 0; t < NE; ++t) {
+        fl_ix[t] = 0;
+        fl_v[t] = 0.0f;
+    }
     for (uint32_t b = (uint32_t)q; b < nb + kHotProducers; b += kHotProducers) {
         const uint32_t n = b / kHotProducers;
         int32_t ix[NE];
         float vv[NE];
         uint32_t sl[NE];
         bool in[NE];
-        U cv[NE];
+        float part[NE];  // cold part of the dot, summed over each aligned group of 8 lanes
         HotMeta nx;
         nx.m = hot_coord(a, b + kHotProducers, B, nb, lane);
         if (b < nb) {
@@ -276,10 +285,14 @@ __device__ __forceinline__ void hot_producer(const HotArgs& h, uint32_t* ready, 
                 }
             }
             hot_meta_load(a, nx);
-            // Only cold entries need their shared-vector value: a hot entry's comes from LDS, and a
-            // padding slot's is not used.
+            // Only cold entries need their shared-vector value.  Their products are summed per
+            // coordinate here, before the wait for the buffer (the loaded values are needed nowhere
+            // else, and holding them would take two registers each for an fp64 shared vector).
+            U cv[NE];
 #pragma unroll
             for (int t = 0; t < NE; ++t) cv[t] = hot_load_u<U>(ub, (uint32_t)ix[t], in[t] && sl[t] == kHotCold);
+#pragma unroll
+            for (int t = 0; t < NE; ++t) part[t] = group_sum<8>(vv[t] * (float)cv[t]);
         }
         // The buffer's previous batch (if any) must have been consumed.
         if (n > 0 || b < nb) {
@@ -290,25 +303,16 @@ __device__ __forceinline__ void hot_producer(const HotArgs& h, uint32_t* ready, 
         // its hot entries).
         uint32_t old_m = kHotEmpty;
         float old_model = 0.0f;
-        int32_t old_k[NE];
         float old_d[NE];
         if (n > 0) {
             if ((uint32_t)lane < B) {
                 old_m = hb.mid[lane];
                 old_model = hb.rec[lane].z;
             }
-            uint32_t c = c0;
-            uint32_t k = k0;
+            uint32_t c = c0, k = k0;
 #pragma unroll
             for (int t = 0; t < NE; ++t) {
-                const uint32_t e = (uint32_t)t * 64u + (uint32_t)lane;
-                old_k[t] = 0;
-                old_d[t] = 0.0f;  // 0: nothing to write out (hot, padding, zero value or zero update)
-                if (e < NB) {
-                    const int2 p = hb.kv[e];
-                    old_k[t] = p.x;
-                    old_d[t] = p.x < 0 && p.y != 0 ? hb.rec[c].w * __int_as_float(p.y) : 0.0f;
-                }
+                old_d[t] = c < B ? hb.rec[c].w * fl_v[t] : 0.0f;
                 c += dc;
                 k += dk;
                 if (k >= Smax) {
@@ -317,18 +321,36 @@ __device__ __forceinline__ void hot_producer(const HotArgs& h, uint32_t* ready, 
                 }
             }
         }
+        int32_t old_ix[NE];
+#pragma unroll
+        for (int t = 0; t < NE; ++t) old_ix[t] = fl_ix[t];
         if (b < nb) {
             if ((uint32_t)lane < B) {
                 hb.mid[lane] = md.m;
                 hb.rec[lane] = make_float4(md.m_old, hot_step_scale<FORM>(md.sn, a.k), md.ylab, 0.0f);
             }
+            uint32_t c = c0, k = k0;
 #pragma unroll
             for (int t = 0; t < NE; ++t) {
                 const uint32_t e = (uint32_t)t * 64u + (uint32_t)lane;
+                const bool hot = in[t] && sl[t] != kHotCold;
+                const bool cold = in[t] && sl[t] == kHotCold;
                 if (e < NB) {
-                    hb.kv[e] = make_int2(!in[t] ? -1 : (sl[t] != kHotCold ? (int32_t)sl[t] : ~ix[t]),
-                                         __float_as_int(in[t] ? vv[t] : 0.0f));
-                    hb.cold[e] = (float)cv[t];
+                    // The consumer lane of this slot is (c mod W) * 8 + k mod 8; the W coordinates
+                    // of one step are consecutive, so c mod 8 tells them apart just as well.
+                    const uint32_t zlane = ((c & 7u) << 3) | (k & 7u);
+                    hb.kv[e] = make_int2(hot ? (int32_t)sl[t] : (int32_t)(h.n_hot + zlane),
+                                         __float_as_int(hot ? vv[t] : 0.0f));
+                    // Added into the coordinate's record (rec.w starts at 0, written above by this wave).
+                    if ((lane & 7) == 0 && part[t] != 0.0f) atomicAdd(&hb.rec[c].w, part[t]);
+                }
+                fl_ix[t] = ix[t];
+                fl_v[t] = cold ? vv[t] : 0.0f;
+                c += dc;
+                k += dk;
+                if (k >= Smax) {
+                    k -= Smax;
+                    ++c;
                 }
             }
             __hip_atomic_store(ready + q, n + 1, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_WORKGROUP);
@@ -338,7 +360,7 @@ __device__ __forceinline__ void hot_producer(const HotArgs& h, uint32_t* ready, 
             if (old_m != kHotEmpty) a.model[old_m] = old_model;
 #pragma unroll
             for (int t = 0; t < NE; ++t)
-                if (old_d[t] != 0.0f) atomic_add_u(uu + ~old_k[t], old_d[t]);
+                if (old_d[t] != 0.0f) atomic_add_u(uu + old_ix[t], old_d[t]);
         }
         if (b >= nb) break;
         md = nx;
@@ -353,29 +375,27 @@ __global__ __launch_bounds__(64 * (1 + kHotProducers)) void k_epoch_hot(HotArgs 
     uint32_t* const ready = reinterpret_cast<uint32_t*>(hot_lds + h.hot_bytes);
     uint32_t* const freed = ready + kHotProducers;
     uint32_t* const abort_flag = freed + kHotProducers;
-    // Scratch: write targets of inactive consumer lanes (kHotWriteScratchBytes), then one atomic
-    // target per consumer lane for cold and padding slots.
+    // Scratch: write targets of inactive consumer lanes.  The hot array ends with kHotZeroCells
+    // zero cells (one per consumer lane) that cold and padding slots point at.
     float* const scr = reinterpret_cast<float*>(hot_lds + h.hot_bytes + kHotFlagBytes);
-    U* const dummy = reinterpret_cast<U*>(hot_lds + h.hot_bytes + kHotFlagBytes + kHotWriteScratchBytes);
-    static_assert(kHotWriteScratchBytes + 64 * sizeof(double) <= kHotScratchBytes, "scratch exceeds its area");
     uint32_t* const bufs = reinterpret_cast<uint32_t*>(hot_lds + h.hot_bytes + kHotFlagBytes + kHotScratchBytes);
     static_assert((2 * kHotProducers + 1) * sizeof(uint32_t) <= kHotFlagBytes, "handover words exceed their area");
     U* const uu = static_cast<U*>(a.u);
     const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
-    for (uint32_t i = tid; i < h.n_hot; i += blockDim.x) hot[i] = uu[h.hot_ids[i]];
+    for (uint32_t i = tid; i < h.n_hot + kHotZeroCells; i += blockDim.x) hot[i] = i < h.n_hot ? uu[h.hot_ids[i]] : U(0);
     if (tid < 2 * kHotProducers + 1) ready[tid] = 0u;  // ready, freed and abort are contiguous
     __syncthreads();
     const uint32_t nb = (a.perm.n + h.B - 1) / h.B;
     if (wave == 0) {
         switch (h.Smax / 8) {  // entries per consumer lane
-            case 1: hot_consumer<FORM, U, 1>(h, hot, dummy, ready, freed, abort_flag, bufs, scr, nb, lane); break;
-            case 2: hot_consumer<FORM, U, 2>(h, hot, dummy, ready, freed, abort_flag, bufs, scr, nb, lane); break;
-            case 3: hot_consumer<FORM, U, 3>(h, hot, dummy, ready, freed, abort_flag, bufs, scr, nb, lane); break;
-            case 4: hot_consumer<FORM, U, 4>(h, hot, dummy, ready, freed, abort_flag, bufs, scr, nb, lane); break;
-            case 5: hot_consumer<FORM, U, 5>(h, hot, dummy, ready, freed, abort_flag, bufs, scr, nb, lane); break;
-            case 6: hot_consumer<FORM, U, 6>(h, hot, dummy, ready, freed, abort_flag, bufs, scr, nb, lane); break;
-            case 7: hot_consumer<FORM, U, 7>(h, hot, dummy, ready, freed, abort_flag, bufs, scr, nb, lane); break;
-            default: hot_consumer<FORM, U, 8>(h, hot, dummy, ready, freed, abort_flag, bufs, scr, nb, lane); break;
+            case 1: hot_consumer<FORM, U, 1>(h, hot, ready, freed, abort_flag, bufs, scr, nb, lane); break;
+            case 2: hot_consumer<FORM, U, 2>(h, hot, ready, freed, abort_flag, bufs, scr, nb, lane); break;
+            case 3: hot_consumer<FORM, U, 3>(h, hot, ready, freed, abort_flag, bufs, scr, nb, lane); break;
+            case 4: hot_consumer<FORM, U, 4>(h, hot, ready, freed, abort_flag, bufs, scr, nb, lane); break;
+            case 5: hot_consumer<FORM, U, 5>(h, hot, ready, freed, abort_flag, bufs, scr, nb, lane); break;
+            case 6: hot_consumer<FORM, U, 6>(h, hot, ready, freed, abort_flag, bufs, scr, nb, lane); break;
+            case 7: hot_consumer<FORM, U, 7>(h, hot, ready, freed, abort_flag, bufs, scr, nb, lane); break;
+            default: hot_consumer<FORM, U, 8>(h, hot, ready, freed, abort_flag, bufs, scr, nb, lane); break;
         }
     } else
         hot_producer<FORM, U>(h, ready, freed, abort_flag, bufs, nb, wave - 1, lane);

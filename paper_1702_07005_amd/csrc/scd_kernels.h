@@ -87,22 +87,20 @@ struct ObjArgs {
 // Hot-set epoch (one workgroup): the n_hot most-updated shared-vector entries live in LDS for the
 // epoch; one consumer wave runs the W in-flight coordinates from LDS only, kHotProducers waves stream
 // the next batches (segment, hot slot or cold value) into LDS buffers.
-constexpr int kHotProducers = 8;
+constexpr int kHotProducers = 11;
 constexpr int kHotEntriesPerLane = 10;  // producer lanes x this >= batch entries (64 x 10 = 640)
 constexpr int kHotFlagBytes = 128;      // LDS handover words: ready[producer], freed[producer], abort
-// Write targets of the consumer's inactive lanes (one 8-byte cell per lane), then one fp64-sized
-// atomic target per consumer lane.
-constexpr int kHotWriteScratchBytes = 512;
-constexpr int kHotScratchBytes = kHotWriteScratchBytes + 64 * 8;
+constexpr int kHotScratchBytes = 64 * 8;  // write targets of the consumer's inactive lanes (8 bytes each)
+constexpr int kHotZeroCells = 64;         // hot-array cells after the hot set, one per consumer lane
 constexpr int kHotMaxWindow = 8;         // consumer wave: W groups of 8 lanes
 constexpr int kHotMaxSegment = 64;
 constexpr uint16_t kHotCold = 0xFFFF;    // slot_of value of an entry that is not hot
 
 // 32-bit words of one batch buffer (B coordinates, Smax entry slots each): a 4-word record per
-// coordinate, key and value per slot, cold value or update per slot, coordinate index; rounded up to
-// 16 bytes so that every buffer and its records stay aligned.
+// coordinate, key and value per slot, coordinate index; rounded up to 16 bytes so that every buffer
+// and its records stay aligned.
 __host__ __device__ constexpr uint32_t hot_buf_words(uint32_t B, uint32_t Smax) {
-    return (5u * B + 3u * B * Smax + 3u) & ~3u;
+    return (5u * B + 2u * B * Smax + 3u) & ~3u;
 }
 
 struct HotArgs {
@@ -114,7 +112,7 @@ struct HotArgs {
     uint32_t W;               // coordinates in flight (<= kHotMaxWindow)
     uint32_t B;               // coordinates per batch (multiple of W)
     uint32_t Smax;            // entries per coordinate reserved in a batch buffer (multiple of 8)
-    uint32_t hot_bytes;       // LDS bytes of the hot array (16-byte aligned)
+    uint32_t hot_bytes;       // LDS bytes of the hot array and its zero cells (16-byte aligned)
     uint32_t spin_limit;      // bounded waits: after this many sleeps a wave gives up and sets *err
     int* err;
 };
