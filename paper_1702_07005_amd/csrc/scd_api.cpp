@@ -125,7 +125,7 @@ struct scd_solver {
     // Hot-set kernel (windows of at most kHotMaxWindow): built on first need.
     int64_t hot = 1;              // option
     int hot_built = 0;
-    uint16_t* slot_entry = nullptr;  // [nnz]: hot slot of each stored entry's index (kHotCold: not hot)
+    int32_t* entry_key = nullptr;    // [nnz]: per stored entry, -1 - its hot slot, or its index when not hot
     int32_t* hot_ids = nullptr;   // [n_hot]
     uint32_t n_hot = 0;
     double hot_cover = 0.0;       // fraction of stored entries that point at a hot entry
@@ -368,19 +368,19 @@ int build_hot_tables(scd_solver* h, hipStream_t s) {
         hip(hipMalloc(&slot_of, sizeof(uint16_t) * (size_t)h->L), "hipMalloc(slot_of)");
         hip(hipMalloc(&h->hot_ids, sizeof(int32_t) * (size_t)cnt), "hipMalloc(hot_ids)");
         hip(launch_hot_assign(hits, h->L, lo, blocks, slot_of, h->hot_ids, s), "hot slots");
-        // Each stored entry's slot, read by the producers beside idx (2 bytes per entry).  Without
-        // the memory for it the hot-set kernel is not used.
+        // Each stored entry's key (-1 - hot slot, or its index), which the producers read in place of
+        // idx (4 bytes per entry).  Without the memory for it the hot-set kernel is not used.
         if (rc == SCD_OK) {
-            const hipError_t e = hipMalloc(&h->slot_entry, sizeof(uint16_t) * (size_t)h->nnz);
+            const hipError_t e = hipMalloc(&h->entry_key, sizeof(int32_t) * (size_t)h->nnz);
             if (e == hipErrorOutOfMemory) {
                 (void)hipGetLastError();
-                h->slot_entry = nullptr;
+                h->entry_key = nullptr;
                 skip = true;
             } else {
-                hip(e, "hipMalloc(slot_entry)");
+                hip(e, "hipMalloc(entry_key)");
             }
         }
-        if (rc == SCD_OK && !skip) hip(launch_hot_entry_slots(h->idx, h->nnz, slot_of, h->slot_entry, s), "entry slots");
+        if (rc == SCD_OK && !skip) hip(launch_hot_entry_keys(h->idx, h->nnz, slot_of, h->entry_key, s), "entry keys");
         hip(hipStreamSynchronize(s), "synchronize");
         if (rc == SCD_OK && !skip) {
             h->n_hot = (uint32_t)cnt;
@@ -392,9 +392,9 @@ int build_hot_tables(scd_solver* h, hipStream_t s) {
     (void)hipFree(blocks);
     (void)hipFree(slot_of);
     if (rc != SCD_OK || skip) {
-        (void)hipFree(h->slot_entry);
+        (void)hipFree(h->entry_key);
         (void)hipFree(h->hot_ids);
-        h->slot_entry = nullptr;
+        h->entry_key = nullptr;
         h->hot_ids = nullptr;
         h->n_hot = 0;
     }
@@ -451,7 +451,7 @@ void release(scd_solver* h) {
     (void)hipFree(h->sums);
     (void)hipFree(h->sink);
     (void)hipFree(h->queue);
-    (void)hipFree(h->slot_entry);
+    (void)hipFree(h->entry_key);
     (void)hipFree(h->hot_ids);
     (void)hipFree(h->hot_err);
     (void)hipHostFree(h->err_host);
@@ -744,7 +744,7 @@ int scd_epochs(scd_handle_t h, uint64_t seed, int32_t n_epochs, void* stream) {
         if (lp.kind == PLAN_HOT) {
             HotArgs ha{};
             ha.e = a;
-            ha.slot_entry = h->slot_entry;
+            ha.entry_key = h->entry_key;
             ha.hot_ids = h->hot_ids;
             ha.n_hot = h->n_hot;
             ha.W = hg.W;

@@ -224,10 +224,10 @@ __device__ __forceinline__ U hot_load_u(const SharedBuf<U>& b, uint32_t i, bool 
 
 // Producer wave q fills buffer q with batches q, q + kHotProducers, ...  Slot e = t * 64 + lane of a
 // batch holds entry e % Smax of coordinate e / Smax; since Smax is a multiple of 8, each aligned
-// group of 8 lanes holds entries of one coordinate.  Per slot the producer loads the index, value and
-// hot slot, and a cold entry's shared-vector value; it writes the key and value of hot entries, and
-// adds each coordinate's cold part of the dot (value times shared-vector value over its cold
-// entries) into the coordinate's record.  It is software-pipelined: the metadata of its next batch
+// group of 8 lanes holds entries of one coordinate.  Per slot the producer loads the entry's key
+// (hot slot or index, precomputed for every stored entry) and value, and a cold entry's
+// shared-vector value; it writes the key and value of hot entries, and adds each coordinate's cold
+// part of the dot (value times shared-vector value over its cold entries) into its record.  It is software-pipelined: the metadata of its next batch
 // is loaded while this batch's entries are in flight, and the consumed batch it replaces is read out
 // of LDS before the new one is written in and written out to global memory (new model values,
 // device-scope atomics for the cold entries' updates) after, so that no wait for this batch's loads
@@ -256,15 +256,14 @@ __device__ __forceinline__ void hot_producer(const HotArgs& h, uint32_t* ready, 
     }
     for (uint32_t b = (uint32_t)q; b < nb + kHotProducers; b += kHotProducers) {
         const uint32_t n = b / kHotProducers;
-        int32_t ix[NE];
+        int32_t ky[NE];  // entry key: -1 - hot slot, or the shared-vector index of a cold entry
         float vv[NE];
-        uint32_t sl[NE];
         bool in[NE];
         float part[NE];  // cold part of the dot, summed over each aligned group of 8 lanes
         HotMeta nx;
         nx.m = hot_coord(a, b + kHotProducers, B, nb, lane);
         if (b < nb) {
-            // Entries (entry 0 stands in for unused slots): index, value and hot slot.
+            // Entries (entry 0 stands in for unused slots): key and value.
             const uint32_t len = md.m != kHotEmpty ? (uint32_t)(md.s1 - md.s0) : 0u;
             uint32_t c = c0, k = k0;
 #pragma unroll
@@ -274,9 +273,8 @@ __device__ __forceinline__ void hot_producer(const HotArgs& h, uint32_t* ready, 
                 const uint32_t lc = (uint32_t)__shfl((int)len, (int)cc);
                 in[t] = c < B && k < lc;
                 const int64_t kk = in[t] ? sc + k : 0;
-                ix[t] = a.idx[kk];
+                ky[t] = h.entry_key[kk];
                 vv[t] = a.val[kk];
-                sl[t] = h.slot_entry[kk];
                 c += dc;
                 k += dk;
                 if (k >= Smax) {
@@ -290,7 +288,7 @@ __device__ __forceinline__ void hot_producer(const HotArgs& h, uint32_t* ready, 
             // else, and holding them would take two registers each for an fp64 shared vector).
             U cv[NE];
 #pragma unroll
-            for (int t = 0; t < NE; ++t) cv[t] = hot_load_u<U>(ub, (uint32_t)ix[t], in[t] && sl[t] == kHotCold);
+            for (int t = 0; t < NE; ++t) cv[t] = hot_load_u<U>(ub, (uint32_t)ky[t], in[t] && ky[t] >= 0);
 #pragma unroll
             for (int t = 0; t < NE; ++t) part[t] = group_sum<8>(vv[t] * (float)cv[t]);
         }
@@ -333,18 +331,18 @@ __device__ __forceinline__ void hot_producer(const HotArgs& h, uint32_t* ready, 
 #pragma unroll
             for (int t = 0; t < NE; ++t) {
                 const uint32_t e = (uint32_t)t * 64u + (uint32_t)lane;
-                const bool hot = in[t] && sl[t] != kHotCold;
-                const bool cold = in[t] && sl[t] == kHotCold;
+                const bool hot = in[t] && ky[t] < 0;
+                const bool cold = in[t] && ky[t] >= 0;
                 if (e < NB) {
                     // The consumer lane of this slot is (c mod W) * 8 + k mod 8; the W coordinates
                     // of one step are consecutive, so c mod 8 tells them apart just as well.
                     const uint32_t zlane = ((c & 7u) << 3) | (k & 7u);
-                    hb.kv[e] = make_int2(hot ? (int32_t)sl[t] : (int32_t)(h.n_hot + zlane),
+                    hb.kv[e] = make_int2(hot ? -1 - ky[t] : (int32_t)(h.n_hot + zlane),
                                          __float_as_int(hot ? vv[t] : 0.0f));
                     // Added into the coordinate's record (rec.w starts at 0, written above by this wave).
                     if ((lane & 7) == 0 && part[t] != 0.0f) atomicAdd(&hb.rec[c].w, part[t]);
                 }
-                fl_ix[t] = ix[t];
+                fl_ix[t] = ky[t];
                 fl_v[t] = cold ? vv[t] : 0.0f;
                 c += dc;
                 k += dk;
@@ -520,18 +518,23 @@ hipError_t launch_hot_block_count(const unsigned* hits, int64_t L, unsigned T, u
     return hipGetLastError();
 }
 
-__global__ __launch_bounds__(256) void k_hot_entry_slots(const int32_t* __restrict__ idx, int64_t nnz,
-                                                         const uint16_t* __restrict__ slot_of,
-                                                         uint16_t* __restrict__ slot_entry) {
-    for (int64_t k = (int64_t)blockIdx.x * 256 + threadIdx.x; k < nnz; k += (int64_t)gridDim.x * 256)
-        slot_entry[k] = slot_of[idx[k]];
+// Each stored entry's key for the producers: -1 - slot for an entry whose shared-vector index is hot,
+// else the index (so a producer reads one array instead of idx and a slot array).
+__global__ __launch_bounds__(256) void k_hot_entry_keys(const int32_t* __restrict__ idx, int64_t nnz,
+                                                        const uint16_t* __restrict__ slot_of,
+                                                        int32_t* __restrict__ entry_key) {
+    for (int64_t k = (int64_t)blockIdx.x * 256 + threadIdx.x; k < nnz; k += (int64_t)gridDim.x * 256) {
+        const int32_t i = idx[k];
+        const uint16_t sl = slot_of[i];
+        entry_key[k] = sl != kHotCold ? -1 - (int32_t)sl : i;
+    }
 }
 
-hipError_t launch_hot_entry_slots(const int32_t* idx, int64_t nnz, const uint16_t* slot_of, uint16_t* slot_entry,
-                                  hipStream_t s) {
+hipError_t launch_hot_entry_keys(const int32_t* idx, int64_t nnz, const uint16_t* slot_of, int32_t* entry_key,
+                                 hipStream_t s) {
     const int64_t want = (nnz + 255) / 256;
     const unsigned blocks = (unsigned)(want < 1 ? 1 : want > 65536 ? 65536 : want);
-    hipLaunchKernelGGL(k_hot_entry_slots, dim3(blocks), dim3(256), 0, s, idx, nnz, slot_of, slot_entry);
+    hipLaunchKernelGGL(k_hot_entry_keys, dim3(blocks), dim3(256), 0, s, idx, nnz, slot_of, entry_key);
     return hipGetLastError();
 }
 

@@ -105,8 +105,8 @@ __host__ __device__ constexpr uint32_t hot_buf_words(uint32_t B, uint32_t Smax) 
 
 struct HotArgs {
     EpochArgs e;
-    const uint16_t* slot_entry;  // [nnz]: LDS slot of each stored entry's shared-vector index, kHotCold
-                                 // when that entry is not hot (read with idx, so no random lookup)
+    const int32_t* entry_key;    // [nnz]: per stored entry, -1 - the LDS slot of its shared-vector
+                                 // index when that entry is hot, else the index itself
     const int32_t* hot_ids;   // [n_hot]: shared-vector index of each slot
     uint32_t n_hot;
     uint32_t W;               // coordinates in flight (<= kHotMaxWindow)
@@ -132,7 +132,7 @@ hipError_t launch_convert_f32_to_f64(const float* in, int64_t n, double* out, hi
 hipError_t launch_convert_f64_to_f32(const double* in, int64_t n, float* out, hipStream_t s);
 hipError_t launch_max_hits(const int32_t* idx, int64_t nnz, int64_t L, unsigned* hits, unsigned* out, hipStream_t s);
 hipError_t launch_count_hits(const int32_t* idx, int64_t nnz, unsigned* hits, hipStream_t s);
-hipError_t launch_hot_entry_slots(const int32_t* idx, int64_t nnz, const uint16_t* slot_of, uint16_t* slot_entry,
+hipError_t launch_hot_entry_keys(const int32_t* idx, int64_t nnz, const uint16_t* slot_of, int32_t* entry_key,
                                   hipStream_t s);
 hipError_t launch_perm_fill(const PermKeys& p, int32_t* out, hipStream_t s);
 hipError_t launch_gather_dots(const int64_t* ptr, const int32_t* idx, const float* val, const float* u, uint32_t C,
