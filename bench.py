@@ -80,10 +80,12 @@ def device_ceilings(L: int):
     return out
 
 
-def cpu_baseline(prob, budget_s: float, seed: int):
+def cpu_baseline(prob, budget_s: float, seed: int, f32_budget_s: float = 0.0):
     """The fp64 sequential oracle on the host, same workload from the zero state, run for
     whole epochs until about `budget_s` seconds of epoch time have elapsed (at least one
-    epoch).  The duality gap after each epoch is evaluated outside the timed epochs."""
+    epoch).  The duality gap after each epoch is evaluated outside the timed epochs.  With
+    `f32_budget_s` > 0, the oracle's single-precision copy of the epochs is timed the same way
+    and reported as `fp32_sequential`."""
     import numpy as np
     from oracle import oracle as orc
 
@@ -109,6 +111,30 @@ def cpu_baseline(prob, budget_s: float, seed: int):
             ttg = (epochs, el)
         if el >= budget_s or epochs >= 1000:
             break
+    # The same sequential epochs in single precision, the precision of the paper's one-thread
+    # baseline, on the same core and a shorter budget.
+    f32 = None
+    if f32_budget_s > 0:
+        m32 = np.zeros(prob.C, dtype=np.float32)
+        s32 = np.zeros(prob.L, dtype=np.float32)
+        e32, el32, ttg32, curve32 = 0, 0.0, None, []
+        while True:
+            t0 = time.perf_counter()
+            orc.epochs_f32(prob.form, prob.n_rows, prob.n_cols, prob.ptr, prob.idx, prob.val, prob.y, prob.lam, seed,
+                           e32, 1, m32, s32)
+            el32 += time.perf_counter() - t0
+            e32 += 1
+            g = orc.objectives(prob.form, prob.n_rows, prob.n_cols, prob.ptr, prob.idx, prob.val, prob.y, prob.lam,
+                               m32.astype(np.float64))[2]
+            curve32.append(g)
+            if ttg32 is None and g <= 1e-3:
+                ttg32 = (e32, el32)
+            if el32 >= f32_budget_s or e32 >= 1000:
+                break
+        f32 = {"value": prob.nnz * e32 / el32, "unit": "nnz/s", "epochs_per_s": e32 / el32,
+               "sample": f"{e32} sequential fp32 epochs from the zero state ({el32:.1f} s of epoch time, same core)",
+               "time_to_gap_1e-3_s": ttg32[1] if ttg32 else None, "epochs_to_gap_1e-3": ttg32[0] if ttg32 else None,
+               "gap_curve": [float(f"{g:.3e}") for g in curve32[:12]]}
     os.sched_setaffinity(0, set(allowed))
     cpu = "unknown"
     try:
@@ -122,7 +148,7 @@ def cpu_baseline(prob, budget_s: float, seed: int):
             "cpu_model": cpu, "host_cores_visible": len(allowed),
             "epochs_per_s": epochs / el,
             "time_to_gap_1e-3_s": ttg[1] if ttg else None, "epochs_to_gap_1e-3": ttg[0] if ttg else None,
-            "gap_curve": [float(f"{g:.3e}") for g in curve[:12]]}
+            "gap_curve": [float(f"{g:.3e}") for g in curve[:12]], "fp32_sequential": f32}
 
 
 def main():
@@ -133,6 +159,8 @@ def main():
     ap.add_argument("--workload", default="sparse_ridge", choices=sorted(WORKLOADS))
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
+    ap.add_argument("--cpu-f32-seconds", type=float, default=8.0,
+                    help="budget of the single-precision sequential epochs timed beside the oracle (0: skip)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--max-gap-epochs", type=int, default=200)
     ap.add_argument("--gap-seconds", type=float, default=60.0,
@@ -289,7 +317,7 @@ def main():
         del src, dst
     if not args.no_cpu_baseline:
         print("# oracle on the host", file=sys.stderr, flush=True)
-        out["cpu_baseline"] = cpu_baseline(prob, args.cpu_seconds, args.seed)
+        out["cpu_baseline"] = cpu_baseline(prob, args.cpu_seconds, args.seed, args.cpu_f32_seconds)
     print(json.dumps(out), flush=True)
 
 

@@ -77,6 +77,8 @@ def lib():
             f = getattr(L, name)
             f.restype = None
             f.argtypes = [_i64, _i64, _p, _p, _p, _p, _dbl, _u64, _i64, _i32, _p, _p]
+        L.oracle_epochs_f32.restype = None
+        L.oracle_epochs_f32.argtypes = [ctypes.c_int, _i64, _i64, _p, _p, _p, _p, _dbl, _u64, _i64, _i32, _p, _p]
         for name in ("oracle_ridge_primal_objectives", "oracle_ridge_dual_objectives",
                      "oracle_svm_dual_objectives"):
             f = getattr(L, name)
@@ -205,6 +207,22 @@ def epochs(form, n_rows, n_cols, ptr, idx, val, y, lam, seed, epoch0, n_epochs, 
     f = getattr(lib(), _FORMS[form][1])
     f(n_rows, n_cols, _ptr(ptr), _ptr(idx), _ptr(val), _ptr(y), lam, seed & 0xFFFFFFFFFFFFFFFF,
       epoch0, n_epochs, _ptr(model), _ptr(shared))
+
+
+_F32_FORMS = {"ridge_primal": 0, "svm_dual": 1, "ridge_dual": 2}
+
+
+def epochs_f32(form, n_rows, n_cols, ptr, idx, val, y, lam, seed, epoch0, n_epochs, model, shared):
+    """Alg. 1 in single precision (the paper's CPU baseline precision), for timing only:
+    ``model`` and ``shared`` are float32 arrays updated in place."""
+    ptr, idx, val = _seg(ptr, idx, val)
+    y = np.ascontiguousarray(y, dtype=np.float32)
+    C, L = _dims(form, n_rows, n_cols)
+    for a, n, what in ((model, C, "model"), (shared, L, "shared")):
+        if not (isinstance(a, np.ndarray) and a.dtype == np.float32 and a.flags.c_contiguous and a.shape == (n,)):
+            raise ValueError(f"{what} must be a contiguous float32 array of length {n}")
+    lib().oracle_epochs_f32(_F32_FORMS[form], n_rows, n_cols, _ptr(ptr), _ptr(idx), _ptr(val), _ptr(y), lam,
+                            seed & 0xFFFFFFFFFFFFFFFF, epoch0, n_epochs, _ptr(model), _ptr(shared))
 
 
 def objectives(form, n_rows, n_cols, ptr, idx, val, y, lam, model, shared=None):

@@ -27,7 +27,8 @@
  * balanced Feistel network with cycle-walking, SplitMix64-derived round keys and the
  * MurmurHash3 32-bit finaliser as round function) is written out in full below.
  *
- * All arithmetic is IEEE double.  fp32 inputs are promoted exactly.
+ * All arithmetic is IEEE double, except in oracle_epochs_f32 (a single-precision
+ * copy of the epochs, for timing only).  fp32 inputs are promoted exactly.
  */
 #include <math.h>
 #include <stddef.h>
@@ -288,6 +289,70 @@ void oracle_svm_dual_epochs(int64_t N, int64_t M, const int64_t *row_ptr, const 
     for (int32_t e = 0; e < n_epochs; ++e) {
         oracle_permutation(seed, (uint64_t)(epoch0 + e), N, order);
         oracle_svm_dual_visit(N, row_ptr, col_idx, val, y, lambda, order, N, norms, alpha, w);
+    }
+    free(order);
+    free(norms);
+}
+
+/* ------------------------------------------------------------------------- */
+/* The same sequential epochs in single precision (timing reference).         */
+/* ------------------------------------------------------------------------- */
+
+/* The paper computes in single precision on the CPU and the GPU (Sec. III-A, III-C)
+ * and quotes its speed-ups against one thread running Alg. 1.  This is Alg. 1 once
+ * more, with the model, the shared vector, the norms and every operation in float,
+ * so that that baseline can be timed; the correctness reference is the fp64 code
+ * above.  form: 0 ridge primal (CSC columns), 1 hinge SVM dual (CSR rows),
+ * 2 ridge dual (CSR rows).  The steps are those of the three visit functions above. */
+void oracle_epochs_f32(int form, int64_t N, int64_t M, const int64_t *ptr, const int32_t *idx,
+                       const float *val, const float *y, double lambda, uint64_t seed,
+                       int64_t epoch0, int32_t n_epochs, float *model, float *shared)
+{
+    int64_t C = form == 0 ? M : N;
+    float lN = (float)(lambda * (double)N);
+    float lam = (float)lambda;
+    float *norms = (float *)malloc(sizeof(float) * (size_t)(C > 0 ? C : 1));
+    int64_t *order = (int64_t *)malloc(sizeof(int64_t) * (size_t)(C > 0 ? C : 1));
+    for (int64_t c = 0; c < C; ++c) {
+        float s = 0.0f;
+        for (int64_t k = ptr[c]; k < ptr[c + 1]; ++k)
+            s += val[k] * val[k];
+        norms[c] = s;
+    }
+    for (int32_t e = 0; e < n_epochs; ++e) {
+        oracle_permutation(seed, (uint64_t)(epoch0 + e), C, order);
+        for (int64_t t = 0; t < C; ++t) {
+            int64_t m = order[t];
+            float g = 0.0f, coef;
+            if (form == 0) {
+                for (int64_t k = ptr[m]; k < ptr[m + 1]; ++k)
+                    g += (y[idx[k]] - shared[idx[k]]) * val[k];
+                float d = (g - lN * model[m]) / (norms[m] + lN);
+                model[m] += d;
+                coef = d;
+            } else if (form == 1) {
+                for (int64_t k = ptr[m]; k < ptr[m + 1]; ++k)
+                    g += shared[idx[k]] * val[k];
+                float a = 1.0f;
+                if (norms[m] > 0.0f) {
+                    a = model[m] + lN * (1.0f - y[m] * g) / norms[m];
+                    if (a < 0.0f)
+                        a = 0.0f;
+                    if (a > 1.0f)
+                        a = 1.0f;
+                }
+                coef = (a - model[m]) * y[m] / lN;
+                model[m] = a;
+            } else {
+                for (int64_t k = ptr[m]; k < ptr[m + 1]; ++k)
+                    g += shared[idx[k]] * val[k];
+                float d = (lam * y[m] - g - lN * model[m]) / (lN + norms[m]);
+                model[m] += d;
+                coef = d;
+            }
+            for (int64_t k = ptr[m]; k < ptr[m + 1]; ++k)
+                shared[idx[k]] += val[k] * coef;
+        }
     }
     free(order);
     free(norms);

@@ -9,7 +9,7 @@ import pytest
 
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 SRC = os.path.join(ROOT, "oracle", "scd_oracle.c")
-PINS = ["tests/test_oracle_perm.py", "tests/test_oracle_ridge.py", "tests/test_oracle_svm.py"]
+PINS = ["tests/test_oracle_perm.py", "tests/test_oracle_ridge.py", "tests/test_oracle_svm.py", "tests/test_oracle_f32.py"]
 
 MUTANTS = {
     "primal_drops_regulariser": ("double d = (g - lN * beta[m]) / (norms[m] + lN);",
@@ -33,6 +33,11 @@ MUTANTS = {
     "keys_ignore_epoch": ("uint64_t base = oracle_splitmix64_nth(seed, epoch + 1);",
                           "uint64_t base = oracle_splitmix64_nth(seed, 1);"),
     "fmix_constant": ("h *= 0xC2B2AE35U;", "h *= 0xC2B2AE37U;"),
+    "f32_primal_drops_regulariser": ("float d = (g - lN * model[m]) / (norms[m] + lN);",
+                                     "float d = (g) / (norms[m] + lN);"),
+    "f32_dual_drops_lambda_y": ("float d = (lam * y[m] - g - lN * model[m]) / (lN + norms[m]);",
+                                "float d = (y[m] - g - lN * model[m]) / (lN + norms[m]);"),
+    "f32_svm_scatter_drops_label": ("coef = (a - model[m]) * y[m] / lN;", "coef = (a - model[m]) / lN;"),
 }
 
 
