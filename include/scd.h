@@ -200,6 +200,12 @@ int scd_set_state(scd_handle_t h, const float *model_dev, const float *shared_de
  *                 (shared vector below 2 GiB; with skewed segment lengths only when each
  *                 in-flight coordinate can have a workgroup of its own, then with workgroups
  *                 taking positions from a queue), 0 = the plain kernels.
+ *   "spread"      1 (default) = when the shared vector has at most 4 M entries and the window
+ *                 does not bind (every coordinate may be in flight), the pipelined kernel runs on a
+ *                 copy that holds one entry per 64 bytes (scd_epochs copies it out before its
+ *                 epochs and back after them, on the same stream), so that the gathers of one
+ *                 coordinate do not wait behind other coordinates' atomics on neighbouring
+ *                 entries; 0 = it runs on the packed vector.
  *   "queue_chunk" consecutive permutation positions each workgroup of the queued kernel claims
  *                 at a time: 0 (default) = 1 per 64 coordinates in flight (at least 1), else
  *                 1..64.  Larger chunks lower the claim rate on the queue's counter and let

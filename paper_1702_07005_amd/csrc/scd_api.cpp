@@ -75,6 +75,8 @@ constexpr int kProbes = 8;                // Hutchinson probes of the coupling e
 constexpr uint32_t kWideHits = 28000;
 // The pipelined kernel addresses the shared vector as a raw buffer (byte offsets below 2^31).
 constexpr int64_t kPipeMaxBytes = (int64_t(1) << 31) - 8;
+// Largest spread copy of the shared vector (64 bytes per entry: up to 4 M entries).
+constexpr int64_t kSpreadMaxBytes = int64_t(256) << 20;
 // Hot-set kernel: hot entries kept in LDS (sized for an fp64 shared vector next to the largest
 // batch buffers), minimum share of stored entries they must cover, and the bound on its waits
 // (sleeps of about 64 cycles each: about half a second).
@@ -120,6 +122,9 @@ struct scd_solver {
     int64_t fresh = 0;
     int64_t pipeline = 1;
     int64_t queue_chunk = 0;  // option: positions per queue claim, 0 = by window
+    int64_t spread = 1;       // option: run an unbound pipelined plan on the spread copy
+    void* us = nullptr;       // spread copy of the shared vector (entry i at byte i << kSpreadShift),
+                              // allocated at create when it takes at most kSpreadMaxBytes
     double* sink = nullptr;  // pipelined kernel, fp64 shared vector: slots inactive lanes add 0 to
     uint32_t* queue = nullptr;  // queued kernel: next position, workgroups finished (zero between launches)
     // Hot-set kernel (windows of at most kHotMaxWindow): built on first need.
@@ -243,6 +248,7 @@ int plan_epoch(const scd_solver* h, LaunchPlan* lp, uint32_t* n_groups) {
         if (pipe_ok) groups = pipe_groups(h, window, groups);
         lp->kind = pipe_ok ? PLAN_PIPE : PLAN_BLOCK;
         lp->drain = pipe_ok ? pipe_drain(h, window, groups) : 0;
+        lp->unbound = window >= h->C;
         lp->group = kBlockThreads;
         lp->blocks = (int)groups;
         *n_groups = (uint32_t)groups;
@@ -290,6 +296,7 @@ int plan_epoch(const scd_solver* h, LaunchPlan* lp, uint32_t* n_groups) {
         groups = pipe_groups(h, window, groups);
         lp->kind = PLAN_PIPE;  // segments beyond the slices take its long path
         lp->drain = pipe_drain(h, window, groups);
+        lp->unbound = window >= h->C;
     }
     lp->group = G;
     lp->blocks = (int)((groups + per_block - 1) / per_block);
@@ -450,6 +457,7 @@ void release(scd_solver* h) {
     (void)hipFree(h->partials);
     (void)hipFree(h->sums);
     (void)hipFree(h->sink);
+    (void)hipFree(h->us);
     (void)hipFree(h->queue);
     (void)hipFree(h->entry_key);
     (void)hipFree(h->hot_ids);
@@ -598,6 +606,7 @@ int scd_create(const scd_matrix_t* A, const float* y, double lambda, int32_t for
         hip(hipMalloc(&h->sink, sink_bytes), "hipMalloc(sink)");
         hip(hipMemsetAsync(h->sink, 0, sink_bytes, s), "zero sink");
         hip(hipMalloc(&h->queue, 2 * sizeof(uint32_t)), "hipMalloc(queue)");
+        if ((h->L << kSpreadShift) <= kSpreadMaxBytes) hip(hipMalloc(&h->us, (size_t)h->L << kSpreadShift), "hipMalloc(spread)");
         hip(hipMemsetAsync(h->queue, 0, 2 * sizeof(uint32_t), s), "zero queue");
     }
     hip(hipHostMalloc(&h->host_sums, sizeof(double) * 8, hipHostMallocDefault), "hipHostMalloc");
@@ -734,11 +743,26 @@ int scd_epochs(scd_handle_t h, uint64_t seed, int32_t n_epochs, void* stream) {
     a.k.lam = (float)h->lambda;
     a.n_groups = n_groups;
     a.u_bytes = shared_bytes(h) <= kPipeMaxBytes ? (uint32_t)shared_bytes(h) : 0u;
+    a.u_shift = h->wide ? 3u : 2u;
+    // With every coordinate in flight (the window does not bind) the pipelined kernel runs on the
+    // spread copy when there is one: packed, the gathers of entries whose 64-byte segment other
+    // coordinates' atomics are updating wait behind those atomics (measured: gather-and-atomic
+    // pairs on 100,000 packed fp32 entries at 9.5 G/s, spread one per 64 bytes at 20 G/s, the rate
+    // of the atomics alone).  With a binding window the epoch is bound by the latency of the
+    // coordinates in flight instead, and a coordinate that gathers many neighbouring entries (a
+    // dense column) would touch one segment per entry instead of one per 16.
+    const bool spread = h->us && h->spread && lp.kind == PLAN_PIPE && lp.unbound && n_epochs > 0;
+    if (spread) {
+        a.u = h->us;
+        a.u_bytes = (uint32_t)(h->L << kSpreadShift);
+        a.u_shift = kSpreadShift;
+    }
     a.sink = h->sink;
     a.drain = (uint32_t)lp.drain;
     a.queue = h->queue;
     a.chunk = (uint32_t)std::max(1, lp.chunk);
     hipStream_t s = (hipStream_t)stream;
+    if (spread) HIP_TRY(launch_spread(h->u, h->us, h->L, h->wide != 0, true, s));
     for (int32_t e = 0; e < n_epochs; ++e) {
         a.perm = make_perm(seed, (uint64_t)h->epoch, (uint32_t)h->C);
         if (lp.kind == PLAN_HOT) {
@@ -759,6 +783,7 @@ int scd_epochs(scd_handle_t h, uint64_t seed, int32_t n_epochs, void* stream) {
         }
         ++h->epoch;
     }
+    if (spread) HIP_TRY(launch_spread(h->u, h->us, h->L, h->wide != 0, false, s));
     return SCD_OK;
 }
 
@@ -872,6 +897,9 @@ int scd_set_option(scd_handle_t h, const char* key, int64_t value) {
     } else if (!strcmp(key, "pipeline")) {
         if (value != 0 && value != 1) return fail(SCD_ERR_INVALID, "pipeline must be 0 or 1");
         h->pipeline = value;
+    } else if (!strcmp(key, "spread")) {
+        if (value != 0 && value != 1) return fail(SCD_ERR_INVALID, "spread must be 0 or 1");
+        h->spread = value;
     } else if (!strcmp(key, "queue_chunk")) {
         if (value < 0 || value > (int64_t)kQueueChunkMax) return fail(SCD_ERR_INVALID, "queue_chunk must be in [0, 64]");
         h->queue_chunk = value;
@@ -907,6 +935,7 @@ int scd_get_option(scd_handle_t h, const char* key, int64_t* value) {
     else if (!strcmp(key, "group")) *value = h->group;
     else if (!strcmp(key, "fresh_reads")) *value = h->fresh;
     else if (!strcmp(key, "pipeline")) *value = h->pipeline;
+    else if (!strcmp(key, "spread")) *value = h->spread;
     else if (!strcmp(key, "queue_chunk")) *value = h->queue_chunk;
     else if (!strcmp(key, "hot")) *value = h->hot;
     else if (!strcmp(key, "hot_wait_limit")) *value = h->hot_wait_limit;

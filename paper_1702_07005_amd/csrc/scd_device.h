@@ -193,19 +193,21 @@ struct SharedBuf {
     uint32_t oob;  // first out-of-range byte offset
     U* base;
     U* sink;       // fp64 only: this lane's scratch slot
+    uint32_t shift;  // log2 of the bytes between consecutive entries
 };
 
 template <typename U>
-__device__ __forceinline__ SharedBuf<U> shared_buf(void* u, uint32_t bytes, U* sink) {
+__device__ __forceinline__ SharedBuf<U> shared_buf(void* u, uint32_t bytes, U* sink, uint32_t shift) {
     // word 3 = 0x00020000: 32-bit data format, the gfx9-family raw-buffer setting.
-    return {__builtin_amdgcn_make_buffer_rsrc(u, (short)0, (int)bytes, 0x00020000), bytes, static_cast<U*>(u), sink};
+    return {__builtin_amdgcn_make_buffer_rsrc(u, (short)0, (int)bytes, 0x00020000), bytes, static_cast<U*>(u), sink,
+            shift};
 }
 
 template <bool FRESH, typename U>
 __device__ __forceinline__ float buf_load(const SharedBuf<U>& b, uint32_t i, bool in) {
     // cache policy 16 = sc1: device-scope load, as __hip_atomic_load at agent scope emits.
     constexpr int pol = FRESH ? 16 : 0;
-    const uint32_t off = in ? i * (uint32_t)sizeof(U) : b.oob;
+    const uint32_t off = in ? i << b.shift : b.oob;
     if constexpr (sizeof(U) == 4) {
         return __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(b.r, (int)off, 0, pol));
     } else {
@@ -217,9 +219,9 @@ __device__ __forceinline__ float buf_load(const SharedBuf<U>& b, uint32_t i, boo
 template <typename U>
 __device__ __forceinline__ void buf_atomic_add(const SharedBuf<U>& b, uint32_t i, bool in, float v) {
     if constexpr (sizeof(U) == 4) {
-        (void)__builtin_amdgcn_raw_ptr_buffer_atomic_fadd_f32(v, b.r, (int)(in ? i * 4u : b.oob), 0, 0);
+        (void)__builtin_amdgcn_raw_ptr_buffer_atomic_fadd_f32(v, b.r, (int)(in ? i << b.shift : b.oob), 0, 0);
     } else {
-        U* p = in ? b.base + i : b.sink;
+        U* p = in ? reinterpret_cast<U*>(reinterpret_cast<char*>(b.base) + ((size_t)i << b.shift)) : b.sink;
         __hip_atomic_fetch_add(p, in ? (double)v : 0.0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     }
 }

@@ -192,7 +192,7 @@ __global__ __launch_bounds__(256) void k_epoch_pipe(EpochArgs a) {
     const uint32_t gid = (blockIdx.x * 256u + threadIdx.x) / G;
     if (gid >= a.n_groups || gid >= a.perm.n) return;  // G = 256: the whole workgroup leaves
     const SharedBuf<U> ub =
-        shared_buf<U>(a.u, a.u_bytes, reinterpret_cast<U*>(a.sink) + (size_t)blockIdx.x * 256 + threadIdx.x);
+        shared_buf<U>(a.u, a.u_bytes, reinterpret_cast<U*>(a.sink) + (size_t)blockIdx.x * 256 + threadIdx.x, a.u_shift);
     const uint32_t P = a.n_groups;
     uint32_t j = gid;
     int buf = 0;
@@ -337,7 +337,8 @@ __global__ __launch_bounds__(256) void k_epoch_queue(EpochArgs a) {
     uint32_t pA = queue_pos(ring, 0, K), pB = queue_pos(ring, 1, K);
     if (pA < n) {
         const SharedBuf<U> ub =
-            shared_buf<U>(a.u, a.u_bytes, reinterpret_cast<U*>(a.sink) + (size_t)blockIdx.x * 256 + threadIdx.x);
+            shared_buf<U>(a.u, a.u_bytes, reinterpret_cast<U*>(a.sink) + (size_t)blockIdx.x * 256 + threadIdx.x,
+                          a.u_shift);
         int buf = 0;
         uint32_t claim = 0, k = 0;
         CoordMeta cA = load_meta_of(a, perm_at(pA, a.perm));

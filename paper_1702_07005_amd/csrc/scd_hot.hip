@@ -215,7 +215,7 @@ __device__ __forceinline__ void hot_meta_load(const EpochArgs& a, HotMeta& t) {
 // the memory operations behind an earlier load stays exact.
 template <typename U>
 __device__ __forceinline__ U hot_load_u(const SharedBuf<U>& b, uint32_t i, bool in) {
-    const uint32_t off = in ? i * (uint32_t)sizeof(U) : b.oob;
+    const uint32_t off = in ? i << b.shift : b.oob;
     if constexpr (sizeof(U) == 4)
         return __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(b.r, (int)off, 0, 0));
     else
@@ -238,7 +238,7 @@ __device__ __forceinline__ void hot_producer(const HotArgs& h, uint32_t* ready, 
                                              uint32_t* bufs, uint32_t nb, int q, int lane) {
     const EpochArgs& a = h.e;
     U* const uu = static_cast<U*>(a.u);
-    const SharedBuf<U> ub = shared_buf<U>(a.u, a.u_bytes, nullptr);
+    const SharedBuf<U> ub = shared_buf<U>(a.u, a.u_bytes, nullptr, a.u_shift);
     const uint32_t B = h.B, Smax = h.Smax, NB = B * Smax;
     const HotBuf hb = hot_buf(bufs + q * hot_buf_words(B, Smax), B, Smax);
     constexpr int NE = kHotEntriesPerLane;

@@ -41,6 +41,8 @@ struct EpochArgs {
     PermKeys perm;       // perm.n = C
     uint32_t n_groups;   // persistent groups (coordinates in flight at most)
     uint32_t u_bytes;    // byte size of the shared vector when below 2^31 (raw-buffer range), else 0
+    uint32_t u_shift;    // log2 of the bytes from one shared-vector entry to the next in u: the
+                         // entry size (2 or 3), or kSpreadShift when u is the spread copy
     double* sink;        // pipelined kernel, fp64 shared vector: 256 slots per workgroup that
                          // inactive lanes add 0 to
     uint32_t drain;      // pipelined kernel: wait for the group's own atomics before its next gathers
@@ -50,6 +52,9 @@ struct EpochArgs {
 };
 
 constexpr uint32_t kQueueChunkMax = 64;
+// Spread copy of a small shared vector for the pipelined and queued kernels: one entry per 64
+// bytes, so that concurrent gathers and atomics of different entries never share a segment.
+constexpr uint32_t kSpreadShift = 6;
 constexpr int kQueueSlices = 16;  // register slices per lane of the queued kernel (256 x 16 entries held)
 
 enum { PLAN_GROUP = 0, PLAN_BLOCK = 1, PLAN_ORDERED_LDS = 2, PLAN_MIXED = 3, PLAN_PIPE = 4, PLAN_HOT = 5, PLAN_QUEUE = 6 };
@@ -66,6 +71,7 @@ struct LaunchPlan {
     int drain;          // PLAN_PIPE: the window binds, so each group lets its scatter land before it gathers again
     int chunk;          // PLAN_QUEUE: consecutive permutation positions per claim
     int wide;           // shared vector stored as double
+    int unbound;        // PLAN_PIPE: the window does not bind (every coordinate may be in flight)
     size_t lds_bytes;
 };
 
@@ -135,6 +141,8 @@ hipError_t launch_count_hits(const int32_t* idx, int64_t nnz, unsigned* hits, hi
 hipError_t launch_hot_entry_keys(const int32_t* idx, int64_t nnz, const uint16_t* slot_of, int32_t* entry_key,
                                   hipStream_t s);
 hipError_t launch_perm_fill(const PermKeys& p, int32_t* out, hipStream_t s);
+// Copies the packed shared vector into its spread copy (entry i at byte i << kSpreadShift), or back.
+hipError_t launch_spread(void* packed, void* spread, int64_t L, bool wide, bool to_spread, hipStream_t s);
 hipError_t launch_gather_dots(const int64_t* ptr, const int32_t* idx, const float* val, const float* u, uint32_t C,
                               int G, int blocks, float* out, hipStream_t s);
 hipError_t launch_norms(const int64_t* ptr, const int32_t* idx, const float* val, const float* y, uint32_t C, int G,

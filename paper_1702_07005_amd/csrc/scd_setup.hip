@@ -274,6 +274,30 @@ __global__ __launch_bounds__(256) void k_sum_partials(const double* __restrict__
         for (int w = 0; w < width; ++w) out[w] = ((sh[0][w] + sh[1][w]) + sh[2][w]) + sh[3][w];
 }
 
+// Packed shared vector <-> its spread copy (entry i at byte offset i << kSpreadShift of the copy; the
+// bytes between entries are never read).
+template <typename U>
+__global__ __launch_bounds__(256) void k_spread(U* __restrict__ packed, U* __restrict__ spread, int64_t L,
+                                                bool to_spread) {
+    constexpr uint32_t step = (1u << kSpreadShift) / sizeof(U);
+    for (int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x; i < L; i += (int64_t)gridDim.x * 256) {
+        if (to_spread)
+            spread[i * step] = packed[i];
+        else
+            packed[i] = spread[i * step];
+    }
+}
+
+hipError_t launch_spread(void* packed, void* spread, int64_t L, bool wide, bool to_spread, hipStream_t s) {
+    if (wide)
+        hipLaunchKernelGGL(k_spread<double>, dim3(grid_for(L)), dim3(256), 0, s, static_cast<double*>(packed),
+                           static_cast<double*>(spread), L, to_spread);
+    else
+        hipLaunchKernelGGL(k_spread<float>, dim3(grid_for(L)), dim3(256), 0, s, static_cast<float*>(packed),
+                           static_cast<float*>(spread), L, to_spread);
+    return hipGetLastError();
+}
+
 hipError_t launch_perm_fill(const PermKeys& p, int32_t* out, hipStream_t s) {
     const uint32_t blocks = (p.n + 255) / 256;
     hipLaunchKernelGGL(k_perm_fill, dim3(blocks), dim3(256), 0, s, p, out);

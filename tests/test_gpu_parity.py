@@ -525,6 +525,33 @@ def test_hot_set_kernel_parity(case):
     s.close()
 
 
+@pytest.mark.parametrize("wide", [0, 1])
+@pytest.mark.parametrize("spread", [0, 1])
+def test_spread_copy_parity(spread, wide):
+    # Every coordinate in flight: the pipelined kernel runs on the copy with one entry per 64 bytes
+    # (fp32: raw-buffer gathers and atomics; fp64: gathers through the buffer, global atomics), and
+    # scd_epochs writes it back to the packed vector that the state and objective calls read.
+    p = problem("sparse_ridge_small")
+    E = 3
+    _, _, curve = _oracle_curve(p, 0, E)
+    s = scd.solver_for(p)
+    s.set_option("spread", spread)
+    s.set_option("shared_fp64", wide)
+    assert s.get_option("spread") == spread and s.info()["kernel"] == "pipelined" and s.info()["window"] == p.C
+    P0, _ = s.objective()
+    for e in range(E):
+        s.epochs(0, 1)
+        gm, gs, ep = s.get_state()
+        assert ep == e + 1
+        assert rel_inf(f64(gs), fresh(p, f64(gm))) <= 1e-4, e
+        G, Gr = s.duality_gap(), curve[e][2]
+        if Gr > 1e-6 * abs(P0):
+            assert G <= 2.0 * Gr, (e, G, Gr)
+    with pytest.raises(scd.ScdError):
+        s.set_option("spread", 2)
+    s.close()
+
+
 def test_hot_set_cold_entry_at_index_zero():
     # The hot-set kernel keys a cold entry by ~index, so shared-vector entry 0 has key -1, the key of
     # padding slots too (those have value 0).  Move a column with 8 stored entries (far below the
