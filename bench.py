@@ -66,14 +66,19 @@ def measured_traffic(workload: str):
 
 def device_ceilings(L: int):
     """Live device-wide rates on this GPU (libscdprobe.so): scattered fp32 atomic adds into an array
-    the size of the shared vector, the same when each add follows a gather from that array, and
-    a 1 GiB streaming copy."""
+    the size of the shared vector; independent gathers from and atomic adds into that array (pairs
+    per second), packed and with one entry per 64 bytes (the spread copy, for up to 4 M entries);
+    and a 1 GiB streaming copy."""
     import ctypes
     lib = ctypes.CDLL(os.path.join(ROOT, "paper_1702_07005_amd", "libscdprobe.so"))
     lib.scd_probe_rate.argtypes = [ctypes.c_int, ctypes.c_uint64, ctypes.c_void_p, ctypes.POINTER(ctypes.c_double)]
     out = {}
-    for mode, key, n in ((0, "atomic_adds_per_s", max(L, 1024)), (1, "gather_then_atomic_per_s", max(L, 1024)),
-                         (2, "copy_bytes_per_s", 1 << 28)):
+    n = max(L, 1024)
+    modes = [(0, "atomic_adds_per_s", n), (1, "gather_and_atomic_pairs_per_s", n)]
+    if n <= (1 << 22):
+        modes.append((3, "gather_and_atomic_pairs_spread_per_s", n))
+    modes.append((2, "copy_bytes_per_s", 1 << 28))
+    for mode, key, n in modes:
         v = ctypes.c_double()
         rc = lib.scd_probe_rate(mode, n, None, ctypes.byref(v))
         out[key] = v.value if rc == 0 else None
@@ -305,7 +310,9 @@ def main():
         out["atomic_roofline"] = {"bound": "device-scope fp32 atomics", "achieved": rate,
                                   "peak": ceil["atomic_adds_per_s"], "unit": "atomic adds/s",
                                   "frac": rate / ceil["atomic_adds_per_s"],
-                                  "gather_then_atomic_per_s": ceil["gather_then_atomic_per_s"],
+                                  "gather_and_atomic_pairs_per_s": ceil["gather_and_atomic_pairs_per_s"],
+                                  "gather_and_atomic_pairs_spread_per_s":
+                                      ceil.get("gather_and_atomic_pairs_spread_per_s"),
                                   "copy_GBps": (ceil["copy_bytes_per_s"] or 0) / 1e9}
     if args.calibrate_copy:
         src = torch.ones(1 << 28, dtype=torch.float32, device=dev)  # 1 GiB
