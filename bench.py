@@ -45,7 +45,8 @@ def algorithmic_bytes(prob) -> int:
 
 def kernel_source_hash() -> str:
     h = hashlib.sha256()
-    for f in ("scd_device.h", "scd_epoch.hip", "scd_hot.hip", "scd_setup.hip", "scd_kernels.h", "scd_api.cpp"):
+    for f in ("scd_device.h", "scd_epoch.hip", "scd_hot.hip", "scd_team.hip", "scd_setup.hip", "scd_kernels.h",
+              "scd_api.cpp"):
         with open(os.path.join(ROOT, "paper_1702_07005_amd", "csrc", f), "rb") as fh:
             h.update(fh.read())
     return h.hexdigest()[:16]

@@ -82,6 +82,11 @@ constexpr int64_t kSpreadMaxBytes = int64_t(256) << 20;
 // (sleeps of about 64 cycles each: about half a second).
 constexpr double kHotMinCover = 0.1;
 constexpr uint32_t kHotSpinLimit = 1u << 24;
+// Team kernel, automatic choice: segments of at least this many entries on average, and a shared
+// vector of at least this many bytes (its gathers miss L2, so a coordinate's time in one workgroup
+// is set by that CU's outstanding misses).
+constexpr double kTeamMinMean = 1024.0;
+constexpr int64_t kTeamMinSharedBytes = int64_t(16) << 20;
 
 }  // namespace
 
@@ -137,6 +142,15 @@ struct scd_solver {
     int* hot_err = nullptr;       // device flag set by a timed-out wait in the hot-set kernel
     int64_t hot_wait_limit = 0;   // option (test hook): sleeps per wait before giving up, 0 = kHotSpinLimit
     int* err_host = nullptr;      // pinned copies of hot_err: one per gap slot + one for reduce_state
+    // Team kernel (long segments, few coordinates in flight): tables built on first need for K.
+    int64_t team = 1;             // option: 0 never, 1 automatic, 2..kTeamMax members forced
+    int team_k = 0;               // K of the built tables (0 = none)
+    int32_t* team_idx = nullptr;  // [nnz]: segment entries grouped by index range
+    float* team_val = nullptr;    // [nnz]
+    uint32_t* team_off = nullptr;  // [C * (K + 1)]
+    uint32_t* team_bound = nullptr;  // [K + 1]
+    uint64_t* team_slots = nullptr;  // [cus * 2 * kTeamMax] partial-sum slots (tag 0 at allocation)
+    uint32_t team_tag = 1;        // tag of the next team step
 };
 
 namespace {
@@ -204,6 +218,34 @@ bool hot_plan(const scd_solver* h, int64_t window, HotGeom* g) {
            shared_bytes(h) <= kPipeMaxBytes && hot_geometry(h, window, g) && g->lds <= h->max_lds;
 }
 
+// Members per in-flight coordinate of the team kernel for the current options, and the number of
+// teams (0 = the team kernel does not apply).  Teams hold one coordinate each between gather and
+// scatter, as draining pipelined groups do, and take the same share of the window.
+int team_members(const scd_solver* h, int64_t* teams) {
+    const int64_t window = h->window ? h->window : h->auto_window;
+    if (h->team == 0 || !h->pipeline || h->group != 0 || shared_bytes(h) > kPipeMaxBytes || window < 2 ||
+        window >= h->C || h->max_seg >= (int64_t(1) << 32) || h->cus < 2)
+        return 0;
+    int64_t groups = pipe_groups(h, window, std::min<int64_t>(window, (int64_t)h->cus));
+    // A team's coordinate stays between its gather and its scatter for a larger part of each step
+    // than a pipelined group's (the exchange of partial sums sits in that interval): on the
+    // text-SVM twin (3,500 x 166,000) the worst per-epoch gap ratio to the sequential algorithm
+    // at a team window of 6 matched the pipelined kernel's at about 8.  With the automatic window
+    // teams therefore take 3/4 of the pipelined share.
+    if (h->window == 0) groups = std::max<int64_t>(1, groups * 3 / 4);
+    int64_t K;
+    if (h->team >= 2) {
+        K = h->team;
+    } else {
+        const double mean = (double)h->nnz / (double)h->C;
+        if (mean < kTeamMinMean || shared_bytes(h) < kTeamMinSharedBytes) return 0;
+        K = std::min<int64_t>(kTeamMax, h->cus / groups);
+    }
+    if (K < 2 || groups * K > h->cus) return 0;
+    *teams = groups;
+    return (int)K;
+}
+
 int plan_epoch(const scd_solver* h, LaunchPlan* lp, uint32_t* n_groups) {
     memset(lp, 0, sizeof *lp);
     lp->fresh = (int)h->fresh;
@@ -226,6 +268,19 @@ int plan_epoch(const scd_solver* h, LaunchPlan* lp, uint32_t* n_groups) {
         lp->fresh = 1;
         lp->blocks = 1;
         *n_groups = 1;
+        return SCD_OK;
+    }
+    // The team kernel first: chosen automatically only for long segments (which the hot-set kernel
+    // never takes), and an explicit "team" option is taken as given.
+    int64_t teams = 0;
+    const int K = team_members(h, &teams);
+    if (K && h->team_k == K) {
+        lp->kind = PLAN_TEAM;
+        lp->team = K;
+        lp->group = kBlockThreads;
+        lp->drain = 1;
+        lp->blocks = (int)(teams * K);
+        *n_groups = (uint32_t)teams;
         return SCD_OK;
     }
     HotGeom hg;
@@ -416,8 +471,92 @@ int hot_if_needed(scd_solver* h, hipStream_t s) {
     return build_hot_tables(h, s);
 }
 
+void free_team_tables(scd_solver* h) {
+    (void)hipFree(h->team_idx);
+    (void)hipFree(h->team_val);
+    (void)hipFree(h->team_off);
+    (void)hipFree(h->team_bound);
+    h->team_idx = nullptr;
+    h->team_val = nullptr;
+    h->team_off = nullptr;
+    h->team_bound = nullptr;
+    h->team_k = 0;
+}
+
+// Tables of the team kernel for K members: index-range bounds with about nnz/K stored entries per
+// range, and a copy of the segments with each segment's entries grouped by range.  Built once per
+// K, on first need (synchronises).  Without memory for the copy the team kernel is not used.
+int build_team_tables(scd_solver* h, int K, hipStream_t s) {
+    if (h->team_k == K) return SCD_OK;
+    free_team_tables(h);
+    size_t free_b = 0, total_b = 0;
+    HIP_TRY(hipMemGetInfo(&free_b, &total_b));
+    const size_t nnz1 = (size_t)std::max<int64_t>(h->nnz, 1);
+    const size_t need = nnz1 * 8 + (size_t)h->C * (K + 1) * 4 + sizeof(unsigned) * (size_t)h->L;
+    if (need + (size_t(1) << 30) > free_b) return SCD_OK;
+    if (!h->team_slots) {
+        const size_t sb = sizeof(uint64_t) * 2 * kTeamMax * (size_t)h->cus;
+        HIP_TRY(hipMalloc(&h->team_slots, sb));
+        HIP_TRY(hipMemsetAsync(h->team_slots, 0, sb, s));
+    }
+    unsigned* hits = nullptr;
+    int rc = SCD_OK;
+    auto hip = [&](hipError_t e, const char* what) {
+        if (rc == SCD_OK && e != hipSuccess) rc = fail(SCD_ERR_HIP, "%s: %s", what, hipGetErrorString(e));
+    };
+    hip(hipMalloc(&hits, sizeof(unsigned) * (size_t)h->L), "hipMalloc(team hits)");
+    hip(hipMalloc(&h->team_idx, sizeof(int32_t) * nnz1), "hipMalloc(team_idx)");
+    hip(hipMalloc(&h->team_val, sizeof(float) * nnz1), "hipMalloc(team_val)");
+    hip(hipMalloc(&h->team_off, sizeof(uint32_t) * (size_t)h->C * (K + 1)), "hipMalloc(team_off)");
+    hip(hipMalloc(&h->team_bound, sizeof(uint32_t) * (K + 1)), "hipMalloc(team_bound)");
+    std::vector<unsigned> hh;
+    if (rc == SCD_OK) {
+        hip(hipMemsetAsync(hits, 0, sizeof(unsigned) * (size_t)h->L, s), "zero team hits");
+        if (h->nnz > 0) hip(launch_count_hits(h->idx, h->nnz, hits, s), "count hits");
+        hh.resize((size_t)h->L);
+        hip(hipMemcpyAsync(hh.data(), hits, sizeof(unsigned) * (size_t)h->L, hipMemcpyDeviceToHost, s), "copy hits");
+        hip(hipStreamSynchronize(s), "synchronize");
+    }
+    if (rc == SCD_OK) {
+        // bound[q] = the first index whose preceding entries number at least q * nnz / K.
+        std::vector<uint32_t> bound((size_t)K + 1, (uint32_t)h->L);
+        bound[0] = 0;
+        const double total = (double)h->nnz;
+        double cum = 0.0;
+        int q = 1;
+        for (int64_t i = 0; i < h->L && q < K; ++i) {
+            while (q < K && cum * K >= q * total) bound[(size_t)q++] = (uint32_t)i;
+            cum += hh[(size_t)i];
+        }
+        hip(hipMemcpyAsync(h->team_bound, bound.data(), sizeof(uint32_t) * (K + 1), hipMemcpyHostToDevice, s),
+            "copy team bounds");
+        hip(launch_team_partition(h->ptr, h->idx, h->val, (uint32_t)h->C, h->team_bound, K, h->team_idx, h->team_val,
+                                  h->team_off, s),
+            "team partition");
+        hip(hipStreamSynchronize(s), "synchronize");
+    }
+    (void)hipFree(hits);
+    if (rc != SCD_OK) {
+        free_team_tables(h);
+        return rc;
+    }
+    h->team_k = K;
+    return SCD_OK;
+}
+
+// Builds the team tables when the current options would use the team kernel.
+int team_if_needed(scd_solver* h, hipStream_t s) {
+    int64_t teams = 0;
+    const int K = team_members(h, &teams);
+    if (!K || h->team_k == K) return SCD_OK;
+    return build_team_tables(h, K, s);
+}
+
 int check_hot_err(int v) {
-    if (v) return fail(SCD_ERR_HIP, "hot-set epoch kernel: a wait between its waves timed out; the state is invalid");
+    if (v)
+        return fail(SCD_ERR_HIP,
+                    "epoch kernel: a bounded wait (between the hot-set kernel's waves or the team kernel's members) "
+                    "timed out; the state is invalid");
     return SCD_OK;
 }
 
@@ -462,6 +601,8 @@ void release(scd_solver* h) {
     (void)hipFree(h->entry_key);
     (void)hipFree(h->hot_ids);
     (void)hipFree(h->hot_err);
+    free_team_tables(h);
+    (void)hipFree(h->team_slots);
     (void)hipHostFree(h->err_host);
     if (h->host_sums) (void)hipHostFree(h->host_sums);
     if (h->slot_sums) (void)hipHostFree(h->slot_sums);
@@ -691,6 +832,7 @@ int scd_create(const scd_matrix_t* A, const float* y, double lambda, int32_t for
             h->auto_window = std::max<int64_t>(1, std::min<int64_t>(w, h->C));
         }
         if (rc == SCD_OK) step(hot_if_needed(h, s));
+        if (rc == SCD_OK) step(team_if_needed(h, s));
         hip(hipMemsetAsync(h->model, 0, sizeof(float) * (size_t)h->C, s), "zero model");
         hip(hipMemsetAsync(h->u, 0, (h->wide ? sizeof(double) : sizeof(float)) * (size_t)h->L, s), "zero shared");
         hip(hipStreamSynchronize(s), "synchronize");
@@ -765,7 +907,22 @@ int scd_epochs(scd_handle_t h, uint64_t seed, int32_t n_epochs, void* stream) {
     if (spread) HIP_TRY(launch_spread(h->u, h->us, h->L, h->wide != 0, true, s));
     for (int32_t e = 0; e < n_epochs; ++e) {
         a.perm = make_perm(seed, (uint64_t)h->epoch, (uint32_t)h->C);
-        if (lp.kind == PLAN_HOT) {
+        if (lp.kind == PLAN_TEAM) {
+            TeamArgs ta{};
+            ta.e = a;
+            ta.e.idx = h->team_idx;
+            ta.e.val = h->team_val;
+            ta.e.drain = 1;
+            ta.off = h->team_off;
+            ta.slots = h->team_slots;
+            ta.K = (uint32_t)lp.team;
+            ta.tag0 = h->team_tag;
+            ta.spin_limit = h->hot_wait_limit > 0 ? (uint32_t)h->hot_wait_limit : kHotSpinLimit;
+            ta.err = h->hot_err;
+            HIP_TRY(launch_epoch_team(h->form, h->wide != 0, lp.fresh != 0, ta, lp.blocks, s));
+            // Steps of the busiest team, plus one: the next launch's tags are all new.
+            h->team_tag += (uint32_t)((h->C + n_groups - 1) / n_groups + 1);
+        } else if (lp.kind == PLAN_HOT) {
             HotArgs ha{};
             ha.e = a;
             ha.entry_key = h->entry_key;
@@ -876,6 +1033,7 @@ int scd_set_option(scd_handle_t h, const char* key, int64_t value) {
         h->window = value;
         if (int r = set_device(h)) return r;
         if (int r = hot_if_needed(h, nullptr)) return r;
+        if (int r = team_if_needed(h, nullptr)) return r;
     } else if (!strcmp(key, "hot")) {
         if (value != 0 && value != 1) return fail(SCD_ERR_INVALID, "hot must be 0 or 1");
         h->hot = value;
@@ -888,6 +1046,12 @@ int scd_set_option(scd_handle_t h, const char* key, int64_t value) {
         h->group = value;
         if (int r = set_device(h)) return r;
         if (int r = hot_if_needed(h, nullptr)) return r;
+        if (int r = team_if_needed(h, nullptr)) return r;
+    } else if (!strcmp(key, "team")) {
+        if (value < 0 || value > kTeamMax) return fail(SCD_ERR_INVALID, "team must be in [0, %d]", kTeamMax);
+        h->team = value;
+        if (int r = set_device(h)) return r;
+        if (int r = team_if_needed(h, nullptr)) return r;
     } else if (!strcmp(key, "fresh_reads")) {
         if (value != 0 && value != 1) return fail(SCD_ERR_INVALID, "fresh_reads must be 0 or 1");
         h->fresh = value;
@@ -897,6 +1061,8 @@ int scd_set_option(scd_handle_t h, const char* key, int64_t value) {
     } else if (!strcmp(key, "pipeline")) {
         if (value != 0 && value != 1) return fail(SCD_ERR_INVALID, "pipeline must be 0 or 1");
         h->pipeline = value;
+        if (int r = set_device(h)) return r;
+        if (int r = team_if_needed(h, nullptr)) return r;
     } else if (!strcmp(key, "spread")) {
         if (value != 0 && value != 1) return fail(SCD_ERR_INVALID, "spread must be 0 or 1");
         h->spread = value;
@@ -922,6 +1088,7 @@ int scd_set_option(scd_handle_t h, const char* key, int64_t value) {
         (void)hipFree(h->u);
         h->u = nu;
         h->wide = (int)value;
+        if (int r = team_if_needed(h, nullptr)) return r;
     } else {
         return fail(SCD_ERR_UNSUPPORTED, "unknown option '%s'", key);
     }
@@ -939,6 +1106,7 @@ int scd_get_option(scd_handle_t h, const char* key, int64_t* value) {
     else if (!strcmp(key, "queue_chunk")) *value = h->queue_chunk;
     else if (!strcmp(key, "hot")) *value = h->hot;
     else if (!strcmp(key, "hot_wait_limit")) *value = h->hot_wait_limit;
+    else if (!strcmp(key, "team")) *value = h->team;
     else if (!strcmp(key, "shared_fp64")) *value = h->wide;
     else return fail(SCD_ERR_UNSUPPORTED, "unknown option '%s'", key);
     return SCD_OK;
@@ -954,7 +1122,9 @@ int scd_get_info(scd_handle_t h, scd_info_t* info) {
     info->group_lanes = (lp.kind == PLAN_GROUP || lp.kind == PLAN_MIXED || lp.kind == PLAN_PIPE || lp.kind == PLAN_HOT ||
                          lp.kind == PLAN_QUEUE)
                             ? lp.group
-                        : lp.kind == PLAN_BLOCK && !lp.ordered ? kBlockThreads : 1024;
+                        : lp.kind == PLAN_TEAM                 ? kBlockThreads * lp.team
+                        : lp.kind == PLAN_BLOCK && !lp.ordered ? kBlockThreads
+                                                               : 1024;
     info->kernel = lp.kind;
     info->hot_entries = (int32_t)h->n_hot;
     info->long_len = lp.kind == PLAN_MIXED ? lp.long_len : 0;

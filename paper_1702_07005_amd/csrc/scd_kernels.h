@@ -57,7 +57,16 @@ constexpr uint32_t kQueueChunkMax = 64;
 constexpr uint32_t kSpreadShift = 6;
 constexpr int kQueueSlices = 16;  // register slices per lane of the queued kernel (256 x 16 entries held)
 
-enum { PLAN_GROUP = 0, PLAN_BLOCK = 1, PLAN_ORDERED_LDS = 2, PLAN_MIXED = 3, PLAN_PIPE = 4, PLAN_HOT = 5, PLAN_QUEUE = 6 };
+enum {
+    PLAN_GROUP = 0,
+    PLAN_BLOCK = 1,
+    PLAN_ORDERED_LDS = 2,
+    PLAN_MIXED = 3,
+    PLAN_PIPE = 4,
+    PLAN_HOT = 5,
+    PLAN_QUEUE = 6,
+    PLAN_TEAM = 7
+};
 
 struct LaunchPlan {
     int kind;        // PLAN_*
@@ -72,6 +81,7 @@ struct LaunchPlan {
     int chunk;          // PLAN_QUEUE: consecutive permutation positions per claim
     int wide;           // shared vector stored as double
     int unbound;        // PLAN_PIPE: the window does not bind (every coordinate may be in flight)
+    int team;           // PLAN_TEAM: workgroups per in-flight coordinate (K)
     size_t lds_bytes;
 };
 
@@ -131,6 +141,31 @@ hipError_t launch_hot_block_count(const unsigned* hits, int64_t L, unsigned T, u
 hipError_t launch_hot_assign(const unsigned* hits, int64_t L, unsigned T, const unsigned* block_base, uint16_t* slot_of,
                              int32_t* hot_ids, hipStream_t s);
 constexpr int kHotAssignBlock = 1024;  // shared-vector indices per workgroup in the slot assignment
+
+// Team epoch: each of the n_groups in-flight coordinates is processed by a team of K workgroups
+// (K <= kTeamMax), member k on the entries of the coordinate's segment whose shared-vector index
+// lies in the k-th of K index ranges.  `e.idx`/`e.val` are the segment entries grouped by range
+// (k_team_partition); member k's part of coordinate m is [ptr[m] + off[m(K+1)+k],
+// ptr[m] + off[m(K+1)+k+1]).  The members exchange their partial dot products through 64-bit slots
+// (fp32 bits, 32-bit step tag): slots[(team * 2 + tag % 2) * kTeamMax + k].
+constexpr int kTeamMax = 16;
+constexpr int kTeamSlices = 4;  // register slices per lane (256 x 4 entries of a member's part held)
+
+struct TeamArgs {
+    EpochArgs e;
+    const uint32_t* off;   // [C * (K + 1)]
+    uint64_t* slots;       // [n_groups * 2 * kTeamMax]
+    uint32_t K;
+    uint32_t tag0;         // tag of the first step of this launch (tags grow by one per step)
+    uint32_t spin_limit;   // bounded waits: after this many sleeps a member gives up and sets *err
+    int* err;
+};
+
+hipError_t launch_epoch_team(int form, bool wide, bool fresh, const TeamArgs& t, int blocks, hipStream_t s);
+// Groups each segment's entries by index range: bound[0] = 0 < bound[1] <= ... <= bound[K] = L.
+hipError_t launch_team_partition(const int64_t* ptr, const int32_t* idx, const float* val, uint32_t C,
+                                 const uint32_t* bound, int K, int32_t* out_idx, float* out_val, uint32_t* off,
+                                 hipStream_t s);
 
 hipError_t launch_epoch(int form, const EpochArgs& a, const LaunchPlan& lp, hipStream_t s);
 hipError_t ordered_lds_prepare(int form, bool wide, size_t lds_bytes);

@@ -525,6 +525,170 @@ def test_hot_set_kernel_parity(case):
     s.close()
 
 
+# ---------------------------------------------------------------------------------- team kernel
+
+def _blank_rows(p, every):
+    # the same CSR matrix with every `every`-th row emptied (empty coordinates in the team kernel)
+    lens = np.diff(p.ptr)
+    keep = np.ones(p.n_rows, dtype=bool)
+    keep[::every] = False
+    mask = np.repeat(keep, lens)
+    ptr = np.zeros(p.n_rows + 1, dtype=np.int64)
+    ptr[1:] = np.cumsum(np.where(keep, lens, 0))
+    return dataclasses.replace(p, ptr=ptr, idx=p.idx[mask].copy(), val=p.val[mask].copy())
+
+
+TEAM_CASES = {
+    # (problem, members K, window, shared_fp64).  The text twin's coupling window is 9; a team's
+    # coordinate is in flight for a larger part of each step than a pipelined group's, so the twin
+    # cases stay at 5.
+    "svm_k2": ("text_svm_twin", 2, 5, 0),
+    "svm_k3_fp64": ("text_svm_twin", 3, 5, 1),
+    "svm_k8": ("text_svm_twin", 8, 5, 0),
+    "svm_k16_fp64": ("text_svm_twin", 16, 4, 1),
+    "ridge_dual_k4": ("ridge_dual_text", 4, 5, 0),
+    # CSC columns of skewed lengths (ridge primal)
+    "ridge_primal_k4": ("text_ridge_twin", 4, 16, 0),
+    # parts longer than the register slices (256 x 4 entries): rows of 3,000 entries over 2 members
+    "svm_long_parts": ("svm_long", 2, 5, 0),
+    # empty rows
+    "svm_empty_rows": ("svm_blank", 4, 5, 0),
+    # a shared vector shorter than the team: most index ranges empty
+    "ridge_dual_tiny_L": ("ridge_dual_tiny", 16, 4, 0),
+    "dense_ridge_k5": ("dense_ridge", 5, 8, 1),
+}
+
+
+def _team_problem(key):
+    if key == "ridge_dual_text":
+        return synth.as_ridge_dual(problem("text_svm_twin"))
+    if key == "svm_long":
+        return synth.make("text_svm", n_rows=1_500, n_cols=166_000, row_nnz=3_000)
+    if key == "svm_blank":
+        return _blank_rows(problem("text_svm_twin"), 5)
+    if key == "ridge_dual_tiny":
+        return synth.as_ridge_dual(synth.make("dense_ridge", n_rows=600, n_cols=10))
+    return problem(key)
+
+
+@pytest.mark.parametrize("case", sorted(TEAM_CASES))
+def test_team_kernel_parity(case):
+    key, K, window, wide = TEAM_CASES[case]
+    p = _team_problem(key)
+    E = 6
+    _, _, curve = _oracle_curve(p, 0, E)
+    s = scd.solver_for(p)
+    s.set_option("shared_fp64", wide)
+    s.set_option("window", window)
+    s.set_option("team", K)
+    info = s.info()
+    print(f"team {case}: kernel {info['kernel']} lanes {info['group_lanes']} window {info['window']} "
+          f"max segment {info['max_segment']}", flush=True)
+    assert info["kernel"] == "team" and info["group_lanes"] == 256 * K and info["window"] == window
+    P0, _ = s.objective()
+    nonempty = np.diff(p.ptr) > 0
+    prev = np.zeros(p.C)
+    for e in range(E):
+        s.epochs(0, 1)
+        gm, gs, ep = s.get_state()
+        assert ep == e + 1
+        model = f64(gm)
+        assert rel_inf(f64(gs), fresh(p, model)) <= 1e-4, e
+        if p.form == "svm_dual":
+            assert model.min() >= 0.0 and model.max() <= 1.0
+        if p.form == "svm_dual" and e == 0:
+            assert np.all(model[~nonempty] == 1.0)  # an empty row's step sets alpha to 1
+        if e == 0 and p.form != "svm_dual":
+            assert np.mean(model[nonempty] != prev[nonempty]) > 0.99  # every coordinate visited
+        prev = model
+        G, Gr = s.duality_gap(), curve[e][2]
+        if Gr > 1e-6 * abs(P0):
+            assert G <= 2.0 * Gr, (e, G, Gr)
+    s.close()
+
+
+@pytest.mark.parametrize("key,E", [("dense_ridge", 60), ("text_svm_twin", 60)])
+def test_team_converged_objective(key, E):
+    # converged primal objective within 1e-5 of the oracle's after the same number of epochs
+    p = problem(key)
+    model = np.zeros(p.C)
+    shared = np.zeros(p.L)
+    orc.epochs(p.form, p.n_rows, p.n_cols, p.ptr, p.idx, p.val, p.y, p.lam, 0, 0, E, model, shared)
+    Pr = orc.objectives(p.form, p.n_rows, p.n_cols, p.ptr, p.idx, p.val, p.y, p.lam, model)[0]
+    s = scd.solver_for(p)
+    s.set_option("window", 8)
+    s.set_option("team", 4)
+    assert s.info()["kernel"] == "team"
+    s.epochs(0, E)
+    P, _ = s.objective()
+    Pf = orc.objectives(p.form, p.n_rows, p.n_cols, p.ptr, p.idx, p.val, p.y, p.lam, f64(s.get_state()[0]))[0]
+    assert abs(P - Pr) <= 1e-5 * abs(Pr), (P, Pr)
+    assert abs(Pf - Pr) <= 1e-5 * abs(Pr), (Pf, Pr)
+    s.close()
+
+
+def test_team_selection_rules():
+    # automatic: long segments (mean >= 1,024) on a shared vector of at least 16 MB, a binding window
+    # and at least two members per team within the CUs; option team = 0 turns it off
+    p = synth.make("text_svm", n_rows=2_000, n_cols=8_000_000, row_nnz=1_200)
+    s = scd.solver_for(p)
+    s.set_option("window", 16)
+    info = s.info()
+    assert info["kernel"] == "team" and info["window"] == 16, info
+    assert info["group_lanes"] % 256 == 0 and 2 <= info["group_lanes"] // 256 <= 16
+    s.set_option("team", 0)
+    assert s.info()["kernel"] == "pipelined"
+    s.set_option("team", 1)
+    s.set_option("window", p.C)  # a window that does not bind: no team
+    assert s.info()["kernel"] != "team"
+    s.set_option("window", 16)
+    s.set_option("pipeline", 0)
+    assert s.info()["kernel"] != "team"
+    s.set_option("pipeline", 1)
+    assert s.info()["kernel"] == "team"
+    for bad in (-1, 17):
+        with pytest.raises(scd.ScdError):
+            s.set_option("team", bad)
+    s.epochs(0, 2)
+    gm, gs, _ = s.get_state()
+    assert rel_inf(f64(gs), fresh(p, f64(gm))) <= 1e-4
+    s.close()
+    t = scd.solver_for(problem("text_svm_twin"))  # short rows (370): the pipelined kernel
+    t.set_option("window", 16)
+    assert t.info()["kernel"] != "team"
+    t.close()
+
+
+def test_team_wait_limit():
+    # the members' bounded waits with a limit of one sleep: either every exchange completes in time
+    # (valid state) or the timeout is reported at the next synchronising call and a written state
+    # replaces the invalid one
+    p = problem("text_svm_twin")
+    s = scd.solver_for(p)
+    s.set_option("window", 8)
+    s.set_option("team", 8)
+    assert s.info()["kernel"] == "team"
+    s.set_option("hot_wait_limit", 1)
+    s.epochs(0, 3)
+    try:
+        s.duality_gap()
+        timed_out = False
+    except scd.ScdError as e:
+        assert "timed out" in str(e)
+        timed_out = True
+    print(f"team wait limit 1: timed out {timed_out}", flush=True)
+    if not timed_out:
+        gm, gs, _ = s.get_state()
+        assert rel_inf(f64(gs), fresh(p, f64(gm))) <= 1e-4
+    s.set_option("hot_wait_limit", 0)
+    s.set_state(torch.zeros(p.C, device=DEV), torch.zeros(p.L, device=DEV), 0)
+    s.epochs(0, 2)
+    gm, gs, _ = s.get_state()
+    assert rel_inf(f64(gs), fresh(p, f64(gm))) <= 1e-4
+    assert s.duality_gap() > 0.0
+    s.close()
+
+
 @pytest.mark.parametrize("wide", [0, 1])
 @pytest.mark.parametrize("spread", [0, 1])
 def test_spread_copy_parity(spread, wide):
