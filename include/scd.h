@@ -92,7 +92,8 @@ typedef struct {
 /* Read-only facts about a handle. */
 typedef struct {
     int32_t formulation;  /* scd_formulation_t                                        */
-    int32_t group_lanes;  /* lanes per coordinate of the epoch kernel (1024 = ordered) */
+    int32_t group_lanes;  /* lanes per coordinate of the epoch kernel (1024 = ordered; the team
+                             kernel: 256 x its members)                                */
     int64_t n_coords;     /* C: M for SCD_RIDGE_PRIMAL, N for the duals                */
     int64_t shared_len;   /* length of the shared vector: N (ridge primal) or M         */
     int64_t nnz;
@@ -117,7 +118,9 @@ typedef struct {
                              workgroup, 4 software-pipelined, 5 hot set in LDS (one
                              workgroup, at most 8 coordinates in flight), 6 one workgroup
                              per coordinate taking positions from a queue (skewed
-                             segment lengths)                                           */
+                             segment lengths), 7 a team of workgroups per coordinate,
+                             each on its own range of shared-vector indices (long
+                             segments, few coordinates in flight)                      */
     int32_t hot_entries;  /* shared-vector entries the hot-set kernel keeps in LDS
                              (0 until it is first needed)                               */
 } scd_info_t;
@@ -171,7 +174,7 @@ int scd_duality_gap_wait(scd_handle_t h, int32_t slot, double *gap, double *prim
  *   model_dev:  float32[n_coords]   (beta, or alpha)
  *   shared_dev: float32[shared_len] (w = A beta, or w(alpha), or wbar = A^T alpha)
  *   epoch:      host int64 (may be NULL).  Enqueues only, so it reports no error of the
- *   epochs before it: a hot-set epoch whose waits timed out (see "hot_wait_limit") leaves a
+ *   epochs before it: a hot-set or team epoch whose waits timed out (see "hot_wait_limit") leaves a
  *   partial state that this call copies as is; the next synchronising call returns the error.
  *   A state copied out and written back with scd_set_state resumes bit-exactly when the shared
  *   vector is stored in fp32 (option "shared_fp64" = 0); an fp64 shared vector is exchanged
@@ -216,10 +219,22 @@ int scd_set_state(scd_handle_t h, const float *model_dev, const float *shared_de
  *                 reads the others ahead of their coordinates; 0 = never.  The hot set is chosen
  *                 (a pass over the matrix, synchronising) when this first applies: at create, or
  *                 when "window" or "hot" is set.
+ *   "team"        1 (default) = with a binding window, segments of at least 1,024 entries on
+ *                 average, a shared vector of at least 16 MB and "group" 0, process each in-flight
+ *                 coordinate with a team of K workgroups (K = CUs / coordinates in flight, at
+ *                 most 16), member k on the entries whose shared-vector index lies in the k-th of
+ *                 K ranges of about equal entry count; the members exchange their partial inner
+ *                 products through device memory.  It needs a copy of A with each segment's
+ *                 entries grouped by range (8 bytes per stored entry, made when this first
+ *                 applies: at create, or when "window", "team", "group", "pipeline" or
+ *                 "shared_fp64" is set; synchronising; skipped when device memory is short).
+ *                 0 = never; 2..16 = K members whenever the window binds and (coordinates in
+ *                 flight) x K is at most the number of CUs.  With the automatic window, teams take
+ *                 3/4 of the window's share that the other draining kernels take.
  *   "hot_wait_limit"  test hook: sleeps (about 64 cycles each) one wait between the waves of the
- *                 hot-set kernel may take before the waves give up; the next synchronising call
- *                 then returns SCD_ERR_HIP and the state stays invalid until scd_set_state.
- *                 0 (default) = 2^24.
+ *                 hot-set kernel, or between the members of a team, may take before giving up;
+ *                 the next synchronising call then returns SCD_ERR_HIP and the state stays invalid
+ *                 until scd_set_state.  0 (default) = 2^24.
  *   "shared_fp64" 1 = store the shared vector in fp64 (fp64 atomic adds), 0 = fp32.  Chosen at
  *                 create: fp64 when some entry receives more than 28,000 atomic adds per epoch,
  *                 where fp32 accumulation would drift by more than about 1e-5 of its magnitude.
