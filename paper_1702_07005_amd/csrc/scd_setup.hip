@@ -119,6 +119,8 @@ __device__ __forceinline__ void block_reduce_store(double (&v)[NS], double* out)
     }
 }
 
+constexpr int kObjSlices = 8;  // entries per lane per block of the objective's gather-dot
+
 template <int FORM, int G, typename U>
 __global__ __launch_bounds__(256) void k_objective(ObjArgs o, double* __restrict__ partials) {
     constexpr int NS = 5;
@@ -127,8 +129,29 @@ __global__ __launch_bounds__(256) void k_objective(ObjArgs o, double* __restrict
     const uint32_t ngroups = gridDim.x * (256u / G);
     double t[NS] = {0.0, 0.0, 0.0, 0.0, 0.0};
     for (uint32_t c = (blockIdx.x * 256u + threadIdx.x) / G; c < o.C; c += ngroups) {
+        // Blocks of G * kObjSlices entries: all index and value loads of a block, then all its
+        // gathers, so that a block costs two memory round trips instead of two per entry.  Lanes
+        // past the end re-read entry s0 with weight 0.
+        const int64_t s0 = o.ptr[c], s1 = o.ptr[c + 1];
         double d = 0.0;
-        for (int64_t k = o.ptr[c] + lane; k < o.ptr[c + 1]; k += G) d += (double)o.val[k] * (double)u[o.idx[k]];
+        for (int64_t b = s0; b < s1; b += (int64_t)G * kObjSlices) {
+            int ix[kObjSlices];
+            float vx[kObjSlices];
+#pragma unroll
+            for (int r = 0; r < kObjSlices; ++r) {
+                const int64_t k = b + lane + (int64_t)r * G;
+                const bool in = k < s1;
+                const int64_t kk = in ? k : s0;
+                ix[r] = o.idx[kk];
+                const float v = o.val[kk];
+                vx[r] = in ? v : 0.0f;
+            }
+            U g[kObjSlices];
+#pragma unroll
+            for (int r = 0; r < kObjSlices; ++r) g[r] = u[ix[r]];
+#pragma unroll
+            for (int r = 0; r < kObjSlices; ++r) d += (double)vx[r] * (double)g[r];
+        }
         d = group_sum_f64<G>(d);
         if (lane == 0) {
             const double mo = o.model[c];
