@@ -198,6 +198,10 @@ def main():
     stream = torch.cuda.current_stream()
     solver = scd.solver_for(prob, device=dev)
     info = solver.info()
+    # The library runs an unbound pipelined plan on its spread copy of a shared vector of at most
+    # 4 M entries, copied out and back inside each scd_epochs call.
+    spread = (info["kernel"] == "pipelined" and info["window"] >= prob.C and prob.L <= (1 << 22)
+              and solver.get_option("spread") == 1)
     zeros_m = torch.zeros(prob.C, dtype=torch.float32, device=dev)
     zeros_s = torch.zeros(prob.L, dtype=torch.float32, device=dev)
 
@@ -294,7 +298,9 @@ def main():
         "gap_epochs_run": len(curve),
         "roofline": {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
                      "frac": achieved / HBM_PEAK_GBS, "traffic": traffic,
-                     "algorithmic_bytes_per_launch": alg, "kernel": "scd::k_epoch_*"},
+                     "algorithmic_bytes_per_launch": alg,
+                     "kernel": f"scd::k_epoch_* ({info['kernel']}); timed: one scd_epochs call of one epoch"
+                               + (", with its two k_spread copies" if spread else "")},
     }
     solver.close()
     ceil = device_ceilings(prob.L)
