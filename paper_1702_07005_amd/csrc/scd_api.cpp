@@ -244,6 +244,14 @@ int team_members(const scd_solver* h, int64_t* teams) {
         if (mean < kTeamMinMean || shared_bytes(h) < kTeamMinSharedBytes) return 0;
         K = std::min<int64_t>(kTeamMax, h->cus / groups);
     }
+    // A member's part beyond the register slices is streamed twice and stays between gather and
+    // scatter for several block round trips: as in the queued kernel, the automatic window is
+    // then halved (a 1,500 x 166,000 case with 1,500-entry parts reached 2.07x the sequential
+    // gap at the undivided share).
+    if (h->window == 0 && K >= 2 && (h->max_seg + K - 1) / K > (int64_t)kBlockThreads * kTeamSlices) {
+        groups = std::max<int64_t>(1, groups / 2);
+        if (h->team < 2) K = std::min<int64_t>(kTeamMax, h->cus / groups);
+    }
     if (K < 2 || groups * K > h->cus) return 0;
     *teams = groups;
     return (int)K;

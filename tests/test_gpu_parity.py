@@ -539,9 +539,8 @@ def _blank_rows(p, every):
 
 
 TEAM_CASES = {
-    # (problem, members K, window, shared_fp64).  The text twin's coupling window is 9; a team's
-    # coordinate is in flight for a larger part of each step than a pipelined group's, so the twin
-    # cases stay at 5.
+    # (problem, members K, largest window, shared_fp64); each case runs at most the teams' share of
+    # its coupling window (text twin: 9 -> 5), halved when parts exceed the register slices.
     "svm_k2": ("text_svm_twin", 2, 5, 0),
     "svm_k3_fp64": ("text_svm_twin", 3, 5, 1),
     "svm_k8": ("text_svm_twin", 8, 5, 0),
@@ -550,7 +549,7 @@ TEAM_CASES = {
     # CSC columns of skewed lengths (ridge primal)
     "ridge_primal_k4": ("text_ridge_twin", 4, 16, 0),
     # parts longer than the register slices (256 x 4 entries): rows of 3,000 entries over 2 members
-    "svm_long_parts": ("svm_long", 2, 5, 0),
+    "svm_long_parts": ("svm_long", 2, 2, 0),
     # empty rows
     "svm_empty_rows": ("svm_blank", 4, 5, 0),
     # a shared vector shorter than the team: most index ranges empty
@@ -579,11 +578,20 @@ def test_team_kernel_parity(case):
     _, _, curve = _oracle_curve(p, 0, E)
     s = scd.solver_for(p)
     s.set_option("shared_fp64", wide)
+    # Within the teams' share of the coupling rule's window (4/5 x 3/4 of it, as the automatic plan
+    # takes), where the gap curve is expected within 2x; below 2 the case runs 2 teams and checks
+    # the invariant, the box and the visiting only.
+    share = s.info()["auto_window"] * 3 // 5
+    if -(-s.info()["max_segment"] // K) > 256 * 4:  # parts beyond the register slices: half of it
+        share //= 2
+    window = min(window, share)
+    gate = window >= 2
+    window = max(window, 2)
     s.set_option("window", window)
     s.set_option("team", K)
     info = s.info()
     print(f"team {case}: kernel {info['kernel']} lanes {info['group_lanes']} window {info['window']} "
-          f"max segment {info['max_segment']}", flush=True)
+          f"(automatic {info['auto_window']}) max segment {info['max_segment']}", flush=True)
     assert info["kernel"] == "team" and info["group_lanes"] == 256 * K and info["window"] == window
     P0, _ = s.objective()
     nonempty = np.diff(p.ptr) > 0
@@ -602,7 +610,7 @@ def test_team_kernel_parity(case):
             assert np.mean(model[nonempty] != prev[nonempty]) > 0.99  # every coordinate visited
         prev = model
         G, Gr = s.duality_gap(), curve[e][2]
-        if Gr > 1e-6 * abs(P0):
+        if gate and Gr > 1e-6 * abs(P0):
             assert G <= 2.0 * Gr, (e, G, Gr)
     s.close()
 
