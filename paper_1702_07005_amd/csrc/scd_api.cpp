@@ -511,15 +511,23 @@ int build_team_tables(scd_solver* h, int K, hipStream_t s) {
         HIP_TRY(hipMemsetAsync(h->team_slots, 0, sb, s));
     }
     unsigned* hits = nullptr;
+    // Without memory for the tables the other kernels run instead: an allocation that fails here
+    // (after the check above, e.g. by fragmentation) is not an error of the calling function.
+    const bool got = hipMalloc(&hits, sizeof(unsigned) * (size_t)h->L) == hipSuccess &&
+                     hipMalloc(&h->team_idx, sizeof(int32_t) * nnz1) == hipSuccess &&
+                     hipMalloc(&h->team_val, sizeof(float) * nnz1) == hipSuccess &&
+                     hipMalloc(&h->team_off, sizeof(uint32_t) * (size_t)h->C * (K + 1)) == hipSuccess &&
+                     hipMalloc(&h->team_bound, sizeof(uint32_t) * (K + 1)) == hipSuccess;
+    if (!got) {
+        (void)hipGetLastError();  // clear the allocation failure
+        (void)hipFree(hits);
+        free_team_tables(h);
+        return SCD_OK;
+    }
     int rc = SCD_OK;
     auto hip = [&](hipError_t e, const char* what) {
         if (rc == SCD_OK && e != hipSuccess) rc = fail(SCD_ERR_HIP, "%s: %s", what, hipGetErrorString(e));
     };
-    hip(hipMalloc(&hits, sizeof(unsigned) * (size_t)h->L), "hipMalloc(team hits)");
-    hip(hipMalloc(&h->team_idx, sizeof(int32_t) * nnz1), "hipMalloc(team_idx)");
-    hip(hipMalloc(&h->team_val, sizeof(float) * nnz1), "hipMalloc(team_val)");
-    hip(hipMalloc(&h->team_off, sizeof(uint32_t) * (size_t)h->C * (K + 1)), "hipMalloc(team_off)");
-    hip(hipMalloc(&h->team_bound, sizeof(uint32_t) * (K + 1)), "hipMalloc(team_bound)");
     std::vector<unsigned> hh;
     if (rc == SCD_OK) {
         hip(hipMemsetAsync(hits, 0, sizeof(unsigned) * (size_t)h->L, s), "zero team hits");
