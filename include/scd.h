@@ -230,7 +230,7 @@ int scd_set_state(scd_handle_t h, const float *model_dev, const float *shared_de
  *                 "shared_fp64" is set; synchronising; skipped when device memory is short).
  *                 0 = never; 2..16 = K members whenever the window binds and (coordinates in
  *                 flight) x K is at most the number of CUs.  With the automatic window, teams take
- *                 3/4 of the window's share that the other draining kernels take.
+ *                 7/8 of the window's share that the other draining kernels take.
  *   "hot_wait_limit"  test hook: sleeps (about 64 cycles each) one wait between the waves of the
  *                 hot-set kernel, or between the members of a team, may take before giving up;
  *                 the next synchronising call then returns SCD_ERR_HIP and the state stays invalid

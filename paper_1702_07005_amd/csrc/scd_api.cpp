@@ -234,8 +234,9 @@ int team_members(const scd_solver* h, int64_t* teams) {
     // than a pipelined group's (the exchange of partial sums sits in that interval): on the
     // text-SVM twin (3,500 x 166,000) the worst per-epoch gap ratio to the sequential algorithm
     // at a team window of 6 matched the pipelined kernel's at about 8.  With the automatic window
-    // teams therefore take 3/4 of the pipelined share.
-    if (h->window == 0) groups = std::max<int64_t>(1, groups * 3 / 4);
+    // teams therefore take 7/8 of the pipelined share (full-size text SVM: 32 -> 28 rows in
+    // flight; worst ratio 1.49 over 24 runs of 8 epochs, against 1.80 at 32).
+    if (h->window == 0) groups = std::max<int64_t>(1, groups * 7 / 8);
     int64_t K;
     if (h->team >= 2) {
         K = h->team;

@@ -578,9 +578,9 @@ def test_team_kernel_parity(case):
     _, _, curve = _oracle_curve(p, 0, E)
     s = scd.solver_for(p)
     s.set_option("shared_fp64", wide)
-    # Within the teams' share of the coupling rule's window (4/5 x 3/4 of it, as the automatic plan
-    # takes), where the gap curve is expected within 2x; below 2 the case runs 2 teams and checks
-    # the invariant, the box and the visiting only.
+    # Within the teams' share of the coupling rule's window (4/5 x 3/4 of it, a little below the
+    # automatic plan's 4/5 x 7/8), where the gap curve is expected within 2x; below 2 the case runs
+    # 2 teams and checks the invariant, the box and the visiting only.
     share = s.info()["auto_window"] * 3 // 5
     if -(-s.info()["max_segment"] // K) > 256 * 4:  # parts beyond the register slices: half of it
         share //= 2
