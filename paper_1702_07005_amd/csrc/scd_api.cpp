@@ -253,10 +253,6 @@ int team_members(const scd_solver* h, int64_t* teams) {
         groups = std::max<int64_t>(1, groups / 2);
         if (h->team < 2) K = std::min<int64_t>(kTeamMax, h->cus / groups);
     }
-    // Teams of a multiple of 4 members ran slower than teams of one member fewer, on every text-like
-    // problem measured (16 teams: 16 members 81.8 ms per epoch against 73.2 with 15, 8 members 91.4
-    // against 80.9 with 7; 32 teams: 8 members 72.7 ms against 50.3 with 7); the cause is not known.
-    if (h->team < 2 && K >= 4 && K % 4 == 0) K -= 1;
     if (K < 2 || groups * K > h->cus) return 0;
     *teams = groups;
     return (int)K;
@@ -295,7 +291,7 @@ int plan_epoch(const scd_solver* h, LaunchPlan* lp, uint32_t* n_groups) {
         lp->team = K;
         lp->group = kBlockThreads;
         lp->drain = 1;
-        lp->blocks = (int)(teams * K);
+        lp->blocks = team_grid(teams, K);
         *n_groups = (uint32_t)teams;
         return SCD_OK;
     }

@@ -149,6 +149,17 @@ constexpr int kHotAssignBlock = 1024;  // shared-vector indices per workgroup in
 // ptr[m] + off[m(K+1)+k+1]).  The members exchange their partial dot products through 64-bit slots
 // (fp32 bits, 32-bit step tag): slots[(team * 2 + tag % 2) * kTeamMax + k].
 constexpr int kTeamMax = 16;
+constexpr uint32_t kTeamXcds = 8;  // XCDs of the MI355X, to which workgroups are dispatched in turn
+// Workgroups of a team launch: kTeamXcds times the most (team, member) pairs placed on one XCD, with
+// member k of team t on XCD (t + k) mod kTeamXcds.
+inline int team_grid(int64_t teams, int64_t K) {
+    int64_t cnt[kTeamXcds] = {0};
+    for (int64_t t = 0; t < teams; ++t)
+        for (int64_t k = 0; k < K; ++k) ++cnt[(t + k) % kTeamXcds];
+    int64_t mx = 0;
+    for (uint32_t x = 0; x < kTeamXcds; ++x) mx = cnt[x] > mx ? cnt[x] : mx;
+    return (int)(mx * kTeamXcds);
+}
 constexpr int kTeamSlices = 4;  // register slices per lane (256 x 4 entries of a member's part held)
 
 struct TeamArgs {

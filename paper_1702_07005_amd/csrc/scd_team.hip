@@ -182,8 +182,29 @@ __global__ __launch_bounds__(256) void k_epoch_team(TeamArgs t) {
     __shared__ float gsum[2];
     __shared__ int gok[2];
     const EpochArgs& a = t.e;
-    const uint32_t team = blockIdx.x / t.K, k = blockIdx.x % t.K;
-    if (team >= a.n_groups || team >= a.perm.n) return;  // the whole workgroup leaves
+    // XCD-aware placement.  Workgroups are dispatched to the kTeamXcds XCDs in turn (workgroup b to XCD
+    // b mod kTeamXcds).  Member k of team t is placed on XCD (t + k) mod kTeamXcds, so the owners of
+    // each index range (member k of every team) are spread over all XCDs whatever K is.  In the plain
+    // order (workgroup t K + k), K = 8 put every owner of range k on XCD k; the scatter into each
+    // range then went through one XCD, and an epoch took 40% longer than at K = 7 or 9.  Workgroup b
+    // takes the (b / kTeamXcds)-th pair, in team-major order, among the pairs placed on its XCD;
+    // workgroups beyond them leave.
+    uint32_t team = 0xFFFFFFFFu, k = 0;
+    {
+        const uint32_t x = blockIdx.x % kTeamXcds, want = blockIdx.x / kTeamXcds;
+        uint32_t seen = 0;
+        for (uint32_t tt = 0; tt < a.n_groups && team == 0xFFFFFFFFu; ++tt)
+            for (uint32_t kk = 0; kk < t.K; ++kk)
+                if ((tt + kk) % kTeamXcds == x) {
+                    if (seen == want) {
+                        team = tt;
+                        k = kk;
+                        break;
+                    }
+                    ++seen;
+                }
+    }
+    if (team == 0xFFFFFFFFu || team >= a.perm.n) return;  // the whole workgroup leaves
     const int lane = threadIdx.x;
     const SharedBuf<U> ub =
         shared_buf<U>(a.u, a.u_bytes, reinterpret_cast<U*>(a.sink) + (size_t)blockIdx.x * 256 + threadIdx.x, a.u_shift);
