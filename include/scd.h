@@ -220,7 +220,8 @@ int scd_set_state(scd_handle_t h, const float *model_dev, const float *shared_de
  *                 (a pass over the matrix, synchronising) when this first applies: at create, or
  *                 when "window" or "hot" is set.
  *   "team"        1 (default) = with a binding window, segments of at least 1,024 entries on
- *                 average, a shared vector of at least 4 MB and "group" 0, process each in-flight
+ *                 average and none longer than 4 times that, a shared vector of at least 4 MB and
+ *                 "group" 0, process each in-flight
  *                 coordinate with a team of K workgroups (K = CUs / coordinates in flight, at
  *                 most 16), member k on the entries whose shared-vector index lies in the k-th of
  *                 K ranges of about equal entry count; the members exchange their partial inner

@@ -89,6 +89,10 @@ constexpr uint32_t kHotSpinLimit = 1u << 24;
 // the 2,000 x 200 dense ridge (8 KB), 47 us against 82 us; rows of 370 entries, 1.02 ms against
 // 1.16 ms.
 constexpr double kTeamMinMean = 1024.0;
+// ... and segments of about equal length: teams walk positions at a fixed stride, so on skewed
+// lengths those that draw long segments fall behind and the processing order drifts from the
+// permutation (the queued kernel's case).
+constexpr double kTeamMaxSkew = 4.0;  // longest segment at most this many times the mean
 constexpr int64_t kTeamMinSharedBytes = int64_t(4) << 20;
 
 }  // namespace
@@ -242,7 +246,8 @@ int team_members(const scd_solver* h, int64_t* teams) {
         K = h->team;
     } else {
         const double mean = (double)h->nnz / (double)h->C;
-        if (mean < kTeamMinMean || shared_bytes(h) < kTeamMinSharedBytes) return 0;
+        if (mean < kTeamMinMean || shared_bytes(h) < kTeamMinSharedBytes || (double)h->max_seg > kTeamMaxSkew * mean)
+            return 0;
         K = std::min<int64_t>(kTeamMax, h->cus / groups);
     }
     // A member's part beyond the register slices is streamed twice and stays between gather and
