@@ -9,7 +9,8 @@ import pytest
 
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 SRC = os.path.join(ROOT, "oracle", "scd_oracle.c")
-PINS = ["tests/test_oracle_perm.py", "tests/test_oracle_ridge.py", "tests/test_oracle_svm.py", "tests/test_oracle_f32.py"]
+PINS = ["tests/test_oracle_perm.py", "tests/test_oracle_ridge.py", "tests/test_oracle_svm.py", "tests/test_oracle_f32.py",
+        "tests/test_oracle_shared_objectives.py"]
 
 MUTANTS = {
     "primal_drops_regulariser": ("double d = (g - lN * beta[m]) / (norms[m] + lN);",
@@ -38,6 +39,10 @@ MUTANTS = {
     "f32_dual_drops_lambda_y": ("float d = (lam * y[m] - g - lN * model[m]) / (lN + norms[m]);",
                                 "float d = (y[m] - g - lN * model[m]) / (lN + norms[m]);"),
     "f32_svm_scatter_drops_label": ("coef = (a - model[m]) * y[m] / lN;", "coef = (a - model[m]) / lN;"),
+    # objectives from a maintained shared vector: the given vector is dropped (left at zero)
+    "ridge_primal_obj_ignores_shared": ("memcpy(w, w_in, sizeof(double) * (size_t)N);", "(void)w_in;"),
+    "ridge_dual_obj_ignores_shared": ("memcpy(wbar, wbar_in, sizeof(double) * (size_t)M);", "(void)wbar_in;"),
+    "svm_obj_ignores_shared": ("memcpy(w, w_in, sizeof(double) * (size_t)M);", "(void)w_in;"),
 }
 
 
