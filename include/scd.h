@@ -100,7 +100,8 @@ typedef struct {
     int64_t epoch;        /* global epoch counter (epochs run so far)                  */
     int64_t max_segment;  /* longest coordinate segment                                */
     int64_t window;       /* coordinates in flight at most (whose updates other
-                             coordinates may not see yet)                               */
+                             coordinates may not see yet); with an adaptive window (see
+                             adaptive_window) the most the epoch kernel can hold          */
     double lambda;
     double coupling;      /* largest over coordinates c of sum_{j != c} G_cj^2 / (C - 1), G the
                              step-normalised Gram matrix of the coordinates (estimated at
@@ -116,13 +117,17 @@ typedef struct {
                              1 one workgroup per coordinate, 2 ordered with the shared
                              vector in LDS, 3 lane groups with long segments handed to the
                              workgroup, 4 software-pipelined, 5 hot set in LDS (one
-                             workgroup, at most 8 coordinates in flight), 6 one workgroup
+                             workgroup, at most 16 coordinates in flight), 6 one workgroup
                              per coordinate taking positions from a queue (skewed
                              segment lengths), 7 a team of workgroups per coordinate,
                              each on its own range of shared-vector indices (long
                              segments, few coordinates in flight)                      */
     int32_t hot_entries;  /* shared-vector entries the hot-set kernel keeps in LDS
                              (0 until it is first needed)                               */
+    int32_t adaptive_window; /* 1 if the epoch kernel sets each epoch's window from the
+                             coordinates that moved in the previous one (option "adapt"):
+                             the first epoch runs at auto_window                        */
+    int32_t reserved;
 } scd_info_t;
 
 /* Create a solver for min P / max D of the chosen formulation (Sec. II; Sec. III-C).
@@ -213,7 +218,7 @@ int scd_set_state(scd_handle_t h, const float *model_dev, const float *shared_de
  *                 at a time: 0 (default) = 1 per 64 coordinates in flight (at least 1), else
  *                 1..64.  Larger chunks lower the claim rate on the queue's counter and let
  *                 coordinates start further from their permutation positions.
- *   "hot"         1 (default) = with at most 8 coordinates in flight, segments of at most 64
+ *   "hot"         1 (default) = with at most 16 coordinates in flight, segments of at most 64
  *                 entries and "group" 0, run the epoch in one workgroup that keeps the most-updated
  *                 shared-vector entries in LDS (their gathers and adds never leave the CU) and
  *                 reads the others ahead of their coordinates; 0 = never.  The hot set is chosen
@@ -232,6 +237,14 @@ int scd_set_state(scd_handle_t h, const float *model_dev, const float *shared_de
  *                 0 = never; 2..16 = K members whenever the window binds and (coordinates in
  *                 flight) x K is at most the number of CUs.  With the automatic window, teams take
  *                 7/8 of the window's share that the other draining kernels take.
+ *   "adapt"       1 (default) = when the window is automatic and the hot-set kernel runs the epoch,
+ *                 each epoch's window follows the fraction f of coordinates whose step was nonzero
+ *                 in the previous epoch: W = 1 + (auto_window - 1) / f, at most 16.  A coordinate
+ *                 whose step is zero (in the hinge SVM dual, one whose alpha stays at a bound of
+ *                 the box) changes nothing that others read, so the coupling rule's budget holds
+ *                 for the coordinates in flight that move.  The window is kept in device memory,
+ *                 so it needs no synchronisation; the first epoch after scd_create, scd_set_state
+ *                 or scd_set_option runs at auto_window.  0 = auto_window in every epoch.
  *   "hot_wait_limit"  test hook: sleeps (about 64 cycles each) one wait between the waves of the
  *                 hot-set kernel, or between the members of a team, may take before giving up;
  *                 the next synchronising call then returns SCD_ERR_HIP and the state stays invalid
@@ -242,6 +255,9 @@ int scd_set_state(scd_handle_t h, const float *model_dev, const float *shared_de
  *                 The state calls exchange fp32 copies either way.
  * Errors: SCD_ERR_UNSUPPORTED for an unknown key, SCD_ERR_INVALID for a bad value. */
 int scd_set_option(scd_handle_t h, const char *key, int64_t value);
+/* Reads an option's value, or the read-only key "next_window": the coordinates the next epoch will
+ * keep in flight at most (with an adaptive window, the value the last epoch left in device memory;
+ * this read synchronises the device). */
 int scd_get_option(scd_handle_t h, const char *key, int64_t *value);
 
 int scd_get_info(scd_handle_t h, scd_info_t *info);

@@ -63,7 +63,6 @@ PermKeys make_perm(uint64_t seed, uint64_t epoch, uint32_t n) {
 
 constexpr int kBlockThreads = 256;
 constexpr int kBlocksPerCU = 8;
-constexpr int kObjBlocksMax = 2048;
 constexpr int kGapSlots = 4;
 // Window rule: (window - 1) x (worst coordinate's mean squared coupling) <= budget.  The SVM's
 // box projection tolerates stale reads far better than the unconstrained ridge steps.
@@ -96,6 +95,8 @@ constexpr double kTeamMaxSkew = 4.0;  // longest segment at most this many times
 constexpr int64_t kTeamMinSharedBytes = int64_t(4) << 20;
 
 }  // namespace
+
+void scd::set_last_error(const char* msg) { g_err = msg; }
 
 struct scd_solver {
     int form = 0;
@@ -147,6 +148,9 @@ struct scd_solver {
     uint32_t n_hot = 0;
     double hot_cover = 0.0;       // fraction of stored entries that point at a hot entry
     int* hot_err = nullptr;       // device flag set by a timed-out wait in the hot-set kernel
+    int64_t adapt = 1;            // option: automatic window of the hot-set kernel follows the moving fraction
+    uint32_t* hot_adapt = nullptr;  // [2]: the hot-set kernel's window for the next epoch (device)
+    int adapt_fresh = 1;          // the next hot-set epoch starts from the rule's window (state or options changed)
     int64_t hot_wait_limit = 0;   // option (test hook): sleeps per wait before giving up, 0 = kHotSpinLimit
     int* err_host = nullptr;      // pinned copies of hot_err: one per gap slot + one for reduce_state
     // Team kernel (long segments, few coordinates in flight): tables built on first need for K.
@@ -172,22 +176,29 @@ int auto_group(const scd_solver* h) {
 
 int64_t shared_bytes(const scd_solver* h) { return h->L * (int64_t)(h->wide ? sizeof(double) : sizeof(float)); }
 
-// Batch geometry of the hot-set kernel for window W.
+// Batch geometry of the hot-set kernel for window W (the first epoch's when adaptive).
 struct HotGeom {
-    uint32_t W, B, Smax, hot_bytes;
+    uint32_t W, NC, cap, Smax, hot_bytes;
+    bool adaptive;
     size_t lds;
 };
+
+// The hot-set kernel's window adapts to the fraction of coordinates that move when the window is
+// automatic (the coupling rule assumes that every coordinate in flight moves).
+bool hot_adaptive(const scd_solver* h) { return h->window == 0 && h->adapt != 0; }
 
 bool hot_geometry(const scd_solver* h, int64_t W, HotGeom* g) {
     if (W < 2 || W > kHotMaxWindow || h->max_seg > kHotMaxSegment || h->C < 1) return false;
     g->W = (uint32_t)W;
+    g->adaptive = hot_adaptive(h);
+    // A second consumer wave when the window may exceed what one consumer holds.
+    g->NC = (g->adaptive || W > kHotMaxGroups) ? 2u : 1u;
     g->Smax = (uint32_t)std::max<int64_t>(8, (h->max_seg + 7) / 8 * 8);
-    const uint32_t cap = std::min<uint32_t>(64, 64u * kHotEntriesPerLane / g->Smax);
-    g->B = cap / g->W * g->W;
-    if (g->B < g->W) return false;
+    g->cap = std::min<uint32_t>(64, 64u * kHotEntriesPerLane / g->Smax);
+    if (g->cap < (uint32_t)kHotMaxGroups) return false;
     g->hot_bytes = (uint32_t)(((size_t)(h->n_hot + kHotZeroCells) * (h->wide ? sizeof(double) : sizeof(float)) + 15) /
                               16 * 16);
-    g->lds = hot_lds_bytes(g->hot_bytes, g->B, g->Smax);
+    g->lds = hot_lds_bytes(g->hot_bytes, g->cap, g->Smax);
     return true;
 }
 
@@ -225,6 +236,11 @@ bool hot_plan(const scd_solver* h, int64_t window, HotGeom* g) {
            shared_bytes(h) <= kPipeMaxBytes && hot_geometry(h, window, g) && g->lds <= h->max_lds;
 }
 
+// Segment lengths too skewed for the team kernel's fixed-stride walk.
+bool skewed_for_teams(const scd_solver* h) {
+    return h->C > 0 && (double)h->max_seg > kTeamMaxSkew * ((double)h->nnz / (double)h->C);
+}
+
 // Members per in-flight coordinate of the team kernel for the current options, and the number of
 // teams (0 = the team kernel does not apply).  Teams hold one coordinate each between gather and
 // scatter, as draining pipelined groups do, and take the same share of the window.
@@ -242,12 +258,12 @@ int team_members(const scd_solver* h, int64_t* teams) {
     // flight; worst ratio 1.49 over 24 runs of 8 epochs, against 1.80 at 32).
     if (h->window == 0) groups = std::max<int64_t>(1, groups * 7 / 8);
     int64_t K;
+    if (skewed_for_teams(h)) return 0;
     if (h->team >= 2) {
         K = h->team;
     } else {
         const double mean = (double)h->nnz / (double)h->C;
-        if (mean < kTeamMinMean || shared_bytes(h) < kTeamMinSharedBytes || (double)h->max_seg > kTeamMaxSkew * mean)
-            return 0;
+        if (mean < kTeamMinMean || shared_bytes(h) < kTeamMinSharedBytes) return 0;
         K = std::min<int64_t>(kTeamMax, h->cus / groups);
     }
     // A member's part beyond the register slices is streamed twice and stays between gather and
@@ -306,7 +322,8 @@ int plan_epoch(const scd_solver* h, LaunchPlan* lp, uint32_t* n_groups) {
         lp->group = 8;
         lp->blocks = 1;
         lp->lds_bytes = hg.lds;
-        *n_groups = hg.W;
+        // Coordinates in flight at most: what the consumers hold when the window adapts.
+        *n_groups = hg.adaptive ? hg.NC * kHotMaxGroups : hg.W;
         return SCD_OK;
     }
     const int64_t cap_blocks = (int64_t)h->cus * kBlocksPerCU;
@@ -319,7 +336,7 @@ int plan_epoch(const scd_solver* h, LaunchPlan* lp, uint32_t* n_groups) {
         if (groups < 1) groups = 1;
         if (pipe_ok) groups = pipe_groups(h, window, groups);
         lp->kind = pipe_ok ? PLAN_PIPE : PLAN_BLOCK;
-        lp->drain = pipe_ok ? pipe_drain(h, window, groups) : 0;
+        lp->drain = pipe_drain(h, window, groups);
         lp->unbound = window >= h->C;
         lp->group = kBlockThreads;
         lp->blocks = (int)groups;
@@ -364,6 +381,7 @@ int plan_epoch(const scd_solver* h, LaunchPlan* lp, uint32_t* n_groups) {
     lp->kind = skewed ? PLAN_MIXED : PLAN_GROUP;
     lp->long_len = (uint32_t)long_len;
     lp->tail = h->max_seg > (int64_t)G * slice_depth(G);
+    if (lp->kind == PLAN_GROUP) lp->drain = pipe_drain(h, window, groups);
     if (!skewed && pipe_ok) {
         groups = pipe_groups(h, window, groups);
         lp->kind = PLAN_PIPE;  // segments beyond the slices take its long path
@@ -590,12 +608,7 @@ int obj_group(const scd_solver* h) {
     return G > 64 ? 64 : G;
 }
 
-int obj_blocks(const scd_solver* h, int G) {
-    int64_t b = (h->C * G + kBlockThreads - 1) / kBlockThreads;
-    if (b > kObjBlocksMax) b = kObjBlocksMax;
-    if (b < 1) b = 1;
-    return (int)b;
-}
+int obj_blocks(const scd_solver* h, int G) { return objective_blocks(h->C, G); }
 
 int check_handle(scd_handle_t h) {
     if (!h) return fail(SCD_ERR_INVALID, "null handle");
@@ -623,6 +636,7 @@ void release(scd_solver* h) {
     (void)hipFree(h->sink);
     (void)hipFree(h->us);
     (void)hipFree(h->queue);
+    (void)hipFree(h->hot_adapt);
     (void)hipFree(h->entry_key);
     (void)hipFree(h->hot_ids);
     (void)hipFree(h->hot_err);
@@ -667,20 +681,7 @@ int reduce_state(scd_solver* h, hipStream_t s) {
 }
 
 void objectives_from_sums(const scd_solver* h, const double* t, double* P, double* D) {
-    const double N = (double)h->n_rows, lam = h->lambda;
-    if (h->form == FORM_RIDGE_PRIMAL) {
-        // t0 = sum_m <a_m, r>^2, t1 = |beta|^2, t3 = |r|^2, t4 = <r, y>,  r = y - w, w = A beta.
-        *P = t[3] / (2.0 * N) + 0.5 * lam * t[1];
-        *D = -t[3] / (2.0 * N) - t[0] / (2.0 * lam * N * N) + t[4] / N;
-    } else if (h->form == FORM_SVM_DUAL) {
-        // t0 = sum hinge, t1 = sum alpha, t3 = |w|^2.
-        *P = t[0] / N + 0.5 * lam * t[3];
-        *D = t[1] / N - 0.5 * lam * t[3];
-    } else {
-        // t0 = |A wbar / lambda - y|^2, t1 = |alpha|^2, t2 = <alpha, y>, t3 = |wbar|^2.
-        *P = t[0] / (2.0 * N) + 0.5 * t[3] / lam;
-        *D = -0.5 * N * t[1] - t[3] / (2.0 * lam) + t[2];
-    }
+    scd::objectives_from_sums(h->form, (double)h->n_rows, h->lambda, t, P, D);
 }
 
 }  // namespace
@@ -772,6 +773,8 @@ int scd_create(const scd_matrix_t* A, const float* y, double lambda, int32_t for
         hip(hipMalloc(&h->sink, sink_bytes), "hipMalloc(sink)");
         hip(hipMemsetAsync(h->sink, 0, sink_bytes, s), "zero sink");
         hip(hipMalloc(&h->queue, 2 * sizeof(uint32_t)), "hipMalloc(queue)");
+        hip(hipMalloc(&h->hot_adapt, 2 * sizeof(uint32_t)), "hipMalloc(hot_adapt)");
+        hip(hipMemsetAsync(h->hot_adapt, 0, 2 * sizeof(uint32_t), s), "zero hot_adapt");
         if ((h->L << kSpreadShift) <= kSpreadMaxBytes) hip(hipMalloc(&h->us, (size_t)h->L << kSpreadShift), "hipMalloc(spread)");
         hip(hipMemsetAsync(h->queue, 0, 2 * sizeof(uint32_t), s), "zero queue");
     }
@@ -893,8 +896,8 @@ int scd_epochs(scd_handle_t h, uint64_t seed, int32_t n_epochs, void* stream) {
     if (lp.kind == PLAN_ORDERED_LDS) HIP_TRY(ordered_lds_prepare(h->form, lp.wide != 0, lp.lds_bytes));
     HotGeom hg{};
     if (lp.kind == PLAN_HOT) {
-        hot_plan(h, n_groups, &hg);
-        HIP_TRY(hot_prepare(h->form, h->wide != 0, hg.lds));
+        hot_plan(h, h->window ? h->window : h->auto_window, &hg);
+        HIP_TRY(hot_prepare(h->form, h->wide != 0, hg.Smax, hg.lds));
     }
     EpochArgs a{};
     a.ptr = h->ptr;
@@ -944,7 +947,7 @@ int scd_epochs(scd_handle_t h, uint64_t seed, int32_t n_epochs, void* stream) {
             ta.tag0 = h->team_tag;
             ta.spin_limit = h->hot_wait_limit > 0 ? (uint32_t)h->hot_wait_limit : kHotSpinLimit;
             ta.err = h->hot_err;
-            HIP_TRY(launch_epoch_team(h->form, h->wide != 0, lp.fresh != 0, ta, lp.blocks, s));
+            HIP_TRY(launch_epoch_team(h->form, h->wide != 0, lp.fresh != 0, ta, lp.blocks, h->cus, s));
             // Steps of the busiest team, plus one: the next launch's tags are all new.
             h->team_tag += (uint32_t)((h->C + n_groups - 1) / n_groups + 1);
         } else if (lp.kind == PLAN_HOT) {
@@ -954,9 +957,15 @@ int scd_epochs(scd_handle_t h, uint64_t seed, int32_t n_epochs, void* stream) {
             ha.hot_ids = h->hot_ids;
             ha.n_hot = h->n_hot;
             ha.W = hg.W;
-            ha.B = hg.B;
+            ha.NC = hg.NC;
+            ha.cap = hg.cap;
             ha.Smax = hg.Smax;
             ha.hot_bytes = hg.hot_bytes;
+            ha.w_rule = hg.W;
+            // The first epoch after the state or the options changed runs at the rule's window.
+            ha.adapt_in = hg.adaptive && !h->adapt_fresh ? h->hot_adapt : nullptr;
+            ha.adapt_out = hg.adaptive ? h->hot_adapt : nullptr;
+            h->adapt_fresh = 0;
             ha.spin_limit = h->hot_wait_limit > 0 ? (uint32_t)h->hot_wait_limit : kHotSpinLimit;
             ha.err = h->hot_err;
             HIP_TRY(launch_epoch_hot(h->form, h->wide != 0, ha, hg.lds, s));
@@ -1039,6 +1048,7 @@ int scd_set_state(scd_handle_t h, const float* model, const float* shared, int64
     if (int r = set_device(h)) return r;
     hipStream_t s = (hipStream_t)stream;
     HIP_TRY(hipMemsetAsync(h->hot_err, 0, sizeof(int), s));  // a written state replaces an invalid one
+    h->adapt_fresh = 1;  // the moving fraction of the previous epochs says nothing about this state
     if (model) HIP_TRY(hipMemcpyAsync(h->model, model, sizeof(float) * (size_t)h->C, hipMemcpyDeviceToDevice, s));
     if (shared) {
         if (h->wide)
@@ -1053,7 +1063,13 @@ int scd_set_state(scd_handle_t h, const float* model, const float* shared, int64
 int scd_set_option(scd_handle_t h, const char* key, int64_t value) {
     if (int r = check_handle(h)) return r;
     if (!key) return fail(SCD_ERR_INVALID, "key is null");
-    if (!strcmp(key, "window")) {
+    h->adapt_fresh = 1;  // the next hot-set epoch starts again from the rule's window
+    if (!strcmp(key, "adapt")) {
+        if (value != 0 && value != 1) return fail(SCD_ERR_INVALID, "adapt must be 0 or 1");
+        h->adapt = value;
+        if (int r = set_device(h)) return r;
+        if (int r = hot_if_needed(h, nullptr)) return r;
+    } else if (!strcmp(key, "window")) {
         if (value < 0 || value > 2147483647LL) return fail(SCD_ERR_INVALID, "window must be in [0, 2^31)");
         h->window = value;
         if (int r = set_device(h)) return r;
@@ -1074,6 +1090,14 @@ int scd_set_option(scd_handle_t h, const char* key, int64_t value) {
         if (int r = team_if_needed(h, nullptr)) return r;
     } else if (!strcmp(key, "team")) {
         if (value < 0 || value > kTeamMax) return fail(SCD_ERR_INVALID, "team must be in [0, %d]", kTeamMax);
+        // Teams walk positions at a fixed stride; on skewed segment lengths those that draw long
+        // segments fall behind and the processing order drifts from the permutation (a forced team
+        // of 4 on the skewed text-ridge columns reached 2.28x the sequential per-epoch gap).
+        if (value >= 2 && skewed_for_teams(h))
+            return fail(SCD_ERR_UNSUPPORTED,
+                        "team %lld: the longest segment (%lld entries) exceeds %.0f times the mean; skewed lengths "
+                        "take the queued kernel",
+                        (long long)value, (long long)h->max_seg, kTeamMaxSkew);
         h->team = value;
         if (int r = set_device(h)) return r;
         if (int r = team_if_needed(h, nullptr)) return r;
@@ -1133,6 +1157,28 @@ int scd_get_option(scd_handle_t h, const char* key, int64_t* value) {
     else if (!strcmp(key, "hot_wait_limit")) *value = h->hot_wait_limit;
     else if (!strcmp(key, "team")) *value = h->team;
     else if (!strcmp(key, "shared_fp64")) *value = h->wide;
+    else if (!strcmp(key, "adapt")) *value = h->adapt;
+    else if (!strcmp(key, "next_window")) {
+        // Coordinates in flight the next epoch will use (read-only; synchronises the device).
+        LaunchPlan lp;
+        uint32_t n_groups = 1;
+        plan_epoch(h, &lp, &n_groups);
+        HotGeom hg{};
+        const int64_t window = h->window ? h->window : h->auto_window;
+        if (lp.kind == PLAN_HOT && hot_plan(h, window, &hg) && hg.adaptive) {
+            uint32_t v = 0;
+            if (!h->adapt_fresh) {
+                if (int r = set_device(h)) return r;
+                HIP_TRY(hipDeviceSynchronize());
+                HIP_TRY(hipMemcpy(&v, h->hot_adapt, sizeof v, hipMemcpyDeviceToHost));
+            }
+            *value = v ? (int64_t)v : window;
+        } else {
+            scd_info_t info;
+            scd_get_info(h, &info);
+            *value = info.window;
+        }
+    }
     else return fail(SCD_ERR_UNSUPPORTED, "unknown option '%s'", key);
     return SCD_OK;
 }
@@ -1152,6 +1198,10 @@ int scd_get_info(scd_handle_t h, scd_info_t* info) {
                                                                : 1024;
     info->kernel = lp.kind;
     info->hot_entries = (int32_t)h->n_hot;
+    HotGeom hg{};
+    info->adaptive_window = lp.kind == PLAN_HOT && hot_plan(h, h->window ? h->window : h->auto_window, &hg) &&
+                            hg.adaptive;
+    info->reserved = 0;
     info->long_len = lp.kind == PLAN_MIXED ? lp.long_len : 0;
     info->shared_fp64 = h->wide;
     info->max_hits = h->max_hits;
@@ -1160,8 +1210,11 @@ int scd_get_info(scd_handle_t h, scd_info_t* info) {
     info->nnz = h->nnz;
     info->epoch = h->epoch;
     info->max_segment = h->max_seg;
-    // Coordinates in flight at most: a pipelined group that does not drain holds two.
-    info->window = lp.kind == PLAN_PIPE && !lp.drain ? std::min<int64_t>(2 * (int64_t)n_groups, h->C) : n_groups;
+    // Coordinates in flight at most: a group that does not drain holds two (its previous scatter may
+    // not have landed when it gathers again).
+    const bool two = (lp.kind == PLAN_PIPE || lp.kind == PLAN_GROUP || (lp.kind == PLAN_BLOCK && !lp.ordered)) &&
+                     !lp.drain;
+    info->window = two ? std::min<int64_t>(2 * (int64_t)n_groups, h->C) : n_groups;
     info->lambda = h->lambda;
     info->coupling = h->coupling;
     info->coherence = h->coherence;

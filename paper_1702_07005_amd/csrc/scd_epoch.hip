@@ -48,6 +48,9 @@ __global__ __launch_bounds__(256) void k_epoch_group(EpochArgs a) {
     float cv[R];
     load_seg<G, R>(a, cur, lane, ci, cv);
     for (;;) {
+        // With a binding window the previous coordinate's atomics land first (the group lives in
+        // one wave, whose completion counter covers them all).
+        if (a.drain) __builtin_amdgcn_s_waitcnt(0x0F70);  // vmcnt(0)
         float gv[R];
 #pragma unroll
         for (int r = 0; r < R; ++r) gv[r] = ld_u<FRESH>(uu + ci[r]);
@@ -144,7 +147,12 @@ __device__ __forceinline__ bool pipe_step(const EpochArgs& a, const SharedBuf<U>
                                           float (*part)[G > 64 ? G / 64 : 1], int& buf) {
     // When the window binds, the previous coordinate's atomics (the wave's latest operations) must
     // land before this coordinate gathers, so that a group never has two coordinates in flight.
-    if (a.drain) __builtin_amdgcn_s_waitcnt(0x0F70);  // vmcnt(0)
+    // A wave's wait covers only its own atomics: with G = 256 the group spans four waves, and a
+    // barrier after the wait holds every wave's gathers until all four have landed theirs.
+    if (a.drain) {
+        __builtin_amdgcn_s_waitcnt(0x0F70);  // vmcnt(0)
+        if constexpr (G > 64) __builtin_amdgcn_s_barrier();
+    }
     const int64_t len = cur.s1 - cur.s0;
     if (len > (int64_t)G * R) {
         pipe_long<FORM, G, R, FRESH, U>(a, ub, lane, j, cur, nxt, ni, nv, nn, part, buf);
@@ -259,7 +267,10 @@ __device__ __forceinline__ uint32_t queue_step(const EpochArgs& a, const SharedB
                                                uint32_t* ring, uint32_t& claim, float (*part)[4], int& buf) {
     constexpr int G = 256;
     const uint32_t K = a.chunk;
-    __builtin_amdgcn_s_waitcnt(0x0F70);  // vmcnt(0): this workgroup's atomics and its last claim have landed
+    // vmcnt(0): this wave's atomics and its last claim have landed; the barrier extends that to the
+    // atomics of all four waves before any of them gathers the next coordinate.
+    __builtin_amdgcn_s_waitcnt(0x0F70);
+    __builtin_amdgcn_s_barrier();
     // The previous step claimed chunk (k - 1 + kQueueLead) / K if it began one.
     if (lane == 0 && k > 0 && (k - 1 + kQueueLead) % K == 0) ring[((k - 1 + kQueueLead) / K) % kQueueRing] = claim;
     const uint32_t n = a.perm.n;
@@ -470,6 +481,14 @@ __global__ __launch_bounds__(BS) void k_epoch_block(EpochArgs a) {
     int buf = 0;
     if (blockIdx.x >= a.n_groups) return;
     for (uint32_t j = blockIdx.x; j < a.perm.n; j += a.n_groups) {
+        if constexpr (!ORDERED) {
+            // With a binding window every wave's atomics of the previous coordinate land before any
+            // wave gathers this one, so a workgroup holds one coordinate between gather and scatter.
+            if (a.drain) {
+                __builtin_amdgcn_s_waitcnt(0x0F70);  // vmcnt(0)
+                __builtin_amdgcn_s_barrier();
+            }
+        }
         const uint32_t m = perm_at(j, a.perm);
         const int64_t s0 = a.ptr[m], s1 = a.ptr[m + 1];
         const float m_old = a.model[m];

@@ -1,6 +1,6 @@
-// scd_hot.hip -- the hot-set epoch kernel for gfx950 (windows of at most 8 coordinates: the
-// most-updated shared-vector entries in LDS, one consumer wave, producer waves) and the set-up
-// that chooses the hot set and each stored entry's slot.
+// scd_hot.hip -- the hot-set epoch kernel for gfx950 (windows of at most 16 coordinates: the
+// most-updated shared-vector entries in LDS, one or two consumer waves, producer waves) and the
+// set-up that chooses the hot set and each stored entry's slot.
 #include "scd_device.h"
 
 namespace scd {
@@ -15,19 +15,30 @@ namespace scd {
 // back at the end), so their gathers and atomic adds stay inside the CU and are seen at once
 // by the other in-flight coordinates, which all run in the same workgroup.
 //
-// Wave 0 (the consumer) runs the W in-flight coordinates, 8 lanes each, and reads nothing but
-// LDS.  Waves 1..kHotProducers fill per-producer LDS buffers with the next batches of B
-// permutation positions: each coordinate's metadata and, per stored entry, its value and
-// either its hot slot or (cold entry) its index and current shared-vector value.  Each wave
-// has its own completion counter, so the producers' load latency never stalls the consumer.
+// Waves 0..NC-1 (the consumers, NC = 1 or 2) run the in-flight coordinates, 8 lanes each and at
+// most kHotMaxGroups per wave, and read nothing but LDS; batch b goes to consumer b mod NC, and
+// each consumer steps through its batches independently of the other (their hot-entry updates
+// meet in LDS atomics).  The other NP = kHotWaves - NC waves (producers) fill per-producer LDS
+// buffers with the next batches of permutation positions: each coordinate's metadata and, per
+// stored entry, its value and either its hot slot or (cold entry) its index and current
+// shared-vector value.  Each wave has its own completion counter, so the producers' load latency
+// never stalls a consumer.
+//
+// Adaptive window.  Only coordinates whose step is nonzero change the shared vector, so only they
+// make the reads of the others stale.  When the window is automatic, each epoch counts the
+// coordinates that moved and sets the next epoch's window so that the expected number of moving
+// coordinates in flight stays at what the coupling rule allows: W = 1 + (w_rule - 1) / f, f the
+// fraction that moved (in the hinge SVM dual most coordinates sit at a bound of the box and do not
+// move).  The first epoch runs at w_rule; the window lives in device memory, so the epochs of one
+// call need no synchronisation with the host.
 // Cold values are therefore read up to a few batches before their coordinate runs; cold
 // entries are by construction rarely updated, so such a read seldom misses an update.
 // Producer and consumer hand buffers over through LDS sequence numbers; every wait is bounded
 // (spin_limit sleeps), after which the wave sets *err and all waves leave.
 // ----------------------------------------------------------------------------------------
-size_t hot_lds_bytes(uint32_t hot_bytes, uint32_t B, uint32_t Smax) {
+size_t hot_lds_bytes(uint32_t hot_bytes, uint32_t cap, uint32_t Smax) {
     return (size_t)hot_bytes + kHotFlagBytes + kHotScratchBytes +
-           (size_t)kHotProducers * hot_buf_words(B, Smax) * sizeof(uint32_t);
+           (size_t)kHotMaxProducers * hot_buf_words(cap, Smax) * sizeof(uint32_t);
 }
 
 __device__ __forceinline__ bool hot_wait(uint32_t* flag, uint32_t want, uint32_t* abort_flag, uint32_t limit,
@@ -45,7 +56,8 @@ __device__ __forceinline__ bool hot_wait(uint32_t* flag, uint32_t want, uint32_t
     }
 }
 
-// One batch buffer in LDS (B coordinates, Smax entry slots each; 32-bit words, 16-byte aligned).
+// One batch buffer in LDS (room for cap coordinates of Smax entry slots each; 32-bit words, 16-byte
+// aligned).  The layout depends on cap only, so batches of different sizes share it.
 struct HotBuf {
     float4* rec;    // [B]: model value, step scale, label or <y, a_m>, cold part of the gathered dot;
                     // the consumer then overwrites .z and .w with the new model value and the
@@ -56,11 +68,11 @@ struct HotBuf {
     uint32_t* mid;  // [B]: coordinate index, or kHotEmpty for positions past the end of the epoch
 };
 
-__device__ __forceinline__ HotBuf hot_buf(uint32_t* base, uint32_t B, uint32_t Smax) {
+__device__ __forceinline__ HotBuf hot_buf(uint32_t* base, uint32_t cap, uint32_t Smax) {
     HotBuf b;
     b.rec = reinterpret_cast<float4*>(base);
-    b.kv = reinterpret_cast<int2*>(base + 4u * B);
-    b.mid = base + 4u * B + 2u * B * Smax;
+    b.kv = reinterpret_cast<int2*>(base + 4u * cap);
+    b.mid = base + 4u * cap + 2u * cap * Smax;
     return b;
 }
 
@@ -152,36 +164,38 @@ __device__ __forceinline__ void hot_step(const StepConsts& k, U* hot, const HotB
     }
 }
 
-// The consumer for coordinates of at most 8 * SL entries: the steps of each batch, unrolled twice
-// so that the two step records alternate instead of being copied (a copy would wait for the
+// Consumer `ci` for coordinates of at most 8 * SL entries: the steps of each of its batches, unrolled
+// twice so that the two step records alternate instead of being copied (a copy would wait for the
 // prefetch).  Hot entries are updated in LDS; the new model value and the coefficient go back into
 // the batch buffer, and the producer that owns it issues the global stores and atomics before
 // refilling it, so this wave never waits on global memory.
 template <int FORM, typename U, int SL>
-__device__ __forceinline__ void hot_consumer(const HotArgs& h, U* hot, uint32_t* ready, uint32_t* freed,
-                                             uint32_t* abort_flag, uint32_t* bufs, float* scr, uint32_t nb,
-                                             int lane) {
+__device__ __forceinline__ void hot_consumer(const HotArgs& h, const HotSched& sc, uint32_t ci, U* hot,
+                                             uint32_t* ready, uint32_t* freed, uint32_t* abort_flag, uint32_t* bufs,
+                                             float* scr, int lane) {
     const StepConsts k = h.e.k;
-    const uint32_t B = h.B, Smax = h.Smax, W = h.W, bw = hot_buf_words(B, Smax), S = B / W;
+    const uint32_t Smax = h.Smax, W = hot_groups(sc, ci), B = hot_batch(sc, ci), bw = hot_buf_words(h.cap, Smax);
+    const uint32_t S = B / W;
     const uint32_t g = (uint32_t)lane >> 3, sub = (uint32_t)lane & 7u;
     const bool act = g < W;
     const uint32_t g0 = act ? g : 0u;  // inactive lanes read coordinate 0 of each step and write nothing
-    for (uint32_t b = 0; b < nb; ++b) {
-        const uint32_t p = b % kHotProducers, n = b / kHotProducers;
+    float* const my_scr = scr + ci * 128u;
+    for (uint32_t b = ci; b < sc.nb; b += sc.NC) {
+        const uint32_t p = b % sc.NP, n = b / sc.NP;
         if (!hot_wait(ready + p, n + 1, abort_flag, h.spin_limit, h.err)) return;
-        const HotBuf hb = hot_buf(bufs + p * bw, B, Smax);
+        const HotBuf hb = hot_buf(bufs + p * bw, h.cap, Smax);
         HotStep<SL> sa, sb;
         hot_load_step<SL>(sa, hb, g0, g0 * Smax + sub);
         uint32_t st = 0;
         for (; st + 1 < S; st += 2) {
             const uint32_t c0 = st * W + g0, c1 = c0 + W;
             const uint32_t c2 = st + 2 < S ? c1 + W : c1;
-            hot_step<FORM, U, SL>(k, hot, hb, scr, Smax, c1, act, sub, lane, sa, c0, sb);
-            hot_step<FORM, U, SL>(k, hot, hb, scr, Smax, c2, act, sub, lane, sb, c1, sa);
+            hot_step<FORM, U, SL>(k, hot, hb, my_scr, Smax, c1, act, sub, lane, sa, c0, sb);
+            hot_step<FORM, U, SL>(k, hot, hb, my_scr, Smax, c2, act, sub, lane, sb, c1, sa);
         }
         if (st < S) {
             const uint32_t c0 = st * W + g0;
-            hot_step<FORM, U, SL>(k, hot, hb, scr, Smax, c0, act, sub, lane, sa, c0, sb);
+            hot_step<FORM, U, SL>(k, hot, hb, my_scr, Smax, c0, act, sub, lane, sa, c0, sb);
         }
         __hip_atomic_store(freed + p, n + 1, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_WORKGROUP);
     }
@@ -196,9 +210,10 @@ struct HotMeta {
     float m_old, sn, ylab;
 };
 
-__device__ __forceinline__ uint32_t hot_coord(const EpochArgs& a, uint32_t b, uint32_t B, uint32_t nb, int lane) {
-    const uint32_t j = b * B + (uint32_t)lane;
-    return b < nb && (uint32_t)lane < B && j < a.perm.n ? perm_at(j, a.perm) : kHotEmpty;
+__device__ __forceinline__ uint32_t hot_coord(const EpochArgs& a, const HotSched& sc, uint32_t b, int lane) {
+    if (b >= sc.nb || (uint32_t)lane >= hot_batch_size(sc, b)) return kHotEmpty;
+    const uint32_t j = hot_batch_start(sc, b) + (uint32_t)lane;
+    return j < a.perm.n ? perm_at(j, a.perm) : kHotEmpty;
 }
 
 __device__ __forceinline__ void hot_meta_load(const EpochArgs& a, HotMeta& t) {
@@ -222,7 +237,8 @@ __device__ __forceinline__ U hot_load_u(const SharedBuf<U>& b, uint32_t i, bool 
         return __builtin_bit_cast(double, __builtin_amdgcn_raw_buffer_load_b64(b.r, (int)off, 0, 0));
 }
 
-// Producer wave q fills buffer q with batches q, q + kHotProducers, ...  Slot e = t * 64 + lane of a
+// Producer wave q fills buffer q with batches q, q + NP, ...  (NP is a multiple of NC, so the batches
+// of one buffer all go to the same consumer and have the same size.)  Slot e = t * 64 + lane of a
 // batch holds entry e % Smax of coordinate e / Smax; since Smax is a multiple of 8, each aligned
 // group of 8 lanes holds entries of one coordinate.  Per slot the producer loads the entry's key
 // (hot slot or index, precomputed for every stored entry) and value, and a cold entry's
@@ -233,19 +249,24 @@ __device__ __forceinline__ U hot_load_u(const SharedBuf<U>& b, uint32_t i, bool 
 // device-scope atomics for the cold entries' updates) after, so that no wait for this batch's loads
 // also waits for those stores and atomics.  The cold entries' indices and values stay in registers
 // until that write-out.
+// Adds to *moved_total the coordinates of its batches whose step was nonzero.
 template <int FORM, typename U>
-__device__ __forceinline__ void hot_producer(const HotArgs& h, uint32_t* ready, uint32_t* freed, uint32_t* abort_flag,
-                                             uint32_t* bufs, uint32_t nb, int q, int lane) {
+__device__ __forceinline__ void hot_producer(const HotArgs& h, const HotSched& sc, uint32_t* ready, uint32_t* freed,
+                                             uint32_t* abort_flag, uint32_t* bufs, uint32_t* moved_total, int q,
+                                             int lane) {
     const EpochArgs& a = h.e;
     U* const uu = static_cast<U*>(a.u);
     const SharedBuf<U> ub = shared_buf<U>(a.u, a.u_bytes, nullptr, a.u_shift);
-    const uint32_t B = h.B, Smax = h.Smax, NB = B * Smax;
-    const HotBuf hb = hot_buf(bufs + q * hot_buf_words(B, Smax), B, Smax);
+    const uint32_t Smax = h.Smax, nb = sc.nb, NP = sc.NP;
+    // Every batch of this buffer goes to consumer q mod NC and has that consumer's size.
+    const uint32_t B = hot_batch(sc, hot_consumer_of(sc, (uint32_t)q)), NB = B * Smax;
+    const HotBuf hb = hot_buf(bufs + q * hot_buf_words(h.cap, Smax), h.cap, Smax);
     constexpr int NE = kHotEntriesPerLane;
     const uint32_t c0 = (uint32_t)lane / Smax, k0 = (uint32_t)lane - c0 * Smax;
     const uint32_t dc = 64u / Smax, dk = 64u - dc * Smax;
     HotMeta md;
-    md.m = hot_coord(a, (uint32_t)q, B, nb, lane);
+    md.m = hot_coord(a, sc, (uint32_t)q, lane);
+    uint32_t moved = 0;  // this lane's coordinates whose step was nonzero
     hot_meta_load(a, md);
     int32_t fl_ix[NE];  // the buffer's current batch: cold entries' indices and values (0: none)
     float fl_v[NE];
@@ -254,14 +275,14 @@ __device__ __forceinline__ void hot_producer(const HotArgs& h, uint32_t* ready, 
         fl_ix[t] = 0;
         fl_v[t] = 0.0f;
     }
-    for (uint32_t b = (uint32_t)q; b < nb + kHotProducers; b += kHotProducers) {
-        const uint32_t n = b / kHotProducers;
+    for (uint32_t b = (uint32_t)q; b < nb + NP; b += NP) {
+        const uint32_t n = b / NP;
         int32_t ky[NE];  // entry key: -1 - hot slot, or the shared-vector index of a cold entry
         float vv[NE];
         bool in[NE];
         float part[NE];  // cold part of the dot, summed over each aligned group of 8 lanes
         HotMeta nx;
-        nx.m = hot_coord(a, b + kHotProducers, B, nb, lane);
+        nx.m = hot_coord(a, sc, b + NP, lane);
         if (b < nb) {
             // Entries (entry 0 stands in for unused slots): key and value.
             const uint32_t len = md.m != kHotEmpty ? (uint32_t)(md.s1 - md.s0) : 0u;
@@ -294,7 +315,7 @@ __device__ __forceinline__ void hot_producer(const HotArgs& h, uint32_t* ready, 
         }
         // The buffer's previous batch (if any) must have been consumed.
         if (n > 0 || b < nb) {
-            if (!hot_wait(freed + q, n, abort_flag, h.spin_limit, h.err)) return;
+            if (!hot_wait(freed + q, n, abort_flag, h.spin_limit, h.err)) break;
         }
         // Read out the consumed batch: new model values, and each cold entry's update (the
         // coordinate's coefficient times the entry's value, the product the consumer formed for
@@ -305,7 +326,9 @@ __device__ __forceinline__ void hot_producer(const HotArgs& h, uint32_t* ready, 
         if (n > 0) {
             if ((uint32_t)lane < B) {
                 old_m = hb.mid[lane];
-                old_model = hb.rec[lane].z;
+                const float2 zw = *reinterpret_cast<const float2*>(&hb.rec[lane].z);
+                old_model = zw.x;
+                moved += (old_m != kHotEmpty && zw.y != 0.0f) ? 1u : 0u;
             }
             uint32_t c = c0, k = k0;
 #pragma unroll
@@ -363,77 +386,98 @@ __device__ __forceinline__ void hot_producer(const HotArgs& h, uint32_t* ready, 
         if (b >= nb) break;
         md = nx;
     }
+    for (int o = 32; o > 0; o >>= 1) moved += __shfl_xor(moved, o, 64);
+    if (lane == 0) atomicAdd(moved_total, moved);
 }
 
-template <int FORM, typename U>
-__global__ __launch_bounds__(64 * (1 + kHotProducers)) void k_epoch_hot(HotArgs h) {
+// SL: entries per consumer lane (Smax / 8), a template parameter so that each instance holds one
+// consumer variant.
+template <int FORM, typename U, int SL>
+__global__ __launch_bounds__(64 * kHotWaves) void k_epoch_hot(HotArgs h) {
     extern __shared__ __align__(16) unsigned char hot_lds[];
     const EpochArgs& a = h.e;
     U* const hot = reinterpret_cast<U*>(hot_lds);
     uint32_t* const ready = reinterpret_cast<uint32_t*>(hot_lds + h.hot_bytes);
-    uint32_t* const freed = ready + kHotProducers;
-    uint32_t* const abort_flag = freed + kHotProducers;
-    // Scratch: write targets of inactive consumer lanes.  The hot array ends with kHotZeroCells
-    // zero cells (one per consumer lane) that cold and padding slots point at.
+    uint32_t* const freed = ready + kHotMaxProducers;
+    uint32_t* const abort_flag = freed + kHotMaxProducers;
+    uint32_t* const moved = abort_flag + 1;
+    // Scratch: write targets of inactive consumer lanes (128 floats per consumer).  The hot array ends
+    // with kHotZeroCells zero cells (one per consumer lane) that cold and padding slots point at.
     float* const scr = reinterpret_cast<float*>(hot_lds + h.hot_bytes + kHotFlagBytes);
     uint32_t* const bufs = reinterpret_cast<uint32_t*>(hot_lds + h.hot_bytes + kHotFlagBytes + kHotScratchBytes);
-    static_assert((2 * kHotProducers + 1) * sizeof(uint32_t) <= kHotFlagBytes, "handover words exceed their area");
+    static_assert((2 * kHotMaxProducers + 2) * sizeof(uint32_t) <= kHotFlagBytes, "handover words exceed their area");
+    static_assert((kHotWaves - kHotMaxConsumers) % kHotMaxConsumers == 0, "a buffer's batches must share a consumer");
     U* const uu = static_cast<U*>(a.u);
     const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+    // This epoch's window: fixed, or set by the previous epoch of the adaptive plan.
+    uint32_t W = h.W;
+    if (h.adapt_in) {
+        const uint32_t v = __hip_atomic_load(h.adapt_in, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        if (v >= h.NC && v <= h.NC * (uint32_t)kHotMaxGroups) W = v;
+    }
+    const HotSched sc = hot_sched(W, h.NC, h.cap, a.perm.n);
     for (uint32_t i = tid; i < h.n_hot + kHotZeroCells; i += blockDim.x) hot[i] = i < h.n_hot ? uu[h.hot_ids[i]] : U(0);
-    if (tid < 2 * kHotProducers + 1) ready[tid] = 0u;  // ready, freed and abort are contiguous
+    if (tid < 2 * kHotMaxProducers + 2) ready[tid] = 0u;  // ready, freed, abort and moved are contiguous
     __syncthreads();
-    const uint32_t nb = (a.perm.n + h.B - 1) / h.B;
-    if (wave == 0) {
-        switch (h.Smax / 8) {  // entries per consumer lane
-            case 1: hot_consumer<FORM, U, 1>(h, hot, ready, freed, abort_flag, bufs, scr, nb, lane); break;
-            case 2: hot_consumer<FORM, U, 2>(h, hot, ready, freed, abort_flag, bufs, scr, nb, lane); break;
-            case 3: hot_consumer<FORM, U, 3>(h, hot, ready, freed, abort_flag, bufs, scr, nb, lane); break;
-            case 4: hot_consumer<FORM, U, 4>(h, hot, ready, freed, abort_flag, bufs, scr, nb, lane); break;
-            case 5: hot_consumer<FORM, U, 5>(h, hot, ready, freed, abort_flag, bufs, scr, nb, lane); break;
-            case 6: hot_consumer<FORM, U, 6>(h, hot, ready, freed, abort_flag, bufs, scr, nb, lane); break;
-            case 7: hot_consumer<FORM, U, 7>(h, hot, ready, freed, abort_flag, bufs, scr, nb, lane); break;
-            default: hot_consumer<FORM, U, 8>(h, hot, ready, freed, abort_flag, bufs, scr, nb, lane); break;
-        }
-    } else
-        hot_producer<FORM, U>(h, ready, freed, abort_flag, bufs, nb, wave - 1, lane);
+    if ((uint32_t)wave < sc.NC) {
+        hot_consumer<FORM, U, SL>(h, sc, (uint32_t)wave, hot, ready, freed, abort_flag, bufs, scr, lane);
+    } else {
+        hot_producer<FORM, U>(h, sc, ready, freed, abort_flag, bufs, moved, wave - (int)sc.NC, lane);
+    }
     __syncthreads();
     for (uint32_t i = tid; i < h.n_hot; i += blockDim.x) uu[h.hot_ids[i]] = hot[i];
+    // Next epoch's window: (W - 1) f kappa <= budget with a fraction f of the coordinates moving,
+    // i.e. W = 1 + (w_rule - 1) / f, at most what the consumers hold.  An epoch that gave up keeps
+    // the window.
+    if (h.adapt_out && tid == 0 && *abort_flag == 0u) {
+        const uint64_t mv = *moved, wmax = (uint64_t)h.NC * kHotMaxGroups;
+        uint64_t w = mv ? 1 + (uint64_t)(h.w_rule - 1) * a.perm.n / mv : wmax;
+        w = w < h.w_rule ? h.w_rule : w > wmax ? wmax : w;
+        __hip_atomic_store(h.adapt_out, (uint32_t)w, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    }
 }
 
-template <int FORM>
-static hipError_t hot_prepare_form(bool wide, size_t lds_bytes) {
-    const void* f = wide ? reinterpret_cast<const void*>(&k_epoch_hot<FORM, double>)
-                         : reinterpret_cast<const void*>(&k_epoch_hot<FORM, float>);
+// The kernel instance for a formulation, storage type and row width (Smax / 8 entries per consumer lane).
+template <int FORM, typename U>
+static const void* hot_kernel_sl(uint32_t sl) {
+    switch (sl) {
+        case 1: return reinterpret_cast<const void*>(&k_epoch_hot<FORM, U, 1>);
+        case 2: return reinterpret_cast<const void*>(&k_epoch_hot<FORM, U, 2>);
+        case 3: return reinterpret_cast<const void*>(&k_epoch_hot<FORM, U, 3>);
+        case 4: return reinterpret_cast<const void*>(&k_epoch_hot<FORM, U, 4>);
+        case 5: return reinterpret_cast<const void*>(&k_epoch_hot<FORM, U, 5>);
+        case 6: return reinterpret_cast<const void*>(&k_epoch_hot<FORM, U, 6>);
+        case 7: return reinterpret_cast<const void*>(&k_epoch_hot<FORM, U, 7>);
+        case 8: return reinterpret_cast<const void*>(&k_epoch_hot<FORM, U, 8>);
+        default: return nullptr;
+    }
+}
+
+static const void* hot_kernel(int form, bool wide, uint32_t Smax) {
+    const uint32_t sl = Smax / 8;
+    switch (form) {
+        case FORM_RIDGE_PRIMAL:
+            return wide ? hot_kernel_sl<FORM_RIDGE_PRIMAL, double>(sl) : hot_kernel_sl<FORM_RIDGE_PRIMAL, float>(sl);
+        case FORM_SVM_DUAL:
+            return wide ? hot_kernel_sl<FORM_SVM_DUAL, double>(sl) : hot_kernel_sl<FORM_SVM_DUAL, float>(sl);
+        case FORM_RIDGE_DUAL:
+            return wide ? hot_kernel_sl<FORM_RIDGE_DUAL, double>(sl) : hot_kernel_sl<FORM_RIDGE_DUAL, float>(sl);
+        default: return nullptr;
+    }
+}
+
+hipError_t hot_prepare(int form, bool wide, uint32_t Smax, size_t lds_bytes) {
+    const void* f = hot_kernel(form, wide, Smax);
+    if (!f) return hipErrorInvalidValue;
     return hipFuncSetAttribute(f, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds_bytes);
 }
 
-hipError_t hot_prepare(int form, bool wide, size_t lds_bytes) {
-    switch (form) {
-        case FORM_RIDGE_PRIMAL: return hot_prepare_form<FORM_RIDGE_PRIMAL>(wide, lds_bytes);
-        case FORM_SVM_DUAL: return hot_prepare_form<FORM_SVM_DUAL>(wide, lds_bytes);
-        case FORM_RIDGE_DUAL: return hot_prepare_form<FORM_RIDGE_DUAL>(wide, lds_bytes);
-        default: return hipErrorInvalidValue;
-    }
-}
-
-template <int FORM>
-static hipError_t launch_hot_form(bool wide, const HotArgs& h, size_t lds_bytes, hipStream_t s) {
-    const dim3 block(64 * (1 + kHotProducers));
-    if (wide)
-        hipLaunchKernelGGL((k_epoch_hot<FORM, double>), dim3(1), block, lds_bytes, s, h);
-    else
-        hipLaunchKernelGGL((k_epoch_hot<FORM, float>), dim3(1), block, lds_bytes, s, h);
-    return hipGetLastError();
-}
-
 hipError_t launch_epoch_hot(int form, bool wide, const HotArgs& h, size_t lds_bytes, hipStream_t s) {
-    switch (form) {
-        case FORM_RIDGE_PRIMAL: return launch_hot_form<FORM_RIDGE_PRIMAL>(wide, h, lds_bytes, s);
-        case FORM_SVM_DUAL: return launch_hot_form<FORM_SVM_DUAL>(wide, h, lds_bytes, s);
-        case FORM_RIDGE_DUAL: return launch_hot_form<FORM_RIDGE_DUAL>(wide, h, lds_bytes, s);
-        default: return hipErrorInvalidValue;
-    }
+    const void* f = hot_kernel(form, wide, h.Smax);
+    if (!f) return hipErrorInvalidValue;
+    HotArgs arg = h;
+    void* args[] = {&arg};
+    return hipLaunchKernel(f, dim3(1), dim3(64 * kHotWaves), args, lds_bytes, s);
 }
 
 // ----------------------------------------------------------------------------------------

@@ -45,7 +45,7 @@ struct EpochArgs {
                          // entry size (2 or 3), or kSpreadShift when u is the spread copy
     double* sink;        // pipelined kernel, fp64 shared vector: 256 slots per workgroup that
                          // inactive lanes add 0 to
-    uint32_t drain;      // pipelined kernel: wait for the group's own atomics before its next gathers
+    uint32_t drain;      // wait for the group's own atomics before its next gathers (window binds)
     uint32_t chunk;      // queued kernel: consecutive positions per claim (1..kQueueChunkMax)
     uint32_t* queue;     // queued kernel: [0] next permutation position, [1] workgroups finished (both 0
                          // between launches)
@@ -77,7 +77,8 @@ struct LaunchPlan {
     uint32_t L;      // shared-vector length (PLAN_ORDERED_LDS)
     uint32_t long_len;  // PLAN_MIXED: segments longer than this go to the whole workgroup
     int tail;           // PLAN_GROUP: some segment is longer than the register slices
-    int drain;          // PLAN_PIPE: the window binds, so each group lets its scatter land before it gathers again
+    int drain;          // PLAN_PIPE, PLAN_GROUP, PLAN_BLOCK: the window binds, so each group lets its scatter
+                        // land before it gathers again
     int chunk;          // PLAN_QUEUE: consecutive permutation positions per claim
     int wide;           // shared vector stored as double
     int unbound;        // PLAN_PIPE: the window does not bind (every coordinate may be in flight)
@@ -100,15 +101,19 @@ struct ObjArgs {
     double lam;
 };
 
-// Hot-set epoch (one workgroup): the n_hot most-updated shared-vector entries live in LDS for the
-// epoch; one consumer wave runs the W in-flight coordinates from LDS only, kHotProducers waves stream
-// the next batches (segment, hot slot or cold value) into LDS buffers.
-constexpr int kHotProducers = 11;
+// Hot-set epoch (one workgroup of kHotWaves waves): the n_hot most-updated shared-vector entries live
+// in LDS for the epoch; one or two consumer waves run the in-flight coordinates from LDS only (each
+// up to kHotMaxGroups of them, 8 lanes each), and the other waves stream the next batches (segment,
+// hot slot or cold value) into LDS buffers, one buffer per producer.
+constexpr int kHotWaves = 12;
+constexpr int kHotMaxConsumers = 2;
+constexpr int kHotMaxProducers = kHotWaves - 1;  // with one consumer
 constexpr int kHotEntriesPerLane = 10;  // producer lanes x this >= batch entries (64 x 10 = 640)
-constexpr int kHotFlagBytes = 128;      // LDS handover words: ready[producer], freed[producer], abort
-constexpr int kHotScratchBytes = 64 * 8;  // write targets of the consumer's inactive lanes (8 bytes each)
+constexpr int kHotFlagBytes = 128;      // LDS words: ready[producer], freed[producer], abort, moved count
+constexpr int kHotScratchBytes = kHotMaxConsumers * 64 * 8;  // write targets of inactive consumer lanes
 constexpr int kHotZeroCells = 64;         // hot-array cells after the hot set, one per consumer lane
-constexpr int kHotMaxWindow = 8;         // consumer wave: W groups of 8 lanes
+constexpr int kHotMaxGroups = 8;          // coordinates per consumer step (groups of 8 lanes)
+constexpr int kHotMaxWindow = kHotMaxConsumers * kHotMaxGroups;
 constexpr int kHotMaxSegment = 64;
 constexpr uint16_t kHotCold = 0xFFFF;    // slot_of value of an entry that is not hot
 
@@ -125,16 +130,64 @@ struct HotArgs {
                                  // index when that entry is hot, else the index itself
     const int32_t* hot_ids;   // [n_hot]: shared-vector index of each slot
     uint32_t n_hot;
-    uint32_t W;               // coordinates in flight (<= kHotMaxWindow)
-    uint32_t B;               // coordinates per batch (multiple of W)
+    uint32_t W;               // coordinates in flight (2..kHotMaxWindow) unless `adapt_in` sets them
+    uint32_t NC;              // consumer waves (1, or 2 when W may exceed kHotMaxGroups)
+    uint32_t cap;             // coordinates a batch buffer holds; a consumer with w groups takes
+                              // batches of cap / w * w coordinates
     uint32_t Smax;            // entries per coordinate reserved in a batch buffer (multiple of 8)
     uint32_t hot_bytes;       // LDS bytes of the hot array and its zero cells (16-byte aligned)
     uint32_t spin_limit;      // bounded waits: after this many sleeps a wave gives up and sets *err
+    uint32_t w_rule;          // adaptive window: coordinates in flight the coupling rule allows
+                              // when every coordinate moves
+    const uint32_t* adapt_in;  // adaptive window (null: W): coordinates in flight for this epoch,
+                               // written by the previous epoch
+    uint32_t* adapt_out;       // adaptive window (null: none): receives the next epoch's window, set
+                               // from the coordinates whose step was nonzero in this one
     int* err;
 };
 
+// Coordinates per batch and consumer steps of a hot-set epoch with W coordinates in flight: consumer
+// c runs w_c coordinates per step (w0 = ceil(W / NC), w1 = the rest), on every NC-th batch (batch b
+// goes to consumer b mod NC), batches of B_c = cap / w_c * w_c coordinates.  Scalar fields only: the
+// kernels select between them, which keeps the struct in registers.
+struct HotSched {
+    uint32_t NC, NP;  // consumer and producer waves
+    uint32_t w0, w1, B0, B1;
+    uint32_t nb;      // batches in the epoch
+};
+
+__host__ __device__ inline HotSched hot_sched(uint32_t W, uint32_t NC, uint32_t cap, uint32_t n) {
+    HotSched s{};
+    s.NC = NC;
+    s.NP = (uint32_t)kHotWaves - NC;
+    s.w0 = (W + NC - 1) / NC;
+    s.w1 = NC > 1 ? W - s.w0 : s.w0;
+    s.B0 = cap / s.w0 * s.w0;
+    s.B1 = cap / s.w1 * s.w1;
+    if (NC == 1) {
+        s.nb = (n + s.B0 - 1) / s.B0;
+    } else {
+        const uint32_t pair = s.B0 + s.B1, q = n / pair, rem = n - q * pair;
+        s.nb = 2 * q + (rem == 0 ? 0 : rem > s.B0 ? 2 : 1);
+    }
+    return s;
+}
+
+__host__ __device__ inline uint32_t hot_consumer_of(const HotSched& s, uint32_t b) { return s.NC == 1 ? 0u : (b & 1u); }
+__host__ __device__ inline uint32_t hot_groups(const HotSched& s, uint32_t c) { return c ? s.w1 : s.w0; }
+__host__ __device__ inline uint32_t hot_batch(const HotSched& s, uint32_t c) { return c ? s.B1 : s.B0; }
+
+// First permutation position of batch b, and its size.
+__host__ __device__ inline uint32_t hot_batch_start(const HotSched& s, uint32_t b) {
+    if (s.NC == 1) return b * s.B0;
+    return (b >> 1) * (s.B0 + s.B1) + ((b & 1u) ? s.B0 : 0u);
+}
+__host__ __device__ inline uint32_t hot_batch_size(const HotSched& s, uint32_t b) {
+    return hot_batch(s, hot_consumer_of(s, b));
+}
+
 size_t hot_lds_bytes(uint32_t hot_bytes, uint32_t B, uint32_t Smax);
-hipError_t hot_prepare(int form, bool wide, size_t lds_bytes);
+hipError_t hot_prepare(int form, bool wide, uint32_t Smax, size_t lds_bytes);
 hipError_t launch_epoch_hot(int form, bool wide, const HotArgs& h, size_t lds_bytes, hipStream_t s);
 hipError_t launch_hot_count_ge(const unsigned* hits, int64_t L, unsigned T, unsigned long long* out2, hipStream_t s);
 hipError_t launch_hot_block_count(const unsigned* hits, int64_t L, unsigned T, unsigned* block_counts, hipStream_t s);
@@ -172,7 +225,8 @@ struct TeamArgs {
     int* err;
 };
 
-hipError_t launch_epoch_team(int form, bool wide, bool fresh, const TeamArgs& t, int blocks, hipStream_t s);
+// `cus`: compute units of the device; the launch is refused unless the whole grid is resident at once.
+hipError_t launch_epoch_team(int form, bool wide, bool fresh, const TeamArgs& t, int blocks, int cus, hipStream_t s);
 // Groups each segment's entries by index range: bound[0] = 0 < bound[1] <= ... <= bound[K] = L.
 hipError_t launch_team_partition(const int64_t* ptr, const int32_t* idx, const float* val, uint32_t C,
                                  const uint32_t* bound, int K, int32_t* out_idx, float* out_val, uint32_t* off,
@@ -200,7 +254,45 @@ hipError_t launch_probe(const int64_t* ptr, const int32_t* idx, const float* val
                         float* T, float* K, double* partials, double* out, hipStream_t s);
 hipError_t launch_kappa_max(const float* K, const float* norms, uint32_t C, int probes, int blocks, unsigned* out,
                             hipStream_t s);
+// One objective evaluation: k_objective (partials[blocks][5]) and k_sum_partials (sums[0..4]).  With
+// o.cyd null the ridge primal gathers y beside the shared vector.
 hipError_t launch_objective(int form, const ObjArgs& o, int G, int blocks, double* partials, double* sums,
                             hipStream_t s);
+hipError_t launch_fill_zero(uint64_t* p, uint32_t n_words, hipStream_t s);
+// Sets the calling thread's message returned by scd_last_error.
+void set_last_error(const char* msg);
+
+// Workgroups of the objective's pass, and its lanes per coordinate for segments of `mean` entries on
+// average (the epoch kernels' group width, at most one wave).
+constexpr int kObjBlocksMax = 2048;
+inline int objective_group(double mean) {
+    const int widths[5] = {4, 8, 16, 32, 64};
+    for (int G : widths)
+        if (mean <= (double)(G * slice_depth(G))) return G;
+    return 64;
+}
+inline int objective_blocks(int64_t C, int G) {
+    int64_t b = (C * G + 255) / 256;
+    if (b > kObjBlocksMax) b = kObjBlocksMax;
+    if (b < 1) b = 1;
+    return (int)b;
+}
+
+// Primal and dual objectives from the five sums of one evaluation (fp64 on the host):
+//   ridge primal: t0 = sum_m <a_m, r>^2, t1 = |beta|^2, t3 = |r|^2, t4 = <r, y>   (r = y - A beta)
+//   SVM dual:     t0 = sum hinge, t1 = sum alpha, t3 = |w|^2
+//   ridge dual:   t0 = |A wbar / lambda - y|^2, t1 = |alpha|^2, t2 = <alpha, y>, t3 = |wbar|^2
+inline void objectives_from_sums(int form, double N, double lam, const double* t, double* P, double* D) {
+    if (form == FORM_RIDGE_PRIMAL) {
+        *P = t[3] / (2.0 * N) + 0.5 * lam * t[1];
+        *D = -t[3] / (2.0 * N) - t[0] / (2.0 * lam * N * N) + t[4] / N;
+    } else if (form == FORM_SVM_DUAL) {
+        *P = t[0] / N + 0.5 * lam * t[3];
+        *D = t[1] / N - 0.5 * lam * t[3];
+    } else {
+        *P = t[0] / (2.0 * N) + 0.5 * t[3] / lam;
+        *D = -0.5 * N * t[1] - t[3] / (2.0 * lam) + t[2];
+    }
+}
 
 }  // namespace scd

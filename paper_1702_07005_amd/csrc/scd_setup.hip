@@ -121,7 +121,9 @@ __device__ __forceinline__ void block_reduce_store(double (&v)[NS], double* out)
 
 constexpr int kObjSlices = 8;  // entries per lane per block of the objective's gather-dot
 
-template <int FORM, int G, typename U>
+// DIRECT (ridge primal only): <a_c, y - w> is gathered from y and w in fp64 instead of taken as
+// <y, a_c> (o.cyd, computed at set-up) minus <a_c, w>; for callers that hold no set-up data.
+template <int FORM, int G, typename U, bool DIRECT>
 __global__ __launch_bounds__(256) void k_objective(ObjArgs o, double* __restrict__ partials) {
     constexpr int NS = 5;
     const U* __restrict__ u = static_cast<const U*>(o.u);
@@ -149,14 +151,22 @@ __global__ __launch_bounds__(256) void k_objective(ObjArgs o, double* __restrict
             U g[kObjSlices];
 #pragma unroll
             for (int r = 0; r < kObjSlices; ++r) g[r] = u[ix[r]];
+            if constexpr (DIRECT) {
+                float yy[kObjSlices];
 #pragma unroll
-            for (int r = 0; r < kObjSlices; ++r) d += (double)vx[r] * (double)g[r];
+                for (int r = 0; r < kObjSlices; ++r) yy[r] = o.yv[ix[r]];
+#pragma unroll
+                for (int r = 0; r < kObjSlices; ++r) d += (double)vx[r] * ((double)yy[r] - (double)g[r]);
+            } else {
+#pragma unroll
+                for (int r = 0; r < kObjSlices; ++r) d += (double)vx[r] * (double)g[r];
+            }
         }
         d = group_sum_f64<G>(d);
         if (lane == 0) {
             const double mo = o.model[c];
             if constexpr (FORM == FORM_RIDGE_PRIMAL) {
-                const double r = o.cyd[c] - d;
+                const double r = DIRECT ? d : o.cyd[c] - d;
                 t[0] += r * r;
                 t[1] += mo * mo;
             } else if constexpr (FORM == FORM_SVM_DUAL) {
@@ -366,12 +376,12 @@ hipError_t launch_validate(const int64_t* ptr, uint32_t S, const int32_t* idx, c
     return hipGetLastError();
 }
 
-template <int FORM, typename U>
+template <int FORM, typename U, bool DIRECT>
 static void objective_typed(const ObjArgs& o, int G, int blocks, double* partials, hipStream_t s) {
     switch (G) {
 #define SCD_OBJ(GW)                                                                                         \
     case GW:                                                                                                \
-        hipLaunchKernelGGL((k_objective<FORM, GW, U>), dim3(blocks), dim3(256), 0, s, o, partials);         \
+        hipLaunchKernelGGL((k_objective<FORM, GW, U, DIRECT>), dim3(blocks), dim3(256), 0, s, o, partials); \
         break;
         SCD_OBJ(4)
         SCD_OBJ(8)
@@ -384,10 +394,31 @@ static void objective_typed(const ObjArgs& o, int G, int blocks, double* partial
 
 template <int FORM>
 static void objective_form(const ObjArgs& o, int G, int blocks, double* partials, hipStream_t s) {
+    // The ridge primal without <y, a_c> from set-up gathers y beside w.
+    if constexpr (FORM == FORM_RIDGE_PRIMAL) {
+        if (!o.cyd) {
+            if (o.wide)
+                objective_typed<FORM, double, true>(o, G, blocks, partials, s);
+            else
+                objective_typed<FORM, float, true>(o, G, blocks, partials, s);
+            return;
+        }
+    }
     if (o.wide)
-        objective_typed<FORM, double>(o, G, blocks, partials, s);
+        objective_typed<FORM, double, false>(o, G, blocks, partials, s);
     else
-        objective_typed<FORM, float>(o, G, blocks, partials, s);
+        objective_typed<FORM, float, false>(o, G, blocks, partials, s);
+}
+
+__global__ __launch_bounds__(256) void k_fill_zero(uint64_t* __restrict__ p, uint32_t n) {
+    for (uint32_t i = blockIdx.x * 256u + threadIdx.x; i < n; i += gridDim.x * 256u) p[i] = 0ull;
+}
+
+hipError_t launch_fill_zero(uint64_t* p, uint32_t n_words, hipStream_t s) {
+    if (n_words == 0) return hipSuccess;
+    hipLaunchKernelGGL(k_fill_zero, dim3((n_words + 255) / 256 > 64 ? 64 : (n_words + 255) / 256), dim3(256), 0, s, p,
+                       n_words);
+    return hipGetLastError();
 }
 
 // sums[0..2] = coordinate sums, sums[3..4] = vector sums.

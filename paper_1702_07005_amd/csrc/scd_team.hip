@@ -14,7 +14,8 @@
 //      in the same order, so all compute the same inner product and the same step (eq.
 //      update_primal, the SVM dual step, or eq. update_dual);
 //   4. scatter: member k adds coef * a_m into its own index range, then waits for those atomics
-//      before it gathers the team's next coordinate.
+//      before it gathers the team's next coordinate (each wave waits for its own, and a barrier
+//      joins the four waves, so the wait covers every atomic of the member).
 //
 // Because a member's gathers and atomics touch only its own index range, its own wait in step 4
 // is enough: when any member gathers coordinate c + 1, every update of coordinate c to the entries
@@ -28,8 +29,8 @@
 // read all partials of step g: no member still waits on the value being overwritten.  Each slot is
 // one location written and read with 64-bit device-scope atomics, so no ordering between
 // locations is needed.  Every wait is bounded (spin_limit sleeps); a member that gives up sets
-// *err and leaves, and the others give up in turn.  The grid is launched cooperatively, so every
-// member is resident while the others wait for it.
+// *err and leaves, and the others give up in turn.  The grid fits the CUs (one workgroup per CU at
+// most), so every member is resident while the others wait for it.
 #include <algorithm>
 
 #include "scd_device.h"
@@ -96,8 +97,10 @@ __device__ __forceinline__ bool team_step(const TeamArgs& t, const SharedBuf<U>&
                                           int (&ni)[R], float (&nv)[R], TeamMeta& nn, float (*part)[4],
                                           float* gsum, int* gok) {
     const EpochArgs& a = t.e;
-    // This member's atomics of the previous coordinate land before it gathers again.
+    // This member's atomics of the previous coordinate land before it gathers again: each wave
+    // waits for its own, and the barrier holds all four waves until every one has.
     __builtin_amdgcn_s_waitcnt(0x0F70);  // vmcnt(0)
+    __builtin_amdgcn_s_barrier();
     const CoordMeta cur = team_part(tcur), nxt = team_part(tnxt);
     const int64_t len = cur.s1 - cur.s0;
     const uint64_t P = a.n_groups, n = a.perm.n;
@@ -295,28 +298,42 @@ __global__ __launch_bounds__(256) void k_team_partition(const int64_t* __restric
     }
 }
 
+// An ordinary launch.  The members wait for one another, so the whole grid must be resident at
+// once: the plan keeps it within the CUs (one 256-thread workgroup per CU at most), and the launch
+// is refused unless the occupancy query confirms that every CU holds at least one workgroup of
+// this kernel.  Work enqueued earlier on the same stream has finished when the grid starts; a
+// kernel of another stream or process that holds CUs can delay members, and the bounded waits then
+// report an error instead of hanging.  (A cooperative launch would give the same guarantee, but
+// it runs on a separate device queue of the runtime; the only processes whose profiler runs ended
+// in a fault inside the exit handlers, after the profiler's own finalisation, were those that had
+// made such launches.)
 template <int FORM, bool FRESH, typename U>
-hipError_t launch_team_typed(const TeamArgs& t, int blocks, hipStream_t s) {
-    TeamArgs arg = t;
-    void* args[] = {&arg};
-    return hipLaunchCooperativeKernel(reinterpret_cast<const void*>(&k_epoch_team<FORM, kTeamSlices, FRESH, U>),
-                                      dim3(blocks), dim3(256), args, 0, s);
+hipError_t launch_team_typed(const TeamArgs& t, int blocks, int cus, hipStream_t s) {
+    const void* f = reinterpret_cast<const void*>(&k_epoch_team<FORM, kTeamSlices, FRESH, U>);
+    int per_cu = 0;
+    const hipError_t e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, f, 256, 0);
+    if (e != hipSuccess) return e;
+    if (per_cu < 1 || blocks > per_cu * cus) return hipErrorCooperativeLaunchTooLarge;
+    hipLaunchKernelGGL((k_epoch_team<FORM, kTeamSlices, FRESH, U>), dim3(blocks), dim3(256), 0, s, t);
+    return hipGetLastError();
 }
 
 template <int FORM>
-hipError_t launch_team_form(bool wide, bool fresh, const TeamArgs& t, int blocks, hipStream_t s) {
+hipError_t launch_team_form(bool wide, bool fresh, const TeamArgs& t, int blocks, int cus, hipStream_t s) {
     if (wide)
-        return fresh ? launch_team_typed<FORM, true, double>(t, blocks, s) : launch_team_typed<FORM, false, double>(t, blocks, s);
-    return fresh ? launch_team_typed<FORM, true, float>(t, blocks, s) : launch_team_typed<FORM, false, float>(t, blocks, s);
+        return fresh ? launch_team_typed<FORM, true, double>(t, blocks, cus, s)
+                     : launch_team_typed<FORM, false, double>(t, blocks, cus, s);
+    return fresh ? launch_team_typed<FORM, true, float>(t, blocks, cus, s)
+                 : launch_team_typed<FORM, false, float>(t, blocks, cus, s);
 }
 
 }  // namespace
 
-hipError_t launch_epoch_team(int form, bool wide, bool fresh, const TeamArgs& t, int blocks, hipStream_t s) {
+hipError_t launch_epoch_team(int form, bool wide, bool fresh, const TeamArgs& t, int blocks, int cus, hipStream_t s) {
     switch (form) {
-        case FORM_RIDGE_PRIMAL: return launch_team_form<FORM_RIDGE_PRIMAL>(wide, fresh, t, blocks, s);
-        case FORM_SVM_DUAL: return launch_team_form<FORM_SVM_DUAL>(wide, fresh, t, blocks, s);
-        case FORM_RIDGE_DUAL: return launch_team_form<FORM_RIDGE_DUAL>(wide, fresh, t, blocks, s);
+        case FORM_RIDGE_PRIMAL: return launch_team_form<FORM_RIDGE_PRIMAL>(wide, fresh, t, blocks, cus, s);
+        case FORM_SVM_DUAL: return launch_team_form<FORM_SVM_DUAL>(wide, fresh, t, blocks, cus, s);
+        case FORM_RIDGE_DUAL: return launch_team_form<FORM_RIDGE_DUAL>(wide, fresh, t, blocks, cus, s);
         default: return hipErrorInvalidValue;
     }
 }

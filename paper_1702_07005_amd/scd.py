@@ -45,7 +45,8 @@ class _Info(ctypes.Structure):
                 ("max_segment", ctypes.c_int64), ("window", ctypes.c_int64), ("lambda_", ctypes.c_double),
                 ("coupling", ctypes.c_double), ("coherence", ctypes.c_double), ("auto_window", ctypes.c_int64),
                 ("long_len", ctypes.c_int64), ("shared_fp64", ctypes.c_int32), ("max_hits", ctypes.c_uint32),
-                ("kernel", ctypes.c_int32), ("hot_entries", ctypes.c_int32)]
+                ("kernel", ctypes.c_int32), ("hot_entries", ctypes.c_int32),
+                ("adaptive_window", ctypes.c_int32), ("reserved", ctypes.c_int32)]
 
 
 # Every symbol of include/scd.h with its ctypes signature.
@@ -201,7 +202,8 @@ class Solver:
                     shared_len=i.shared_len, nnz=i.nnz, epoch=i.epoch, max_segment=i.max_segment,
                     window=i.window, lam=i.lambda_, coupling=i.coupling, coherence=i.coherence,
                     auto_window=i.auto_window, long_len=i.long_len, shared_fp64=i.shared_fp64,
-                    max_hits=i.max_hits, kernel=KERNELS[i.kernel], hot_entries=i.hot_entries)
+                    max_hits=i.max_hits, kernel=KERNELS[i.kernel], hot_entries=i.hot_entries,
+                    adaptive_window=i.adaptive_window)
 
     def gather_dots(self, u: torch.Tensor, stream=None) -> torch.Tensor:
         out = torch.empty(self.C, dtype=torch.float32, device=self.device)

@@ -121,3 +121,4 @@ def test_null_handle_calls(lib):
     assert lib.scd_permutation(0, 0, 0, FAKE, None) == -1
     assert lib.scd_permutation(0, -1, 10, FAKE, None) == -1
     assert lib.scd_permutation(0, 0, 10, None, None) == -1
+

@@ -5,10 +5,11 @@ The oracle cannot run these to convergence in a test, so the checks are the ones
 size, that it can compute one by one, or that it computed once:
   * gathered dots of 2,000 sampled coordinates on a frozen vector (oracle on those segments only),
     |gpu - fp64| <= 1e-4 * sum |a_i u_i|;
-  * after one epoch, |w - A model|_inf / |w|_inf <= 1e-4 with A model recomputed in fp64 (scipy);
+  * after each of the first 5 epochs, |w - A model|_inf / |w|_inf <= 1e-4 with A model recomputed
+    in fp64 (scipy);
   * SVM box constraints after every epoch;
-  * the duality gap after every epoch within 2x of the oracle's at the same epoch (while the
-    oracle's is above 1e-6 P(0)), against tests/golden/fullsize_gap_curves.json, which
+  * the duality gap after every epoch within 2x of the oracle's at the same epoch, plus the fp32
+    floor 1e-6 P(0), against tests/golden/fullsize_gap_curves.json, which
     tests/golden/make_fullsize_curves.py writes from the oracle on the same seeded inputs.
 """
 import gc
@@ -74,20 +75,20 @@ def test_full_size(name):
     for e, Gr in enumerate(ref["gap"]):
         s.epochs(ref["seed"], 1)
         G = s.duality_gap()
-        print(f"  epoch {e + 1}: gap {G:.3e}, oracle {Gr:.3e}", flush=True)
-        if Gr > 1e-6 * abs(P0):
-            assert G <= 2.0 * Gr, (e + 1, G, Gr)
-        if e == 0 or p.form == "svm_dual":
+        print(f"  epoch {e + 1}: gap {G:.3e}, oracle {Gr:.3e}, ratio {G / Gr:.3f}", flush=True)
+        assert G <= 2.0 * Gr + 1e-6 * abs(P0), (e + 1, G, Gr)
+        if e < 5 or p.form == "svm_dual":
             gm, gs, ep = s.get_state()
             assert ep == e + 1
             model = gm.cpu().numpy().astype(np.float64)
             if p.form == "svm_dual":
                 assert model.min() >= 0.0 and model.max() <= 1.0
-            if e == 0:
-                print("  checking the invariant", flush=True)
+            if e < 5:
                 shared = gs.cpu().numpy().astype(np.float64)
                 fresh = _fresh_shared(p, model)
-                assert np.max(np.abs(shared - fresh)) <= 1e-4 * np.max(np.abs(fresh))
+                err = np.max(np.abs(shared - fresh)) / np.max(np.abs(fresh))
+                print(f"  invariant after epoch {e + 1}: {err:.2e}", flush=True)
+                assert err <= 1e-4, (e + 1, err)
                 del shared, fresh
             del gm, gs, model
     s.close()
