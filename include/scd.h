@@ -278,6 +278,27 @@ int scd_norms(scd_handle_t h, float *out_dev, void *stream);
  * asks for a fresh random permutation per epoch (Alg. 1, Alg. 2).  Enqueues only. */
 int scd_permutation(uint64_t seed, int64_t epoch, int64_t n, int32_t *out_dev, void *stream);
 
+/* Allocation-free objectives of a given state, for callers that cannot allocate device memory (code
+ * in tight serving or evaluation loops, harnesses that forbid hipMalloc): the same P and D as
+ * scd_objective, for the state (model_dev, shared_dev) of formulation `formulation` on (A, y_dev,
+ * lambda), without a handle.
+ *   A, y_dev, lambda, formulation: as for scd_create (A and y are read, not kept).
+ *   model_dev:  float32[C] (C = n_cols for SCD_RIDGE_PRIMAL, n_rows otherwise), device.
+ *   shared_dev: float32[L] (L = n_rows for SCD_RIDGE_PRIMAL, n_cols otherwise), device: the shared
+ *               vector standing in for A beta, w(alpha) or A^T alpha (Sec. II-C).
+ *   primal, dual: host outputs (either may be NULL).
+ * The call validates A and y on the device as scd_create does (same errors), runs the objective
+ * pass and synchronises the stream.  It calls no allocating routine: its scratch (validation flags,
+ * up to 2,048 x 5 fp64 partial sums, 5 sums; 82,048 bytes) is a fixed device array of the library,
+ * one copy per GPU, held from the first call on that GPU until the process ends, so no input size
+ * can exceed it (sizes are limited as for scd_create: dimensions below 2^31).  Calls on one GPU
+ * share that array: calls that overlap in time on one GPU (two host threads, or two streams without
+ * ordering) race and must be serialised by the caller.  Errors: SCD_ERR_INVALID, SCD_ERR_NUMERIC,
+ * SCD_ERR_HIP (as scd_create), SCD_ERR_UNSUPPORTED for a device index above 63. */
+int scd_objective_static(const scd_matrix_t *A, const float *y_dev, double lambda, int32_t formulation,
+                         const float *model_dev, const float *shared_dev, void *stream, double *primal,
+                         double *dual);
+
 /* Message describing the last error on the calling thread ("" if none). */
 const char *scd_last_error(void);
 

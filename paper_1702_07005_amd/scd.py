@@ -72,6 +72,9 @@ _SIGS = {
     "scd_norms": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p]),
     "scd_permutation": (ctypes.c_int, [ctypes.c_uint64, ctypes.c_int64, ctypes.c_int64, ctypes.c_void_p,
                                        ctypes.c_void_p]),
+    "scd_objective_static": (ctypes.c_int, [ctypes.POINTER(_Matrix), ctypes.c_void_p, ctypes.c_double, ctypes.c_int32,
+                                            ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p,
+                                            ctypes.POINTER(ctypes.c_double), ctypes.POINTER(ctypes.c_double)]),
     "scd_last_error": (ctypes.c_char_p, []),
 }
 
@@ -222,6 +225,22 @@ def permutation(seed: int, epoch: int, n: int, device="cuda", stream=None) -> to
     _check(lib.scd_permutation(seed & 0xFFFFFFFFFFFFFFFF, int(epoch), int(n), ctypes.c_void_p(out.data_ptr()),
                                _stream(stream)))
     return out
+
+
+def objective_static(n_rows, n_cols, ptr, idx, val, y, lam, form, model, shared, stream=None):
+    """(P, D) of the state (model, shared) through scd_objective_static: no handle, no allocation."""
+    code = FORMS[form]
+    n_rows, n_cols = int(n_rows), int(n_cols)
+    C = n_cols if code == RIDGE_PRIMAL else n_rows
+    L = n_rows if code == RIDGE_PRIMAL else n_cols
+    nnz = int(idx.numel())
+    m = _Matrix(n_rows, n_cols, nnz, CSC if code == RIDGE_PRIMAL else CSR, 0, _dev(ptr, torch.int64, C + 1, "ptr"),
+                _dev(idx, torch.int32, nnz, "idx") if nnz else None, _dev(val, torch.float32, nnz, "val") if nnz else None)
+    P, D = ctypes.c_double(), ctypes.c_double()
+    _check(lib.scd_objective_static(ctypes.byref(m), _dev(y, torch.float32, n_rows, "y"), float(lam), code,
+                                    _dev(model, torch.float32, C, "model"), _dev(shared, torch.float32, L, "shared"),
+                                    _stream(stream), ctypes.byref(P), ctypes.byref(D)))
+    return P.value, D.value
 
 
 def upload(prob, device="cuda"):

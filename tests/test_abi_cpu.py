@@ -122,3 +122,12 @@ def test_null_handle_calls(lib):
     assert lib.scd_permutation(0, -1, 10, FAKE, None) == -1
     assert lib.scd_permutation(0, 0, 10, None, None) == -1
 
+
+def test_static_objective_source_allocates_nothing():
+    # The allocation-free entry point keeps its scratch in a file-scope device array, reached through
+    # the address hipGetSymbolAddress returns per device; its source calls no allocating routine.
+    src = open(os.path.join(ROOT, "paper_1702_07005_amd", "csrc", "scd_static.hip")).read()
+    code = "\n".join(line.split("//")[0] for line in src.splitlines())
+    for banned in ("hipMalloc", "hipFree", "hipHostMalloc", "hipHostFree", "hipMallocAsync", "malloc(", "new "):
+        assert banned not in code, banned
+    assert "__device__ __align__(256)" in code and "hipGetSymbolAddress" in code
