@@ -121,7 +121,8 @@ typedef struct {
                              per coordinate taking positions from a queue (skewed
                              segment lengths), 7 a team of workgroups per coordinate,
                              each on its own range of shared-vector indices (long
-                             segments, few coordinates in flight)                      */
+                             segments, few coordinates in flight), 8 hot set in LDS with
+                             stager workgroups assembling the batches (option "staged") */
     int32_t hot_entries;  /* shared-vector entries the hot-set kernel keeps in LDS
                              (0 until it is first needed)                               */
     int32_t adaptive_window; /* 1 if the epoch kernel sets each epoch's window from the
@@ -237,6 +238,14 @@ int scd_set_state(scd_handle_t h, const float *model_dev, const float *shared_de
  *                 0 = never; 2..16 = K members whenever the window binds and (coordinates in
  *                 flight) x K is at most the number of CUs.  With the automatic window, teams take
  *                 7/8 of the window's share that the other draining kernels take.
+ *   "staged"      1 (default) = when the hot-set kernel runs the epoch and the matrix's entries take more
+ *                 than 256 MB (beyond the GPU's Infinity Cache), the batches it runs are assembled by
+ *                 stager workgroups on the hot-set workgroup's XCD (coordinate metadata, entry keys and
+ *                 values) and passed through a ring of 64 records in device memory, so that the one
+ *                 workgroup only loads records, gathers the cold entries and runs the steps; 2 =
+ *                 whenever the hot-set kernel runs; 0 = never.  The stagers need the GPU's CUs beside
+ *                 the hot-set workgroup: a kernel of another stream that holds them delays the epoch,
+ *                 and its bounded waits then report SCD_ERR_HIP.
  *   "adapt"       1 (default) = when the window is automatic and the hot-set kernel runs the epoch,
  *                 each epoch's window follows the fraction f of coordinates whose step was nonzero
  *                 in the previous epoch: W = 1 + (auto_window - 1) / f, at most 16.  A coordinate

@@ -93,6 +93,9 @@ constexpr double kTeamMinMean = 1024.0;
 // permutation (the queued kernel's case).
 constexpr double kTeamMaxSkew = 4.0;  // longest segment at most this many times the mean
 constexpr int64_t kTeamMinSharedBytes = int64_t(4) << 20;
+// Staged hot-set epochs, automatic choice: matrices whose entries (8 bytes each) exceed the
+// 256 MB Infinity Cache, so that the producers' loads go to HBM, and a GPU with CUs for the stagers.
+constexpr int64_t kStagedMinBytes = int64_t(256) << 20;
 
 }  // namespace
 
@@ -151,6 +154,14 @@ struct scd_solver {
     int64_t adapt = 1;            // option: automatic window of the hot-set kernel follows the moving fraction
     uint32_t* hot_adapt = nullptr;  // [2]: the hot-set kernel's window for the next epoch (device)
     int adapt_fresh = 1;          // the next hot-set epoch starts from the rule's window (state or options changed)
+    // Staged hot-set epochs (stager workgroups assemble the batches): ring and flags, allocated with the
+    // hot-set tables.
+    int64_t staged = 1;           // option: 0 never, 1 automatic (large matrices), 2 whenever the hot set runs
+    uint32_t* ring = nullptr;     // [kHotRing][staged_rec_words(cap, Smax)]
+    uint32_t* ring_flags = nullptr;  // [kHotFlagWords]
+    uint64_t* ring_results = nullptr;  // [kHotResultWords]
+    uint32_t* ring_prog = nullptr;   // [4]
+    uint32_t ring_tag = 1;        // tag of the next staged launch (never 0)
     int64_t hot_wait_limit = 0;   // option (test hook): sleeps per wait before giving up, 0 = kHotSpinLimit
     int* err_host = nullptr;      // pinned copies of hot_err: one per gap slot + one for reduce_state
     // Team kernel (long segments, few coordinates in flight): tables built on first need for K.
@@ -228,6 +239,13 @@ int pipe_drain(const scd_solver* h, int64_t window, int64_t groups) {
 int64_t pipe_groups(const scd_solver* h, int64_t window, int64_t groups) {
     if (h->window != 0 || !pipe_drain(h, window, groups)) return groups;
     return std::max<int64_t>(1, groups * 4 / 5);
+}
+
+// The staged variant: option 2, or option 1 with a matrix beyond the Infinity Cache; it needs its ring and
+// enough CUs for the stagers (all on the XCD of the hot-set workgroup).
+bool staged_plan(const scd_solver* h) {
+    if (h->staged == 0 || !h->ring || h->cus < 1 + kHotXcds * kHotStagers) return false;
+    return h->staged == 2 || h->nnz * 8 > kStagedMinBytes;
 }
 
 bool hot_plan(const scd_solver* h, int64_t window, HotGeom* g) {
@@ -318,7 +336,7 @@ int plan_epoch(const scd_solver* h, LaunchPlan* lp, uint32_t* n_groups) {
     }
     HotGeom hg;
     if (hot_plan(h, window, &hg)) {
-        lp->kind = PLAN_HOT;
+        lp->kind = staged_plan(h) ? PLAN_HOT_STAGED : PLAN_HOT;
         lp->group = 8;
         lp->blocks = 1;
         lp->lds_bytes = hg.lds;
@@ -482,6 +500,26 @@ int build_hot_tables(scd_solver* h, hipStream_t s) {
         if (rc == SCD_OK && !skip) {
             h->n_hot = (uint32_t)cnt;
             h->hot_cover = (double)sum / (double)h->nnz;
+            // The staged variant's ring (a few hundred KB); without it only the single-workgroup kernel runs.
+            const uint32_t Smax = (uint32_t)std::max<int64_t>(8, (h->max_seg + 7) / 8 * 8);
+            const uint32_t cap = std::min<uint32_t>(64, 64u * kHotEntriesPerLane / Smax);
+            const size_t ring_bytes = sizeof(uint32_t) * (size_t)kHotRing * staged_rec_words(cap, Smax);
+            if (hipMalloc(&h->ring, ring_bytes) != hipSuccess ||
+                hipMalloc(&h->ring_flags, sizeof(uint32_t) * kHotFlagWords) != hipSuccess ||
+                hipMalloc(&h->ring_results, sizeof(uint64_t) * kHotResultWords) != hipSuccess ||
+                hipMalloc(&h->ring_prog, 4 * sizeof(uint32_t)) != hipSuccess) {
+                (void)hipGetLastError();
+                (void)hipFree(h->ring);
+                (void)hipFree(h->ring_flags);
+                (void)hipFree(h->ring_results);
+                (void)hipFree(h->ring_prog);
+                h->ring = nullptr;
+                h->ring_flags = nullptr;
+                h->ring_results = nullptr;
+                h->ring_prog = nullptr;
+            } else {
+                hip(hipMemsetAsync(h->ring_prog, 0, 4 * sizeof(uint32_t), s), "zero ring_prog");
+            }
         }
     }
     (void)hipFree(hits);
@@ -637,6 +675,10 @@ void release(scd_solver* h) {
     (void)hipFree(h->us);
     (void)hipFree(h->queue);
     (void)hipFree(h->hot_adapt);
+    (void)hipFree(h->ring);
+    (void)hipFree(h->ring_flags);
+    (void)hipFree(h->ring_results);
+    (void)hipFree(h->ring_prog);
     (void)hipFree(h->entry_key);
     (void)hipFree(h->hot_ids);
     (void)hipFree(h->hot_err);
@@ -895,9 +937,12 @@ int scd_epochs(scd_handle_t h, uint64_t seed, int32_t n_epochs, void* stream) {
     if (int r = plan_epoch(h, &lp, &n_groups)) return r;
     if (lp.kind == PLAN_ORDERED_LDS) HIP_TRY(ordered_lds_prepare(h->form, lp.wide != 0, lp.lds_bytes));
     HotGeom hg{};
-    if (lp.kind == PLAN_HOT) {
+    if (lp.kind == PLAN_HOT || lp.kind == PLAN_HOT_STAGED) {
         hot_plan(h, h->window ? h->window : h->auto_window, &hg);
-        HIP_TRY(hot_prepare(h->form, h->wide != 0, hg.Smax, hg.lds));
+        if (lp.kind == PLAN_HOT)
+            HIP_TRY(hot_prepare(h->form, h->wide != 0, hg.Smax, hg.lds));
+        else
+            HIP_TRY(staged_prepare(h->form, h->wide != 0, hg.Smax, hg.lds));
     }
     EpochArgs a{};
     a.ptr = h->ptr;
@@ -950,7 +995,7 @@ int scd_epochs(scd_handle_t h, uint64_t seed, int32_t n_epochs, void* stream) {
             HIP_TRY(launch_epoch_team(h->form, h->wide != 0, lp.fresh != 0, ta, lp.blocks, h->cus, s));
             // Steps of the busiest team, plus one: the next launch's tags are all new.
             h->team_tag += (uint32_t)((h->C + n_groups - 1) / n_groups + 1);
-        } else if (lp.kind == PLAN_HOT) {
+        } else if (lp.kind == PLAN_HOT || lp.kind == PLAN_HOT_STAGED) {
             HotArgs ha{};
             ha.e = a;
             ha.entry_key = h->entry_key;
@@ -968,7 +1013,18 @@ int scd_epochs(scd_handle_t h, uint64_t seed, int32_t n_epochs, void* stream) {
             h->adapt_fresh = 0;
             ha.spin_limit = h->hot_wait_limit > 0 ? (uint32_t)h->hot_wait_limit : kHotSpinLimit;
             ha.err = h->hot_err;
-            HIP_TRY(launch_epoch_hot(h->form, h->wide != 0, ha, hg.lds, s));
+            if (lp.kind == PLAN_HOT_STAGED) {
+                ha.ring = h->ring;
+                ha.flags = h->ring_flags;
+                ha.results = h->ring_results;
+                ha.prog = h->ring_prog;
+                ha.tag = h->ring_tag;
+                ha.stagers = kHotStagers;
+                h->ring_tag = h->ring_tag == 0xFFFFFFFFu ? 1u : h->ring_tag + 1u;
+                HIP_TRY(launch_epoch_staged(h->form, h->wide != 0, ha, hg.lds, s));
+            } else {
+                HIP_TRY(launch_epoch_hot(h->form, h->wide != 0, ha, hg.lds, s));
+            }
         } else {
             HIP_TRY(launch_epoch(h->form, a, lp, s));
         }
@@ -1064,7 +1120,10 @@ int scd_set_option(scd_handle_t h, const char* key, int64_t value) {
     if (int r = check_handle(h)) return r;
     if (!key) return fail(SCD_ERR_INVALID, "key is null");
     h->adapt_fresh = 1;  // the next hot-set epoch starts again from the rule's window
-    if (!strcmp(key, "adapt")) {
+    if (!strcmp(key, "staged")) {
+        if (value < 0 || value > 2) return fail(SCD_ERR_INVALID, "staged must be 0, 1 or 2");
+        h->staged = value;
+    } else if (!strcmp(key, "adapt")) {
         if (value != 0 && value != 1) return fail(SCD_ERR_INVALID, "adapt must be 0 or 1");
         h->adapt = value;
         if (int r = set_device(h)) return r;
@@ -1158,6 +1217,7 @@ int scd_get_option(scd_handle_t h, const char* key, int64_t* value) {
     else if (!strcmp(key, "team")) *value = h->team;
     else if (!strcmp(key, "shared_fp64")) *value = h->wide;
     else if (!strcmp(key, "adapt")) *value = h->adapt;
+    else if (!strcmp(key, "staged")) *value = h->staged;
     else if (!strcmp(key, "next_window")) {
         // Coordinates in flight the next epoch will use (read-only; synchronises the device).
         LaunchPlan lp;
@@ -1165,7 +1225,7 @@ int scd_get_option(scd_handle_t h, const char* key, int64_t* value) {
         plan_epoch(h, &lp, &n_groups);
         HotGeom hg{};
         const int64_t window = h->window ? h->window : h->auto_window;
-        if (lp.kind == PLAN_HOT && hot_plan(h, window, &hg) && hg.adaptive) {
+        if ((lp.kind == PLAN_HOT || lp.kind == PLAN_HOT_STAGED) && hot_plan(h, window, &hg) && hg.adaptive) {
             uint32_t v = 0;
             if (!h->adapt_fresh) {
                 if (int r = set_device(h)) return r;
@@ -1191,7 +1251,7 @@ int scd_get_info(scd_handle_t h, scd_info_t* info) {
     plan_epoch(h, &lp, &n_groups);
     info->formulation = h->form;
     info->group_lanes = (lp.kind == PLAN_GROUP || lp.kind == PLAN_MIXED || lp.kind == PLAN_PIPE || lp.kind == PLAN_HOT ||
-                         lp.kind == PLAN_QUEUE)
+                         lp.kind == PLAN_HOT_STAGED || lp.kind == PLAN_QUEUE)
                             ? lp.group
                         : lp.kind == PLAN_TEAM                 ? kBlockThreads * lp.team
                         : lp.kind == PLAN_BLOCK && !lp.ordered ? kBlockThreads
@@ -1199,8 +1259,8 @@ int scd_get_info(scd_handle_t h, scd_info_t* info) {
     info->kernel = lp.kind;
     info->hot_entries = (int32_t)h->n_hot;
     HotGeom hg{};
-    info->adaptive_window = lp.kind == PLAN_HOT && hot_plan(h, h->window ? h->window : h->auto_window, &hg) &&
-                            hg.adaptive;
+    info->adaptive_window = (lp.kind == PLAN_HOT || lp.kind == PLAN_HOT_STAGED) &&
+                            hot_plan(h, h->window ? h->window : h->auto_window, &hg) && hg.adaptive;
     info->reserved = 0;
     info->long_len = lp.kind == PLAN_MIXED ? lp.long_len : 0;
     info->shared_fp64 = h->wide;

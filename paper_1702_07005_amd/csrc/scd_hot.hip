@@ -437,6 +437,367 @@ __global__ __launch_bounds__(64 * kHotWaves) void k_epoch_hot(HotArgs h) {
     }
 }
 
+// ----------------------------------------------------------------------------------------
+// Staged hot-set epoch (large matrices).  At full size the single workgroup's producer waves bound
+// the epoch: each batch costs a producer wave about 1,400 instructions (slot layout, metadata,
+// 64-bit entry addresses) and three dependent memory round trips, and one CU holds only twelve such
+// waves (their registers).  Here that work runs on other CUs of workgroup 0's XCD:
+//
+//   stager waves (workgroups kHotXcds, 2 kHotXcds, ...): claim the next batch from a counter, wait
+//     until its ring record is free, read the coordinates' metadata and entry keys and values,
+//     assemble the batch's LDS image in their own LDS (records, hot keys and values, zero-cell keys
+//     for cold slots) and copy it into the record, followed by the cold (index, value) pairs; then
+//     wait until those stores have completed and publish the record's tag (batch + 1).  Last they
+//     load the batch's cold shared-vector entries (values unused), so the loader finds them in L2.
+//   loader waves (workgroup 0, in place of the producers): once the consumer has finished the
+//     buffer's previous batch, publish its results (each coordinate's new model value and scatter
+//     coefficient) in a result ring; then wait for the record of the next batch, load it
+//     (device-scope loads, which read the XCD's L2), free the record, gather the cold values (as
+//     fresh as the producers' are), sum each coordinate's cold part and hand the buffer over.
+//   The stager of a batch waits for its results and writes the model values and the cold entries'
+//     updates out, so the hot-set workgroup never waits behind a device-scope atomic.
+//
+// Records travel through the L2 of one XCD: a stager's plain stores reach that L2 when its wait
+// for them ends, and the loader's device-scope loads miss its own L1.  So every stager checks that
+// it runs on workgroup 0's XCD (hardware XCC_ID) and leaves otherwise.  The flags are zeroed
+// before every launch; every wait is bounded.
+// ----------------------------------------------------------------------------------------
+__device__ __forceinline__ uint32_t hot_xcc_id() {
+    return (uint32_t)__builtin_amdgcn_s_getreg((3 << 11) | (0 << 6) | 20) & 15u;
+}
+
+// The ring, its flags and the result ring are shared by workgroups of one XCD only, so they are
+// accessed through that XCD's L2: loads with sc0 (they miss the CU's L1, which may hold an older copy),
+// stores with sc0 (written through to L2).  Device-scope (sc1) accesses would also be correct but take
+// the longer path that keeps all XCDs coherent.  Byte offsets; polls are volatile (re-read each time).
+typedef int xcd_v2 __attribute__((ext_vector_type(2)));
+typedef int xcd_v4 __attribute__((ext_vector_type(4)));
+constexpr int kXcdLoad = 1;                    // sc0
+constexpr int kXcdPoll = 1 | (int)(1u << 31);  // sc0, volatile
+
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t xcd_rsrc(const void* p, uint32_t bytes) {
+    // word 3 = 0x00020000: 32-bit data format, the gfx9-family raw-buffer setting.
+    return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(p), (short)0, (int)bytes, 0x00020000);
+}
+
+__device__ __forceinline__ bool flag_wait(__amdgpu_buffer_rsrc_t r, uint32_t off, uint32_t want, uint32_t limit,
+                                          int* err) {
+    for (uint32_t spins = 0;; ++spins) {
+        if ((uint32_t)__builtin_amdgcn_raw_buffer_load_b32(r, (int)off, 0, kXcdPoll) == want) return true;
+        if (spins >= limit) {
+            __hip_atomic_fetch_or(err, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            return false;
+        }
+        __builtin_amdgcn_s_sleep(1);
+    }
+}
+
+__device__ __forceinline__ void flag_set(__amdgpu_buffer_rsrc_t r, uint32_t off, uint32_t v) {
+    __builtin_amdgcn_raw_buffer_store_b32((int)v, r, (int)off, 0, kXcdLoad);
+}
+
+template <int FORM, typename U>
+__device__ void staged_stager(const HotArgs& h, const HotSched& sc, uint32_t* lds) {
+    const EpochArgs& a = h.e;
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    {
+        uint32_t* const same_xcd_word = lds + (uint32_t)kHotWaves * hot_buf_words(h.cap, h.Smax);
+        uint32_t& same_xcd = *same_xcd_word;
+        if (threadIdx.x == 0) {
+            uint32_t ok = 0;
+            for (uint32_t spins = 0; spins < h.spin_limit; ++spins) {
+                if (__hip_atomic_load(h.prog, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) == h.tag) {
+                    ok = __hip_atomic_load(h.prog + 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) == hot_xcc_id();
+                    break;
+                }
+                __builtin_amdgcn_s_sleep(2);
+            }
+            same_xcd = ok;
+        }
+        __syncthreads();
+        if (!same_xcd) return;
+    }
+    const SharedBuf<U> ub = shared_buf<U>(a.u, a.u_bytes, nullptr, a.u_shift);
+    const uint32_t Smax = h.Smax, cap = h.cap, IW = hot_buf_words(cap, Smax), RW = staged_rec_words(cap, Smax);
+    const HotBuf hb = hot_buf(lds + (uint32_t)wave * IW, cap, Smax);
+    const __amdgpu_buffer_rsrc_t fr = xcd_rsrc(h.flags, kHotFlagWords * 4u);
+    const __amdgpu_buffer_rsrc_t rr = xcd_rsrc(h.results, kHotResultWords * 8u);
+    uint32_t* const claim = h.flags + 3 * kHotRing;
+    U* const uu = static_cast<U*>(a.u);
+    constexpr int NE = kHotEntriesPerLane;
+    const uint32_t c0 = (uint32_t)lane / Smax, k0 = (uint32_t)lane - c0 * Smax;
+    const uint32_t dc = 64u / Smax, dk = 64u - dc * Smax;
+    float touch = 0.0f;
+    for (;;) {
+        uint32_t b = 0;
+        if (lane == 0) b = __hip_atomic_fetch_add(claim, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        b = (uint32_t)__shfl((int)b, 0);
+        if (b >= sc.nb) break;
+        const uint32_t s = b % kHotRing;
+        // The record's previous batch (b - kHotRing) must have been loaded.
+        if (b >= kHotRing && !flag_wait(fr, (kHotRing + s) * 4u, b - kHotRing + 1u, h.spin_limit, h.err)) break;
+        const uint32_t B = hot_batch_size(sc, b), NB = B * Smax;
+        HotMeta md;
+        md.m = hot_coord(a, sc, b, lane);
+        hot_meta_load(a, md);
+        const uint32_t len = md.m != kHotEmpty ? (uint32_t)(md.s1 - md.s0) : 0u;
+        int32_t ky[NE];
+        float vv[NE];
+        bool in[NE];
+        uint32_t c = c0, k = k0;
+#pragma unroll
+        for (int t = 0; t < NE; ++t) {
+            const uint32_t cc = c < B ? c : 0u;
+            const int64_t s0 = __shfl(md.s0, (int)cc);
+            const uint32_t lc = (uint32_t)__shfl((int)len, (int)cc);
+            in[t] = c < B && k < lc;
+            const int64_t kk = in[t] ? s0 + k : 0;
+            ky[t] = h.entry_key[kk];
+            vv[t] = a.val[kk];
+            c += dc;
+            k += dk;
+            if (k >= Smax) {
+                k -= Smax;
+                ++c;
+            }
+        }
+        // The LDS image, as a producer writes it (the cold part of each record stays 0: the loader adds it).
+        if ((uint32_t)lane < B) {
+            hb.mid[lane] = md.m;
+            hb.rec[lane] = make_float4(md.m_old, hot_step_scale<FORM>(md.sn, a.k), md.ylab, 0.0f);
+        }
+        uint32_t* const rec = h.ring + (size_t)s * RW;
+        int2* const pairs = reinterpret_cast<int2*>(rec + IW);
+        c = c0;
+        k = k0;
+#pragma unroll
+        for (int t = 0; t < NE; ++t) {
+            const uint32_t e = (uint32_t)t * 64u + (uint32_t)lane;
+            const bool hot = in[t] && ky[t] < 0, cold = in[t] && ky[t] >= 0;
+            if (e < NB) {
+                const uint32_t zlane = ((c & 7u) << 3) | (k & 7u);
+                hb.kv[e] = make_int2(hot ? -1 - ky[t] : (int32_t)(h.n_hot + zlane), __float_as_int(hot ? vv[t] : 0.0f));
+            }
+            if (e < cap * Smax) pairs[e] = make_int2(cold ? ky[t] : 0, __float_as_int(cold ? vv[t] : 0.0f));
+            c += dc;
+            k += dk;
+            if (k >= Smax) {
+                k -= Smax;
+                ++c;
+            }
+        }
+        // Copy the image into the record (the wave's LDS operations complete in order).
+        const uint4* src = reinterpret_cast<const uint4*>(hb.rec);
+        uint4* dst = reinterpret_cast<uint4*>(rec);
+        for (uint32_t i = (uint32_t)lane; i < IW / 4u; i += 64u) dst[i] = src[i];
+        // Publish only after every store of the record has completed.
+        __atomic_signal_fence(__ATOMIC_SEQ_CST);
+        __builtin_amdgcn_s_waitcnt(0x0F70);  // vmcnt(0)
+        __atomic_signal_fence(__ATOMIC_SEQ_CST);
+        if (lane == 0) flag_set(fr, s * 4u, b + 1u);
+        // Bring the cold entries into L2 for the loader's gathers.
+#pragma unroll
+        for (int t = 0; t < NE; ++t) touch += (float)hot_load_u<U>(ub, (uint32_t)ky[t], in[t] && ky[t] >= 0);
+        // Wait for the batch's results (lane c: coordinate c's model value and coefficient, tagged b + 1),
+        // then write the model values and the cold entries' updates out.
+        const uint32_t roff = (s * 64u + (uint32_t)lane) * 16u;
+        float model_new = 0.0f, coef = 0.0f;
+        bool got = false;
+        for (uint32_t spins = 0;; ++spins) {
+            if ((uint32_t)lane < B && !got) {
+                const xcd_v4 w = __builtin_amdgcn_raw_buffer_load_b128(rr, (int)roff, 0, kXcdPoll);
+                if ((uint32_t)w[1] == b + 1u && (uint32_t)w[3] == b + 1u) {
+                    got = true;
+                    model_new = __int_as_float(w[0]);
+                    coef = __int_as_float(w[2]);
+                }
+            }
+            if (__all(got || (uint32_t)lane >= B)) break;
+            if (spins >= h.spin_limit) {
+                if (lane == 0) __hip_atomic_fetch_or(h.err, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                return;
+            }
+            __builtin_amdgcn_s_sleep(1);
+        }
+        // The results are read: the record's result slot may take batch b + R.
+        if (lane == 0) flag_set(fr, (2 * kHotRing + s) * 4u, b + 1u);
+        if ((uint32_t)lane < B && md.m != kHotEmpty) a.model[md.m] = model_new;
+        c = c0;
+        k = k0;
+#pragma unroll
+        for (int t = 0; t < NE; ++t) {
+            const float cf = __shfl(coef, (int)(c < B ? c : 0u));
+            const float d = in[t] && ky[t] >= 0 ? cf * vv[t] : 0.0f;
+            if (d != 0.0f) atomic_add_u(uu + ky[t], d);
+            c += dc;
+            k += dk;
+            if (k >= Smax) {
+                k -= Smax;
+                ++c;
+            }
+        }
+    }
+    if (touch == 1.2345678e-38f) h.prog[3] = 1u;  // keeps the loads (prog[3] is read by nothing)
+}
+
+constexpr uint32_t kStagedImageVecs = (hot_buf_words(64, kHotEntriesPerLane) / 4 + 63) / 64;  // uint4 per lane, at most
+
+// Loader wave q of workgroup 0 (buffer q, batches q, q + NP, ...).  Per batch: once the consumer has
+// finished the buffer's previous batch, publish that batch's results (model value and coefficient of
+// each coordinate, as 64-bit words tagged with the batch) for its stager; then wait for the new batch's
+// record, load it, free the record, gather the cold values and sum each coordinate's cold part, and
+// hand the buffer to the consumer.  The loader issues no atomic on the shared vector, so none of its
+// waits for loads also waits for a scatter.
+template <int FORM, typename U>
+__device__ __forceinline__ void staged_loader(const HotArgs& h, const HotSched& sc, uint32_t* ready, uint32_t* freed,
+                                              uint32_t* abort_flag, uint32_t* bufs, uint32_t* moved_total, int q,
+                                              int lane) {
+    const EpochArgs& a = h.e;
+    const SharedBuf<U> ub = shared_buf<U>(a.u, a.u_bytes, nullptr, a.u_shift);
+    const uint32_t Smax = h.Smax, nb = sc.nb, NP = sc.NP, cap = h.cap;
+    const uint32_t IW = hot_buf_words(cap, Smax), RW = staged_rec_words(cap, Smax);
+    const uint32_t B = hot_batch(sc, hot_consumer_of(sc, (uint32_t)q)), NB = B * Smax;
+    const HotBuf hb = hot_buf(bufs + q * IW, cap, Smax);
+    const __amdgpu_buffer_rsrc_t fr = xcd_rsrc(h.flags, kHotFlagWords * 4u);
+    const __amdgpu_buffer_rsrc_t rr = xcd_rsrc(h.results, kHotResultWords * 8u);
+    const __amdgpu_buffer_rsrc_t gr = xcd_rsrc(h.ring, kHotRing * RW * 4u);
+    constexpr int NE = kHotEntriesPerLane;
+    constexpr int IV = (int)kStagedImageVecs;
+    const uint32_t c0 = (uint32_t)lane / Smax, k0 = (uint32_t)lane - c0 * Smax;
+    const uint32_t dc = 64u / Smax, dk = 64u - dc * Smax;
+    uint32_t moved = 0;
+    for (uint32_t b = (uint32_t)q; b < nb + NP; b += NP) {
+        const uint32_t n = b / NP;
+        if (n > 0 || b < nb) {
+            if (!hot_wait(freed + q, n, abort_flag, h.spin_limit, h.err)) break;
+        }
+        if (n > 0) {
+            // Results of the buffer's previous batch, for the stager that assembled it.
+            const uint32_t c = b - NP, s = c % kHotRing;
+            if (c >= kHotRing && !flag_wait(fr, (2 * kHotRing + s) * 4u, c - kHotRing + 1u, h.spin_limit, h.err)) {
+                __hip_atomic_store(abort_flag, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+                break;
+            }
+            if ((uint32_t)lane < B) {
+                const uint32_t m = hb.mid[lane];
+                const float2 zw = *reinterpret_cast<const float2*>(&hb.rec[lane].z);
+                moved += (m != kHotEmpty && zw.y != 0.0f) ? 1u : 0u;
+                // Each 8-byte half (value, tag) is written and read whole, so a reader that sees the tag
+                // sees its value.
+                const xcd_v2 w0 = {__float_as_int(zw.x), (int)(c + 1u)}, w1 = {__float_as_int(zw.y), (int)(c + 1u)};
+                const uint32_t roff = (s * 64u + (uint32_t)lane) * 16u;
+                __builtin_amdgcn_raw_buffer_store_b64(w0, rr, (int)roff, 0, kXcdLoad);
+                __builtin_amdgcn_raw_buffer_store_b64(w1, rr, (int)roff + 8, 0, kXcdLoad);
+            }
+        }
+        if (b >= nb) break;
+        const uint32_t s = b % kHotRing;
+        if (!flag_wait(fr, s * 4u, b + 1u, h.spin_limit, h.err)) {
+            __hip_atomic_store(abort_flag, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+            break;
+        }
+        // Loads that miss this CU's L1, which may hold the record's previous batch; lanes past the
+        // record read at an out-of-range offset (0, no access).
+        const uint32_t rbase = s * RW * 4u;
+        xcd_v4 img[IV];
+#pragma unroll
+        for (int v = 0; v < IV; ++v) {
+            const uint32_t i = (uint32_t)lane + 64u * (uint32_t)v;
+            img[v] = __builtin_amdgcn_raw_buffer_load_b128(gr, (int)(i < IW / 4u ? rbase + 16u * i : 0x7FFFFFF0u), 0,
+                                                           kXcdLoad);
+        }
+        int32_t ix[NE];
+        float vx[NE];
+#pragma unroll
+        for (int t = 0; t < NE; ++t) {
+            const uint32_t e = (uint32_t)t * 64u + (uint32_t)lane;
+            const xcd_v2 p = __builtin_amdgcn_raw_buffer_load_b64(
+                gr, (int)(e < cap * Smax ? rbase + 4u * IW + 8u * e : 0x7FFFFFF0u), 0, kXcdLoad);
+            ix[t] = p[0];
+            vx[t] = __int_as_float(p[1]);
+        }
+        U cv[NE];
+#pragma unroll
+        for (int t = 0; t < NE; ++t) cv[t] = hot_load_u<U>(ub, (uint32_t)ix[t], vx[t] != 0.0f);
+        float part[NE];
+#pragma unroll
+        for (int t = 0; t < NE; ++t) part[t] = group_sum<8>(vx[t] * (float)cv[t]);
+        // The record has been read (the sums above waited for every load): free it for batch b + R.
+        __atomic_signal_fence(__ATOMIC_SEQ_CST);
+        __builtin_amdgcn_s_waitcnt(0x0F70);  // vmcnt(0)
+        __atomic_signal_fence(__ATOMIC_SEQ_CST);
+        if (lane == 0) flag_set(fr, (kHotRing + s) * 4u, b + 1u);
+        xcd_v4* const dst = reinterpret_cast<xcd_v4*>(hb.rec);
+#pragma unroll
+        for (int v = 0; v < IV; ++v) {
+            const uint32_t i = (uint32_t)lane + 64u * (uint32_t)v;
+            if (i < IW / 4u) dst[i] = img[v];
+        }
+        uint32_t c = c0, k = k0;
+#pragma unroll
+        for (int t = 0; t < NE; ++t) {
+            const uint32_t e = (uint32_t)t * 64u + (uint32_t)lane;
+            if (e < NB && (lane & 7) == 0 && part[t] != 0.0f) atomicAdd(&hb.rec[c].w, part[t]);
+            c += dc;
+            k += dk;
+            if (k >= Smax) {
+                k -= Smax;
+                ++c;
+            }
+        }
+        __hip_atomic_store(ready + q, n + 1, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_WORKGROUP);
+    }
+    for (int o = 32; o > 0; o >>= 1) moved += __shfl_xor(moved, o, 64);
+    if (lane == 0) atomicAdd(moved_total, moved);
+}
+
+template <int FORM, typename U, int SL>
+__global__ __launch_bounds__(64 * kHotWaves) void k_epoch_staged(HotArgs h) {
+    extern __shared__ __align__(16) unsigned char hot_lds[];
+    const EpochArgs& a = h.e;
+    uint32_t W = h.W;
+    if (h.adapt_in) {
+        const uint32_t v = __hip_atomic_load(h.adapt_in, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        if (v >= h.NC && v <= h.NC * (uint32_t)kHotMaxGroups) W = v;
+    }
+    const HotSched sc = hot_sched(W, h.NC, h.cap, a.perm.n);
+    if (blockIdx.x > 0) {
+        if (blockIdx.x % kHotXcds == 0 && blockIdx.x / kHotXcds <= h.stagers)
+            staged_stager<FORM, U>(h, sc, reinterpret_cast<uint32_t*>(hot_lds));
+        return;
+    }
+    U* const hot = reinterpret_cast<U*>(hot_lds);
+    uint32_t* const ready = reinterpret_cast<uint32_t*>(hot_lds + h.hot_bytes);
+    uint32_t* const freed = ready + kHotMaxProducers;
+    uint32_t* const abort_flag = freed + kHotMaxProducers;
+    uint32_t* const moved = abort_flag + 1;
+    float* const scr = reinterpret_cast<float*>(hot_lds + h.hot_bytes + kHotFlagBytes);
+    uint32_t* const bufs = reinterpret_cast<uint32_t*>(hot_lds + h.hot_bytes + kHotFlagBytes + kHotScratchBytes);
+    U* const uu = static_cast<U*>(a.u);
+    const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+    if (tid == 0) {
+        // Workgroup 0's XCD and this launch, for the stagers.
+        __hip_atomic_store(h.prog + 1, hot_xcc_id(), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        __builtin_amdgcn_s_waitcnt(0x0F70);
+        __hip_atomic_store(h.prog, h.tag, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    }
+    for (uint32_t i = tid; i < h.n_hot + kHotZeroCells; i += blockDim.x) hot[i] = i < h.n_hot ? uu[h.hot_ids[i]] : U(0);
+    if (tid < 2 * kHotMaxProducers + 2) ready[tid] = 0u;
+    __syncthreads();
+    if ((uint32_t)wave < sc.NC)
+        hot_consumer<FORM, U, SL>(h, sc, (uint32_t)wave, hot, ready, freed, abort_flag, bufs, scr, lane);
+    else
+        staged_loader<FORM, U>(h, sc, ready, freed, abort_flag, bufs, moved, wave - (int)sc.NC, lane);
+    __syncthreads();
+    for (uint32_t i = tid; i < h.n_hot; i += blockDim.x) uu[h.hot_ids[i]] = hot[i];
+    if (h.adapt_out && tid == 0 && *abort_flag == 0u) {
+        const uint64_t mv = *moved, wmax = (uint64_t)h.NC * kHotMaxGroups;
+        uint64_t w = mv ? 1 + (uint64_t)(h.w_rule - 1) * a.perm.n / mv : wmax;
+        w = w < h.w_rule ? h.w_rule : w > wmax ? wmax : w;
+        __hip_atomic_store(h.adapt_out, (uint32_t)w, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    }
+}
+
 // The kernel instance for a formulation, storage type and row width (Smax / 8 entries per consumer lane).
 template <int FORM, typename U>
 static const void* hot_kernel_sl(uint32_t sl) {
@@ -470,6 +831,53 @@ hipError_t hot_prepare(int form, bool wide, uint32_t Smax, size_t lds_bytes) {
     const void* f = hot_kernel(form, wide, Smax);
     if (!f) return hipErrorInvalidValue;
     return hipFuncSetAttribute(f, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds_bytes);
+}
+
+template <int FORM, typename U>
+static const void* staged_kernel_sl(uint32_t sl) {
+    switch (sl) {
+        case 1: return reinterpret_cast<const void*>(&k_epoch_staged<FORM, U, 1>);
+        case 2: return reinterpret_cast<const void*>(&k_epoch_staged<FORM, U, 2>);
+        case 3: return reinterpret_cast<const void*>(&k_epoch_staged<FORM, U, 3>);
+        case 4: return reinterpret_cast<const void*>(&k_epoch_staged<FORM, U, 4>);
+        case 5: return reinterpret_cast<const void*>(&k_epoch_staged<FORM, U, 5>);
+        case 6: return reinterpret_cast<const void*>(&k_epoch_staged<FORM, U, 6>);
+        case 7: return reinterpret_cast<const void*>(&k_epoch_staged<FORM, U, 7>);
+        case 8: return reinterpret_cast<const void*>(&k_epoch_staged<FORM, U, 8>);
+        default: return nullptr;
+    }
+}
+
+static const void* staged_kernel(int form, bool wide, uint32_t Smax) {
+    const uint32_t sl = Smax / 8;
+    switch (form) {
+        case FORM_RIDGE_PRIMAL:
+            return wide ? staged_kernel_sl<FORM_RIDGE_PRIMAL, double>(sl) : staged_kernel_sl<FORM_RIDGE_PRIMAL, float>(sl);
+        case FORM_SVM_DUAL:
+            return wide ? staged_kernel_sl<FORM_SVM_DUAL, double>(sl) : staged_kernel_sl<FORM_SVM_DUAL, float>(sl);
+        case FORM_RIDGE_DUAL:
+            return wide ? staged_kernel_sl<FORM_RIDGE_DUAL, double>(sl) : staged_kernel_sl<FORM_RIDGE_DUAL, float>(sl);
+        default: return nullptr;
+    }
+}
+
+hipError_t staged_prepare(int form, bool wide, uint32_t Smax, size_t lds_bytes) {
+    const void* f = staged_kernel(form, wide, Smax);
+    if (!f) return hipErrorInvalidValue;
+    return hipFuncSetAttribute(f, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds_bytes);
+}
+
+hipError_t launch_epoch_staged(int form, bool wide, const HotArgs& h, size_t lds_bytes, hipStream_t s) {
+    const void* f = staged_kernel(form, wide, h.Smax);
+    if (!f || !h.ring || !h.flags || !h.results || !h.prog || h.stagers < 1 || h.cap > 64) return hipErrorInvalidValue;
+    // A stager keeps one batch image per wave in the dynamic LDS every workgroup of the launch receives.
+    if ((size_t)kHotWaves * hot_buf_words(h.cap, h.Smax) * 4 + 16 > lds_bytes) return hipErrorInvalidValue;
+    hipError_t e = launch_fill_zero(reinterpret_cast<uint64_t*>(h.flags), kHotFlagWords / 2, s);
+    if (e == hipSuccess) e = launch_fill_zero(h.results, kHotResultWords, s);
+    if (e != hipSuccess) return e;
+    HotArgs arg = h;
+    void* args[] = {&arg};
+    return hipLaunchKernel(f, dim3(1 + kHotXcds * h.stagers), dim3(64 * kHotWaves), args, lds_bytes, s);
 }
 
 hipError_t launch_epoch_hot(int form, bool wide, const HotArgs& h, size_t lds_bytes, hipStream_t s) {

@@ -65,7 +65,8 @@ enum {
     PLAN_PIPE = 4,
     PLAN_HOT = 5,
     PLAN_QUEUE = 6,
-    PLAN_TEAM = 7
+    PLAN_TEAM = 7,
+    PLAN_HOT_STAGED = 8  // PLAN_HOT with stager workgroups assembling the batches (large matrices)
 };
 
 struct LaunchPlan {
@@ -115,6 +116,7 @@ constexpr int kHotZeroCells = 64;         // hot-array cells after the hot set, 
 constexpr int kHotMaxGroups = 8;          // coordinates per consumer step (groups of 8 lanes)
 constexpr int kHotMaxWindow = kHotMaxConsumers * kHotMaxGroups;
 constexpr int kHotMaxSegment = 64;
+
 constexpr uint16_t kHotCold = 0xFFFF;    // slot_of value of an entry that is not hot
 
 // 32-bit words of one batch buffer (B coordinates, Smax entry slots each): a 4-word record per
@@ -123,6 +125,25 @@ constexpr uint16_t kHotCold = 0xFFFF;    // slot_of value of an entry that is no
 __host__ __device__ constexpr uint32_t hot_buf_words(uint32_t B, uint32_t Smax) {
     return (5u * B + 2u * B * Smax + 3u) & ~3u;
 }
+
+// Staged variant of the hot-set epoch: stager workgroups (on the XCD of workgroup 0: workgroups
+// kHotXcds, 2 kHotXcds, ...) claim batches, read their metadata and entries, and write each batch's
+// LDS image and its cold (index, value) pairs into a ring of kHotRing records in device memory;
+// workgroup 0's loader waves copy records into LDS, gather the cold values and write the results out.
+constexpr int kHotXcds = 8;
+constexpr int kHotStagers = 16;
+constexpr uint32_t kHotRing = 64;
+// 32-bit words of one ring record: the LDS image of a batch buffer, then cap * Smax (index, value)
+// pairs, rounded to 16 bytes.
+__host__ __device__ constexpr uint32_t staged_rec_words(uint32_t cap, uint32_t Smax) {
+    return hot_buf_words(cap, Smax) + ((2u * cap * Smax + 3u) & ~3u);
+}
+// Words of the ring's flags: tag[R] (batch + 1 staged), slot_free[R] (batch + 1 loaded), res_free[R]
+// (batch + 1 whose results its stager has read), the claim counter, padded; zeroed before every launch.
+constexpr uint32_t kHotFlagWords = 3 * kHotRing + 64;
+// 64-bit words of the result ring: per record, 2 words (model value, coefficient; each with the batch
+// + 1 in its high half) per coordinate of the batch; zeroed before every launch.
+constexpr uint32_t kHotResultWords = kHotRing * 64 * 2;
 
 struct HotArgs {
     EpochArgs e;
@@ -139,6 +160,13 @@ struct HotArgs {
     uint32_t spin_limit;      // bounded waits: after this many sleeps a wave gives up and sets *err
     uint32_t w_rule;          // adaptive window: coordinates in flight the coupling rule allows
                               // when every coordinate moves
+    // Staged variant only (null otherwise):
+    uint32_t* ring;            // [kHotRing][staged_rec_words(cap, Smax)]
+    uint32_t* flags;           // [kHotFlagWords], zero at launch
+    uint64_t* results;         // [kHotResultWords], zero at launch
+    uint32_t* prog;            // [4]: launch tag and XCD of workgroup 0, for the stagers
+    uint32_t tag;              // this launch's tag (nonzero, new for every staged launch of the handle)
+    uint32_t stagers;          // stager workgroups
     const uint32_t* adapt_in;  // adaptive window (null: W): coordinates in flight for this epoch,
                                // written by the previous epoch
     uint32_t* adapt_out;       // adaptive window (null: none): receives the next epoch's window, set
@@ -189,6 +217,10 @@ __host__ __device__ inline uint32_t hot_batch_size(const HotSched& s, uint32_t b
 size_t hot_lds_bytes(uint32_t hot_bytes, uint32_t B, uint32_t Smax);
 hipError_t hot_prepare(int form, bool wide, uint32_t Smax, size_t lds_bytes);
 hipError_t launch_epoch_hot(int form, bool wide, const HotArgs& h, size_t lds_bytes, hipStream_t s);
+// The staged variant (h.ring, h.flags, h.prog set): zeroes the flags, then launches 1 + kHotXcds *
+// h.stagers workgroups.
+hipError_t launch_epoch_staged(int form, bool wide, const HotArgs& h, size_t lds_bytes, hipStream_t s);
+hipError_t staged_prepare(int form, bool wide, uint32_t Smax, size_t lds_bytes);
 hipError_t launch_hot_count_ge(const unsigned* hits, int64_t L, unsigned T, unsigned long long* out2, hipStream_t s);
 hipError_t launch_hot_block_count(const unsigned* hits, int64_t L, unsigned T, unsigned* block_counts, hipStream_t s);
 hipError_t launch_hot_assign(const unsigned* hits, int64_t L, unsigned T, const unsigned* block_base, uint16_t* slot_of,

@@ -36,7 +36,7 @@ class _Matrix(ctypes.Structure):
                 ("idx", ctypes.c_void_p), ("val", ctypes.c_void_p)]
 
 
-KERNELS = ("group", "block", "ordered_lds", "mixed", "pipelined", "hot_lds", "queued", "team")
+KERNELS = ("group", "block", "ordered_lds", "mixed", "pipelined", "hot_lds", "queued", "team", "hot_staged")
 
 
 class _Info(ctypes.Structure):
