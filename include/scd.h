@@ -108,8 +108,9 @@ typedef struct {
                              create with Rademacher probes)                             */
     double coherence;     /* mean off-diagonal entry of G (signed sum)                  */
     int64_t auto_window;  /* window chosen from `coupling` when the option is 0         */
-    int64_t long_len;     /* segments longer than this are processed by a whole
-                             workgroup inside the group kernel (0 = none are)          */
+    int64_t long_len;     /* kernel 3: segments longer than this are processed by a
+                             whole workgroup inside the group kernel; kernel 9: the part
+                             length (entries); 0 otherwise                              */
     int32_t shared_fp64;  /* 1 if the shared vector is stored in fp64                   */
     uint32_t max_hits;    /* most stored entries sharing one shared-vector index, i.e.
                              the most atomic adds one entry receives per epoch          */
@@ -122,7 +123,9 @@ typedef struct {
                              segment lengths), 7 a team of workgroups per coordinate,
                              each on its own range of shared-vector indices (long
                              segments, few coordinates in flight), 8 hot set in LDS with
-                             stager workgroups assembling the batches (option "staged") */
+                             stager workgroups assembling the batches (option "staged"),
+                             9 as 6 over work units, long segments split into parts
+                             that many workgroups process side by side (option "split") */
     int32_t hot_entries;  /* shared-vector entries the hot-set kernel keeps in LDS
                              (0 until it is first needed)                               */
     int32_t adaptive_window; /* 1 if the epoch kernel sets each epoch's window from the
@@ -180,7 +183,7 @@ int scd_duality_gap_wait(scd_handle_t h, int32_t slot, double *gap, double *prim
  *   model_dev:  float32[n_coords]   (beta, or alpha)
  *   shared_dev: float32[shared_len] (w = A beta, or w(alpha), or wbar = A^T alpha)
  *   epoch:      host int64 (may be NULL).  Enqueues only, so it reports no error of the
- *   epochs before it: a hot-set or team epoch whose waits timed out (see "hot_wait_limit") leaves a
+ *   epochs before it: a hot-set, team or split epoch whose waits timed out (see "hot_wait_limit") leaves a
  *   partial state that this call copies as is; the next synchronising call returns the error.
  *   A state copied out and written back with scd_set_state resumes bit-exactly when the shared
  *   vector is stored in fp32 (option "shared_fp64" = 0); an fp64 shared vector is exchanged
@@ -219,6 +222,22 @@ int scd_set_state(scd_handle_t h, const float *model_dev, const float *shared_de
  *                 at a time: 0 (default) = 1 per 64 coordinates in flight (at least 1), else
  *                 1..64.  Larger chunks lower the claim rate on the queue's counter and let
  *                 coordinates start further from their permutation positions.
+ *   "split"       1 (default) = where the queued kernel (6) would run and some segment is longer than
+ *                 "split_part" entries, run kernel 9 instead: before each epoch a pre-pass (three
+ *                 kernels on the same stream) lays out the epoch's work units in permutation order,
+ *                 one per segment of at most split_part entries, and for a longer one of k parts, k
+ *                 gather units (partial inner products, published in device memory) followed by k
+ *                 scatter units (each waits for the k partials, takes the step and scatters its
+ *                 part).  Workgroups claim units in order, so a long segment is gathered and
+ *                 scattered by many CUs at once, and the window is not halved for long segments.
+ *                 The unit tables (40 bytes per unit, about one unit per coordinate) are made when
+ *                 this first applies for a part length: at create, on any scd_set_option, or at the
+ *                 first such epoch (synchronising).  Segments of more than 256 parts, or more than
+ *                 4e9 units, take kernel 6.  0 = never; 2 = a test hook: kernel 9 whenever "group" is 0,
+ *                 "pipeline" is 1 and the shared vector takes less than 2 GB, with as many workgroups
+ *                 as the window (window 1: one workgroup, which takes the units in order).
+ *   "split_part"  entries per part of kernel 9: 0 (default) = 4,096 (what a workgroup's register
+ *                 slices hold), else a multiple of 64 in [64, 4096].
  *   "hot"         1 (default) = with at most 16 coordinates in flight, segments of at most 64
  *                 entries and "group" 0, run the epoch in one workgroup that keeps the most-updated
  *                 shared-vector entries in LDS (their gathers and adds never leave the CU) and
@@ -255,7 +274,8 @@ int scd_set_state(scd_handle_t h, const float *model_dev, const float *shared_de
  *                 so it needs no synchronisation; the first epoch after scd_create, scd_set_state
  *                 or scd_set_option runs at auto_window.  0 = auto_window in every epoch.
  *   "hot_wait_limit"  test hook: sleeps (about 64 cycles each) one wait between the waves of the
- *                 hot-set kernel, or between the members of a team, may take before giving up;
+ *                 hot-set kernel, between the members of a team, or of a scatter unit of kernel 9
+ *                 for its segment's partials, may take before giving up;
  *                 the next synchronising call then returns SCD_ERR_HIP and the state stays invalid
  *                 until scd_set_state.  0 (default) = 2^24.
  *   "shared_fp64" 1 = store the shared vector in fp64 (fp64 atomic adds), 0 = fp32.  Chosen at

@@ -15,7 +15,8 @@ CSRC = os.path.join(HERE, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 LIB = os.path.join(HERE, "libscd.so")
 SOURCES = [os.path.join(CSRC, f)
-           for f in ("scd_epoch.hip", "scd_hot.hip", "scd_team.hip", "scd_setup.hip", "scd_static.hip", "scd_api.cpp")]
+           for f in ("scd_epoch.hip", "scd_hot.hip", "scd_team.hip", "scd_split.hip", "scd_setup.hip", "scd_static.hip",
+                     "scd_api.cpp")]
 # Measurement aid used by bench.py (device-wide atomic and copy rates); not linked into libscd.
 PROBE_LIB = os.path.join(HERE, "libscdprobe.so")
 PROBE_SOURCES = [os.path.join(CSRC, "ceiling.hip")]

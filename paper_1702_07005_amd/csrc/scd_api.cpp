@@ -173,6 +173,16 @@ struct scd_solver {
     uint32_t* team_bound = nullptr;  // [K + 1]
     uint64_t* team_slots = nullptr;  // [cus * 2 * kTeamMax] partial-sum slots (tag 0 at allocation)
     uint32_t team_tag = 1;        // tag of the next team step
+    // Split kernel (long segments cut into parts, many CUs each): unit tables built on first need for
+    // a part length.
+    int64_t split = 1;            // option: 0 never, 1 automatic, 2 wherever the queued kernel could run
+    int64_t split_part = 0;       // option: entries per part, 0 = kSplitMaxPart
+    uint32_t split_built = 0;     // part length of the tables (0 = none)
+    uint32_t split_n = 0;         // units per epoch at that part length
+    SplitUnit* split_units = nullptr;  // [split_n] records, rewritten by each epoch's pre-pass
+    uint64_t* split_partials = nullptr;  // [split_n] tagged partial sums (tag 0 at allocation)
+    uint32_t* split_tiles = nullptr;  // [ceil(C / kSplitPrepTile)] pre-pass scratch
+    uint32_t split_tag = 1;       // tag of the next split launch (never 0)
 };
 
 namespace {
@@ -297,12 +307,40 @@ int team_members(const scd_solver* h, int64_t* teams) {
     return (int)K;
 }
 
+uint32_t split_part_len(const scd_solver* h) { return h->split_part ? (uint32_t)h->split_part : kSplitMaxPart; }
+
+// The split kernel's limits: at most kSplitMaxParts parts per segment, fewer than 2^32 units per epoch
+// (a bound that does not depend on the permutation: each position yields one unit, or two per part).
+bool split_fits(const scd_solver* h, uint32_t part) {
+    if (h->split == 0 || h->max_seg > (int64_t)part * kSplitMaxParts) return false;
+    const double bound = (double)h->C + 2.0 * ((double)h->nnz / part + (double)h->C);
+    return bound < 4.0e9;
+}
+
 int plan_epoch(const scd_solver* h, LaunchPlan* lp, uint32_t* n_groups) {
     memset(lp, 0, sizeof *lp);
     lp->fresh = (int)h->fresh;
     const int G = h->group ? (int)h->group : auto_group(h);
     const int64_t window = h->window ? h->window : h->auto_window;
     lp->wide = h->wide;
+    const int64_t cap_blocks = (int64_t)h->cus * kBlocksPerCU;
+    // The pipelined, queued and split kernels address the shared vector as a raw buffer.
+    const bool pipe_ok = h->pipeline && shared_bytes(h) <= kPipeMaxBytes;
+    if (h->split == 2 && pipe_ok && h->group == 0 && split_fits(h, split_part_len(h))) {
+        // Forced (a test hook): the split kernel with `window` workgroups, also for window 1, where its
+        // single workgroup takes the units in order.
+        int64_t groups = std::min<int64_t>(window > 0 ? window : cap_blocks, std::min<int64_t>(cap_blocks, h->C));
+        groups = std::max<int64_t>(groups, 1);
+        lp->kind = PLAN_SPLIT;
+        lp->part = split_part_len(h);
+        lp->drain = 1;
+        lp->chunk = (int)(h->queue_chunk ? h->queue_chunk
+                                         : std::min<int64_t>(kQueueChunkMax, std::max<int64_t>(1, groups / 64)));
+        lp->group = kBlockThreads;
+        lp->blocks = (int)groups;
+        *n_groups = (uint32_t)groups;
+        return SCD_OK;
+    }
     if (window == 1) {
         const size_t need = (size_t)((h->L + 63) & ~int64_t(63)) * (h->wide ? sizeof(double) : sizeof(float)) +
                             2 * 16 * sizeof(float);
@@ -344,9 +382,6 @@ int plan_epoch(const scd_solver* h, LaunchPlan* lp, uint32_t* n_groups) {
         *n_groups = hg.adaptive ? hg.NC * kHotMaxGroups : hg.W;
         return SCD_OK;
     }
-    const int64_t cap_blocks = (int64_t)h->cus * kBlocksPerCU;
-    // Software-pipelined kernel: shared vector within a raw buffer's range.
-    const bool pipe_ok = h->pipeline && shared_bytes(h) <= kPipeMaxBytes;
     if (G == kBlockThreads) {
         int64_t groups = cap_blocks;
         if (window > 0 && window < groups) groups = window;
@@ -383,9 +418,14 @@ int plan_epoch(const scd_solver* h, LaunchPlan* lp, uint32_t* n_groups) {
         // within 1.06x of the sequential algorithm's (30 runs, text-ridge 3,500 x 166,000); at
         // full size (columns of up to 350,000 entries) the same rule went past 2x in 5 runs of 12,
         // half of it in none.
-        if (h->window == 0 && h->max_seg > (int64_t)kBlockThreads * kQueueSlices)
+        const uint32_t part = split_part_len(h);
+        const bool split = h->split == 1 && split_fits(h, part) && h->max_seg > (int64_t)part;
+        if (!split && h->window == 0 && h->max_seg > (int64_t)kBlockThreads * kQueueSlices)
             groups = std::max<int64_t>(1, groups / 2);
-        lp->kind = PLAN_QUEUE;
+        // The split kernel cuts such segments into parts that many workgroups gather and scatter side
+        // by side, so a dense column is in flight for about two unit steps: the window is kept.
+        lp->kind = split ? PLAN_SPLIT : PLAN_QUEUE;
+        lp->part = part;
         lp->drain = 1;
         // One counter serves about 8e7 claims per second; a workgroup claims about once per
         // 2-4 us, so every 64 workgroups share one claim per step.
@@ -633,11 +673,61 @@ int team_if_needed(scd_solver* h, hipStream_t s) {
     return build_team_tables(h, K, s);
 }
 
+void free_split_tables(scd_solver* h) {
+    (void)hipFree(h->split_units);
+    (void)hipFree(h->split_partials);
+    (void)hipFree(h->split_tiles);
+    h->split_units = nullptr;
+    h->split_partials = nullptr;
+    h->split_tiles = nullptr;
+    h->split_built = 0;
+    h->split_n = 0;
+}
+
+// Unit tables of the split kernel for part length `part`: the number of units per epoch (the same
+// for every permutation), the records the pre-pass rewrites each epoch, the tagged partial sums and
+// the pre-pass's tile counts.  Built once per part length (synchronises).
+int build_split_tables(scd_solver* h, uint32_t part, hipStream_t s) {
+    if (h->split_built == part) return SCD_OK;
+    free_split_tables(h);
+    unsigned long long* total = nullptr;
+    unsigned long long n = 0;
+    HIP_TRY(hipMalloc(&total, sizeof *total));
+    hipError_t e = launch_split_total(h->ptr, (uint32_t)h->C, part, total, s);
+    if (e == hipSuccess) e = hipMemcpyAsync(&n, total, sizeof n, hipMemcpyDeviceToHost, s);
+    if (e == hipSuccess) e = hipStreamSynchronize(s);
+    (void)hipFree(total);
+    if (e != hipSuccess) return fail(SCD_ERR_HIP, "split unit count: %s", hipGetErrorString(e));
+    if (n == 0 || n >= 0xFFFFFFFFull) return fail(SCD_ERR_UNSUPPORTED, "split kernel: %llu units per epoch", n);
+    const size_t tiles = (size_t)((h->C + kSplitPrepTile - 1) / kSplitPrepTile);
+    e = hipMalloc(&h->split_units, sizeof(SplitUnit) * (size_t)n);
+    if (e == hipSuccess) e = hipMalloc(&h->split_partials, sizeof(uint64_t) * (size_t)n);
+    if (e == hipSuccess) e = hipMalloc(&h->split_tiles, sizeof(uint32_t) * std::max<size_t>(tiles, 1));
+    if (e == hipSuccess) e = hipMemsetAsync(h->split_partials, 0, sizeof(uint64_t) * (size_t)n, s);
+    if (e == hipSuccess) e = hipStreamSynchronize(s);
+    if (e != hipSuccess) {
+        free_split_tables(h);
+        return fail(SCD_ERR_HIP, "split tables (%llu units): %s", n, hipGetErrorString(e));
+    }
+    h->split_built = part;
+    h->split_n = (uint32_t)n;
+    h->split_tag = 1;
+    return SCD_OK;
+}
+
+// Builds the split tables when the current options would use the split kernel.
+int split_if_needed(scd_solver* h, hipStream_t s) {
+    LaunchPlan lp;
+    uint32_t n_groups = 1;
+    if (plan_epoch(h, &lp, &n_groups) != SCD_OK || lp.kind != PLAN_SPLIT) return SCD_OK;
+    return build_split_tables(h, lp.part, s);
+}
+
 int check_hot_err(int v) {
     if (v)
         return fail(SCD_ERR_HIP,
-                    "epoch kernel: a bounded wait (between the hot-set kernel's waves or the team kernel's members) "
-                    "timed out; the state is invalid");
+                    "epoch kernel: a bounded wait (between the hot-set kernel's waves, the team kernel's members or "
+                    "the split kernel's parts) timed out; the state is invalid");
     return SCD_OK;
 }
 
@@ -683,6 +773,7 @@ void release(scd_solver* h) {
     (void)hipFree(h->hot_ids);
     (void)hipFree(h->hot_err);
     free_team_tables(h);
+    free_split_tables(h);
     (void)hipFree(h->team_slots);
     (void)hipHostFree(h->err_host);
     if (h->host_sums) (void)hipHostFree(h->host_sums);
@@ -903,6 +994,7 @@ int scd_create(const scd_matrix_t* A, const float* y, double lambda, int32_t for
         }
         if (rc == SCD_OK) step(hot_if_needed(h, s));
         if (rc == SCD_OK) step(team_if_needed(h, s));
+        if (rc == SCD_OK) step(split_if_needed(h, s));
         hip(hipMemsetAsync(h->model, 0, sizeof(float) * (size_t)h->C, s), "zero model");
         hip(hipMemsetAsync(h->u, 0, (h->wide ? sizeof(double) : sizeof(float)) * (size_t)h->L, s), "zero shared");
         hip(hipStreamSynchronize(s), "synchronize");
@@ -936,6 +1028,8 @@ int scd_epochs(scd_handle_t h, uint64_t seed, int32_t n_epochs, void* stream) {
     uint32_t n_groups = 1;
     if (int r = plan_epoch(h, &lp, &n_groups)) return r;
     if (lp.kind == PLAN_ORDERED_LDS) HIP_TRY(ordered_lds_prepare(h->form, lp.wide != 0, lp.lds_bytes));
+    if (lp.kind == PLAN_SPLIT)
+        if (int r = build_split_tables(h, lp.part, (hipStream_t)stream)) return r;
     HotGeom hg{};
     if (lp.kind == PLAN_HOT || lp.kind == PLAN_HOT_STAGED) {
         hot_plan(h, h->window ? h->window : h->auto_window, &hg);
@@ -995,6 +1089,18 @@ int scd_epochs(scd_handle_t h, uint64_t seed, int32_t n_epochs, void* stream) {
             HIP_TRY(launch_epoch_team(h->form, h->wide != 0, lp.fresh != 0, ta, lp.blocks, h->cus, s));
             // Steps of the busiest team, plus one: the next launch's tags are all new.
             h->team_tag += (uint32_t)((h->C + n_groups - 1) / n_groups + 1);
+        } else if (lp.kind == PLAN_SPLIT) {
+            SplitArgs sa{};
+            sa.e = a;
+            sa.units = h->split_units;
+            sa.partials = h->split_partials;
+            sa.n_units = h->split_n;
+            sa.tag = h->split_tag;
+            sa.spin_limit = h->hot_wait_limit > 0 ? (uint32_t)h->hot_wait_limit : kHotSpinLimit;
+            sa.err = h->hot_err;
+            HIP_TRY(launch_epoch_split(h->form, h->wide != 0, lp.fresh != 0, sa, lp.part, h->split_tiles, h->split_units,
+                                       lp.blocks, s));
+            h->split_tag = h->split_tag == 0xFFFFFFFFu ? 1u : h->split_tag + 1u;
         } else if (lp.kind == PLAN_HOT || lp.kind == PLAN_HOT_STAGED) {
             HotArgs ha{};
             ha.e = a;
@@ -1177,6 +1283,13 @@ int scd_set_option(scd_handle_t h, const char* key, int64_t value) {
     } else if (!strcmp(key, "queue_chunk")) {
         if (value < 0 || value > (int64_t)kQueueChunkMax) return fail(SCD_ERR_INVALID, "queue_chunk must be in [0, 64]");
         h->queue_chunk = value;
+    } else if (!strcmp(key, "split")) {
+        if (value < 0 || value > 2) return fail(SCD_ERR_INVALID, "split must be 0, 1 or 2");
+        h->split = value;
+    } else if (!strcmp(key, "split_part")) {
+        if (value != 0 && (value < 64 || value > (int64_t)kSplitMaxPart || value % 64 != 0))
+            return fail(SCD_ERR_INVALID, "split_part must be 0 or a multiple of 64 in [64, %u]", kSplitMaxPart);
+        h->split_part = value;
     } else if (!strcmp(key, "shared_fp64")) {
         if (value != 0 && value != 1) return fail(SCD_ERR_INVALID, "shared_fp64 must be 0 or 1");
         if (value == h->wide) return SCD_OK;
@@ -1200,7 +1313,8 @@ int scd_set_option(scd_handle_t h, const char* key, int64_t value) {
     } else {
         return fail(SCD_ERR_UNSUPPORTED, "unknown option '%s'", key);
     }
-    return SCD_OK;
+    if (int r = set_device(h)) return r;
+    return split_if_needed(h, nullptr);
 }
 
 int scd_get_option(scd_handle_t h, const char* key, int64_t* value) {
@@ -1212,6 +1326,8 @@ int scd_get_option(scd_handle_t h, const char* key, int64_t* value) {
     else if (!strcmp(key, "pipeline")) *value = h->pipeline;
     else if (!strcmp(key, "spread")) *value = h->spread;
     else if (!strcmp(key, "queue_chunk")) *value = h->queue_chunk;
+    else if (!strcmp(key, "split")) *value = h->split;
+    else if (!strcmp(key, "split_part")) *value = h->split_part;
     else if (!strcmp(key, "hot")) *value = h->hot;
     else if (!strcmp(key, "hot_wait_limit")) *value = h->hot_wait_limit;
     else if (!strcmp(key, "team")) *value = h->team;
@@ -1251,7 +1367,7 @@ int scd_get_info(scd_handle_t h, scd_info_t* info) {
     plan_epoch(h, &lp, &n_groups);
     info->formulation = h->form;
     info->group_lanes = (lp.kind == PLAN_GROUP || lp.kind == PLAN_MIXED || lp.kind == PLAN_PIPE || lp.kind == PLAN_HOT ||
-                         lp.kind == PLAN_HOT_STAGED || lp.kind == PLAN_QUEUE)
+                         lp.kind == PLAN_HOT_STAGED || lp.kind == PLAN_QUEUE || lp.kind == PLAN_SPLIT)
                             ? lp.group
                         : lp.kind == PLAN_TEAM                 ? kBlockThreads * lp.team
                         : lp.kind == PLAN_BLOCK && !lp.ordered ? kBlockThreads
@@ -1262,7 +1378,7 @@ int scd_get_info(scd_handle_t h, scd_info_t* info) {
     info->adaptive_window = (lp.kind == PLAN_HOT || lp.kind == PLAN_HOT_STAGED) &&
                             hot_plan(h, h->window ? h->window : h->auto_window, &hg) && hg.adaptive;
     info->reserved = 0;
-    info->long_len = lp.kind == PLAN_MIXED ? lp.long_len : 0;
+    info->long_len = lp.kind == PLAN_MIXED ? lp.long_len : lp.kind == PLAN_SPLIT ? lp.part : 0;
     info->shared_fp64 = h->wide;
     info->max_hits = h->max_hits;
     info->n_coords = h->C;

@@ -66,7 +66,8 @@ enum {
     PLAN_HOT = 5,
     PLAN_QUEUE = 6,
     PLAN_TEAM = 7,
-    PLAN_HOT_STAGED = 8  // PLAN_HOT with stager workgroups assembling the batches (large matrices)
+    PLAN_HOT_STAGED = 8,  // PLAN_HOT with stager workgroups assembling the batches (large matrices)
+    PLAN_SPLIT = 9        // PLAN_QUEUE over work units: long segments split into parts (many CUs each)
 };
 
 struct LaunchPlan {
@@ -80,7 +81,8 @@ struct LaunchPlan {
     int tail;           // PLAN_GROUP: some segment is longer than the register slices
     int drain;          // PLAN_PIPE, PLAN_GROUP, PLAN_BLOCK: the window binds, so each group lets its scatter
                         // land before it gathers again
-    int chunk;          // PLAN_QUEUE: consecutive permutation positions per claim
+    int chunk;          // PLAN_QUEUE, PLAN_SPLIT: consecutive positions (units) per claim
+    uint32_t part;      // PLAN_SPLIT: entries per part of a long segment (multiple of 64, <= kSplitMaxPart)
     int wide;           // shared vector stored as double
     int unbound;        // PLAN_PIPE: the window does not bind (every coordinate may be in flight)
     int team;           // PLAN_TEAM: workgroups per in-flight coordinate (K)
@@ -263,6 +265,50 @@ hipError_t launch_epoch_team(int form, bool wide, bool fresh, const TeamArgs& t,
 hipError_t launch_team_partition(const int64_t* ptr, const int32_t* idx, const float* val, uint32_t C,
                                  const uint32_t* bound, int K, int32_t* out_idx, float* out_val, uint32_t* off,
                                  hipStream_t s);
+
+// Split epoch: the queued kernel over work units instead of permutation positions.  Before each
+// epoch a pre-pass lays the units out in permutation order: a segment of at most `part` entries is
+// one FULL unit; a longer one, of k = ceil(len / part) parts, is k GATHER units (part i's partial
+// inner product) followed by k SCATTER units (each waits for the coordinate's k partials, sums them
+// in a fixed order, takes the step and scatters part i).  The workgroups claim units in order from
+// the queue, so a long segment's parts are gathered, and then scattered, by many CUs at once.
+constexpr uint32_t kSplitMaxPart = 256 * kQueueSlices;  // a part fits the register slices
+constexpr uint32_t kSplitMaxParts = 256;                // parts per segment (4 per lane of the polling wave)
+constexpr uint32_t kSplitPrepTile = 2048;               // positions per workgroup of the pre-pass
+enum { SPLIT_FULL = 0, SPLIT_GATHER = 1, SPLIT_SCATTER = 2 };
+
+// One work unit, 32 bytes.  info = kind << 30 | parts << 15 | part index (parts, index < 2^15).
+// m_old is the model value at the start of the epoch: each coordinate is visited once per epoch and
+// only its own step writes it.
+struct SplitUnit {
+    int64_t s0;    // first entry of the unit's range
+    uint32_t len;  // entries in the range
+    uint32_t m;    // coordinate
+    float m_old, sn, ylab;
+    uint32_t info;
+};
+static_assert(sizeof(SplitUnit) == 32, "SplitUnit is 32 bytes");
+
+__host__ __device__ inline uint32_t split_units_of(int64_t len, uint32_t part) {
+    return len <= (int64_t)part ? 1u : 2u * (uint32_t)((len + part - 1) / part);
+}
+
+struct SplitArgs {
+    EpochArgs e;           // e.perm: the epoch's permutation; e.queue, e.chunk as for the queued kernel
+    const SplitUnit* units;
+    uint64_t* partials;    // [n_units]: GATHER unit u writes (fp32 bits | tag << 32) at partials[u]
+    uint32_t n_units;
+    uint32_t tag;          // this launch's tag (never 0; the host counts launches)
+    uint32_t spin_limit;   // bounded waits: after this many sleeps a SCATTER unit gives up and sets *err
+    int* err;
+};
+
+// Units of all coordinates for part length `part` (independent of the permutation): out[0] (u64).
+hipError_t launch_split_total(const int64_t* ptr, uint32_t C, uint32_t part, unsigned long long* out, hipStream_t s);
+// Pre-pass and epoch.  `block_units` holds ceil(C / kSplitPrepTile) words of scratch; `units` holds
+// n_units records.
+hipError_t launch_epoch_split(int form, bool wide, bool fresh, const SplitArgs& sa, uint32_t part,
+                              uint32_t* block_units, SplitUnit* units, int blocks, hipStream_t s);
 
 hipError_t launch_epoch(int form, const EpochArgs& a, const LaunchPlan& lp, hipStream_t s);
 hipError_t ordered_lds_prepare(int form, bool wide, size_t lds_bytes);

@@ -36,7 +36,8 @@ class _Matrix(ctypes.Structure):
                 ("idx", ctypes.c_void_p), ("val", ctypes.c_void_p)]
 
 
-KERNELS = ("group", "block", "ordered_lds", "mixed", "pipelined", "hot_lds", "queued", "team", "hot_staged")
+KERNELS = ("group", "block", "ordered_lds", "mixed", "pipelined", "hot_lds", "queued", "team", "hot_staged",
+           "split")
 
 
 class _Info(ctypes.Structure):
