@@ -451,29 +451,37 @@ __global__ __launch_bounds__(64 * kHotWaves) void k_epoch_hot(HotArgs h) {
 //     load the batch's cold shared-vector entries (values unused), so the loader finds them in L2.
 //   loader waves (workgroup 0, in place of the producers): once the consumer has finished the
 //     buffer's previous batch, publish its results (each coordinate's new model value and scatter
-//     coefficient) in a result ring; then wait for the record of the next batch, load it
-//     (device-scope loads, which read the XCD's L2), free the record, gather the cold values (as
-//     fresh as the producers' are), sum each coordinate's cold part and hand the buffer over.
+//     coefficient) in a result ring; then wait for the record of the next batch, load it, free
+//     the record, gather the cold values (as fresh as the producers' are), sum each coordinate's
+//     cold part and hand the buffer over.
 //   The stager of a batch waits for its results and writes the model values and the cold entries'
 //     updates out, so the hot-set workgroup never waits behind a device-scope atomic.
 //
-// Records travel through the L2 of one XCD: a stager's plain stores reach that L2 when its wait
-// for them ends, and the loader's device-scope loads miss its own L1.  So every stager checks that
-// it runs on workgroup 0's XCD (hardware XCC_ID) and leaves otherwise.  The flags are zeroed
-// before every launch; every wait is bounded.
+// A record is published by its stager's stores, a wait until they have completed, and the tag
+// store; the loader polls the tag (system scope) and then, before it loads the record, drops every
+// clean line the XCD's caches may hold (an agent-scope acquire: L1 and L2 invalidate).  Without
+// that acquire (sc0 loads only, which the compiler's model treats as coherent between the CUs of
+// one XCD) the loader now and then took some rows of a record stale: about one corrupted batch in
+// 5-10 epochs of the full click workload, each row's model value stored while its update never
+// reached the shared vector.  An L1 invalidate alone did not prevent it (3 of 3 runs corrupted);
+// the acquire did (132 epochs without one, over the variants tried), at about 5% of the epoch
+// time.  A full agent-scope release on the stager side (an L2 write-back per batch) doubled the
+// epoch.  Each stager workgroup also acquires once when it starts, before it reads the metadata
+// (the model values the previous epoch stored).  The stagers run on workgroup 0's XCD (hardware
+// XCC_ID; the others leave), so the ring stays in one L2.  The flags are zeroed before every
+// launch; every wait is bounded.
 // ----------------------------------------------------------------------------------------
 __device__ __forceinline__ uint32_t hot_xcc_id() {
     return (uint32_t)__builtin_amdgcn_s_getreg((3 << 11) | (0 << 6) | 20) & 15u;
 }
 
-// The ring, its flags and the result ring are shared by workgroups of one XCD only, so they are
-// accessed through that XCD's L2: loads with sc0 (they miss the CU's L1, which may hold an older copy),
-// stores with sc0 (written through to L2).  Device-scope (sc1) accesses would also be correct but take
-// the longer path that keeps all XCDs coherent.  Byte offsets; polls are volatile (re-read each time).
+// Ring, flags and results as raw buffers (byte offsets), shared by the CUs of one XCD: stores with sc0,
+// polls volatile (system scope, re-read each time), record loads after an agent-scope acquire.
 typedef int xcd_v2 __attribute__((ext_vector_type(2)));
 typedef int xcd_v4 __attribute__((ext_vector_type(4)));
 constexpr int kXcdLoad = 1;                    // sc0
 constexpr int kXcdPoll = 1 | (int)(1u << 31);  // sc0, volatile
+constexpr int kXcdStore = 1;                   // sc0
 
 __device__ __forceinline__ __amdgpu_buffer_rsrc_t xcd_rsrc(const void* p, uint32_t bytes) {
     // word 3 = 0x00020000: 32-bit data format, the gfx9-family raw-buffer setting.
@@ -493,7 +501,7 @@ __device__ __forceinline__ bool flag_wait(__amdgpu_buffer_rsrc_t r, uint32_t off
 }
 
 __device__ __forceinline__ void flag_set(__amdgpu_buffer_rsrc_t r, uint32_t off, uint32_t v) {
-    __builtin_amdgcn_raw_buffer_store_b32((int)v, r, (int)off, 0, kXcdLoad);
+    __builtin_amdgcn_raw_buffer_store_b32((int)v, r, (int)off, 0, kXcdStore);
 }
 
 template <int FORM, typename U>
@@ -517,6 +525,8 @@ __device__ void staged_stager(const HotArgs& h, const HotSched& sc, uint32_t* ld
         __syncthreads();
         if (!same_xcd) return;
     }
+    // Metadata written by the previous launch (model values) is read below: drop clean cached lines.
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
     const SharedBuf<U> ub = shared_buf<U>(a.u, a.u_bytes, nullptr, a.u_shift);
     const uint32_t Smax = h.Smax, cap = h.cap, IW = hot_buf_words(cap, Smax), RW = staged_rec_words(cap, Smax);
     const HotBuf hb = hot_buf(lds + (uint32_t)wave * IW, cap, Smax);
@@ -686,8 +696,8 @@ __device__ __forceinline__ void staged_loader(const HotArgs& h, const HotSched& 
                 // sees its value.
                 const xcd_v2 w0 = {__float_as_int(zw.x), (int)(c + 1u)}, w1 = {__float_as_int(zw.y), (int)(c + 1u)};
                 const uint32_t roff = (s * 64u + (uint32_t)lane) * 16u;
-                __builtin_amdgcn_raw_buffer_store_b64(w0, rr, (int)roff, 0, kXcdLoad);
-                __builtin_amdgcn_raw_buffer_store_b64(w1, rr, (int)roff + 8, 0, kXcdLoad);
+                __builtin_amdgcn_raw_buffer_store_b64(w0, rr, (int)roff, 0, kXcdStore);
+                __builtin_amdgcn_raw_buffer_store_b64(w1, rr, (int)roff + 8, 0, kXcdStore);
             }
         }
         if (b >= nb) break;
@@ -696,8 +706,9 @@ __device__ __forceinline__ void staged_loader(const HotArgs& h, const HotSched& 
             __hip_atomic_store(abort_flag, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
             break;
         }
-        // Loads that miss this CU's L1, which may hold the record's previous batch; lanes past the
-        // record read at an out-of-range offset (0, no access).
+        // Agent-scope acquire: no line cached from the slot's previous batch is read below.  Lanes
+        // past the record read at an out-of-range offset (0, no access).
+        __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
         const uint32_t rbase = s * RW * 4u;
         xcd_v4 img[IV];
 #pragma unroll

@@ -200,7 +200,7 @@ def test_split_limits():
 ASYNC = {
     # (problem, part, window: 0 = automatic, extra options)
     "text_ridge_part256": ("text_ridge_twin", 256, 0, {}),
-    "text_ridge_part64_w300": ("text_ridge_twin", 64, 300, {}),
+    "text_ridge_part64": ("text_ridge_twin", 64, 0, {}),
     "text_ridge_part256_fp64": ("text_ridge_twin", 256, 0, {"shared_fp64": 1}),
     "text_ridge_part256_chunk3": ("text_ridge_twin", 256, 0, {"queue_chunk": 3}),
     "text_ridge_part128_fresh": ("text_ridge_twin", 128, 0, {"fresh_reads": 1}),
@@ -313,7 +313,7 @@ def test_split_wait_limit():
     # time (valid state) or the timeout is reported at the next synchronising call and a written
     # state replaces the invalid one.
     p = problem("text_ridge_twin")
-    s = forced(p, 64, 300)
+    s = forced(p, 64, 300)  # many workgroups, many parts: waits are likely to meet unpublished partials
     assert s.info()["kernel"] == "split"
     s.set_option("hot_wait_limit", 1)
     s.epochs(0, 2)
