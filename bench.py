@@ -51,8 +51,8 @@ def algorithmic_bytes(prob) -> int:
 
 def kernel_source_hash() -> str:
     h = hashlib.sha256()
-    for f in ("scd_device.h", "scd_epoch.hip", "scd_hot.hip", "scd_team.hip", "scd_setup.hip", "scd_kernels.h",
-              "scd_api.cpp"):
+    for f in ("scd_device.h", "scd_epoch.hip", "scd_hot.hip", "scd_team.hip", "scd_split.hip", "scd_setup.hip",
+              "scd_kernels.h", "scd_api.cpp"):
         with open(os.path.join(ROOT, "paper_1702_07005_amd", "csrc", f), "rb") as fh:
             h.update(fh.read())
     return h.hexdigest()[:16]
@@ -325,9 +325,13 @@ def main():
     if ceil["atomic_adds_per_s"]:
         # The scatter issues one device-scope atomic per stored entry.
         rate = prob.nnz / epoch_avg
+        frac = rate / ceil["atomic_adds_per_s"]
         out["atomic_roofline"] = {"bound": "device-scope fp32 atomics", "achieved": rate,
                                   "peak": ceil["atomic_adds_per_s"], "unit": "atomic adds/s",
-                                  "frac": rate / ceil["atomic_adds_per_s"],
+                                  "frac": frac,
+                                  # every atomic is resolved beyond L2 at any scope, so this rate, not
+                                  # HBM bandwidth, binds an epoch that runs near it
+                                  "binding": frac >= 0.5,
                                   "gather_and_atomic_pairs_per_s": ceil["gather_and_atomic_pairs_per_s"],
                                   "gather_and_atomic_pairs_spread_per_s":
                                       ceil.get("gather_and_atomic_pairs_spread_per_s"),
