@@ -130,7 +130,7 @@ typedef struct {
                              (0 until it is first needed)                               */
     int32_t adaptive_window; /* 1 if the epoch kernel sets each epoch's window from the
                              coordinates that moved in the previous one (option "adapt"):
-                             the first epoch runs at auto_window                        */
+                             the first epoch opens at auto_window                       */
     int32_t reserved;
 } scd_info_t;
 
@@ -271,8 +271,10 @@ int scd_set_state(scd_handle_t h, const float *model_dev, const float *shared_de
  *                 whose step is zero (in the hinge SVM dual, one whose alpha stays at a bound of
  *                 the box) changes nothing that others read, so the coupling rule's budget holds
  *                 for the coordinates in flight that move.  The window is kept in device memory,
- *                 so it needs no synchronisation; the first epoch after scd_create, scd_set_state
- *                 or scd_set_option runs at auto_window.  0 = auto_window in every epoch.
+ *                 so it needs no synchronisation.  The first epoch after scd_create, scd_set_state
+ *                 or scd_set_option is two launches: its first ceil(C / 16) positions at
+ *                 auto_window, the rest at the window that the fraction moving among those gives
+ *                 (one launch at auto_window when C < 32).  0 = auto_window in every epoch.
  *   "hot_wait_limit"  test hook: sleeps (about 64 cycles each) one wait between the waves of the
  *                 hot-set kernel, between the members of a team, or of a scatter unit of kernel 9
  *                 for its segment's partials, may take before giving up;

@@ -1113,23 +1113,33 @@ int scd_epochs(scd_handle_t h, uint64_t seed, int32_t n_epochs, void* stream) {
             ha.Smax = hg.Smax;
             ha.hot_bytes = hg.hot_bytes;
             ha.w_rule = hg.W;
-            // The first epoch after the state or the options changed runs at the rule's window.
-            ha.adapt_in = hg.adaptive && !h->adapt_fresh ? h->hot_adapt : nullptr;
             ha.adapt_out = hg.adaptive ? h->hot_adapt : nullptr;
-            h->adapt_fresh = 0;
             ha.spin_limit = h->hot_wait_limit > 0 ? (uint32_t)h->hot_wait_limit : kHotSpinLimit;
             ha.err = h->hot_err;
-            if (lp.kind == PLAN_HOT_STAGED) {
-                ha.ring = h->ring;
-                ha.flags = h->ring_flags;
-                ha.results = h->ring_results;
-                ha.prog = h->ring_prog;
-                ha.tag = h->ring_tag;
-                ha.stagers = kHotStagers;
-                h->ring_tag = h->ring_tag == 0xFFFFFFFFu ? 1u : h->ring_tag + 1u;
-                HIP_TRY(launch_epoch_staged(h->form, h->wide != 0, ha, hg.lds, s));
-            } else {
-                HIP_TRY(launch_epoch_hot(h->form, h->wide != 0, ha, hg.lds, s));
+            // The first epoch after the state or the options changed has no moving fraction to go by:
+            // its opening segment (1/kHotOpening of the positions) runs at the rule's window, and the
+            // rest at the window that the rule gives from that segment's moving fraction.  Every
+            // later epoch is one launch at the window its predecessor left.
+            const uint32_t C = (uint32_t)h->C;
+            const bool opening = hg.adaptive && h->adapt_fresh && C >= 2 * kHotOpening;
+            const uint32_t n_open = opening ? (C + kHotOpening - 1) / kHotOpening : C;
+            for (int part = 0; part < (opening ? 2 : 1); ++part) {
+                ha.pos0 = part ? n_open : 0u;
+                ha.pos_n = part ? C - n_open : n_open;
+                ha.adapt_in = hg.adaptive && !h->adapt_fresh ? h->hot_adapt : nullptr;
+                h->adapt_fresh = 0;
+                if (lp.kind == PLAN_HOT_STAGED) {
+                    ha.ring = h->ring;
+                    ha.flags = h->ring_flags;
+                    ha.results = h->ring_results;
+                    ha.prog = h->ring_prog;
+                    ha.tag = h->ring_tag;
+                    ha.stagers = kHotStagers;
+                    h->ring_tag = h->ring_tag == 0xFFFFFFFFu ? 1u : h->ring_tag + 1u;
+                    HIP_TRY(launch_epoch_staged(h->form, h->wide != 0, ha, hg.lds, s));
+                } else {
+                    HIP_TRY(launch_epoch_hot(h->form, h->wide != 0, ha, hg.lds, s));
+                }
             }
         } else {
             HIP_TRY(launch_epoch(h->form, a, lp, s));

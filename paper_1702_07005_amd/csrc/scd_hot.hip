@@ -210,10 +210,10 @@ struct HotMeta {
     float m_old, sn, ylab;
 };
 
-__device__ __forceinline__ uint32_t hot_coord(const EpochArgs& a, const HotSched& sc, uint32_t b, int lane) {
+__device__ __forceinline__ uint32_t hot_coord(const HotArgs& h, const HotSched& sc, uint32_t b, int lane) {
     if (b >= sc.nb || (uint32_t)lane >= hot_batch_size(sc, b)) return kHotEmpty;
-    const uint32_t j = hot_batch_start(sc, b) + (uint32_t)lane;
-    return j < a.perm.n ? perm_at(j, a.perm) : kHotEmpty;
+    const uint32_t k = hot_batch_start(sc, b) + (uint32_t)lane;  // position within this launch's range
+    return k < h.pos_n ? perm_at(h.pos0 + k, h.e.perm) : kHotEmpty;
 }
 
 __device__ __forceinline__ void hot_meta_load(const EpochArgs& a, HotMeta& t) {
@@ -265,7 +265,7 @@ __device__ __forceinline__ void hot_producer(const HotArgs& h, const HotSched& s
     const uint32_t c0 = (uint32_t)lane / Smax, k0 = (uint32_t)lane - c0 * Smax;
     const uint32_t dc = 64u / Smax, dk = 64u - dc * Smax;
     HotMeta md;
-    md.m = hot_coord(a, sc, (uint32_t)q, lane);
+    md.m = hot_coord(h, sc, (uint32_t)q, lane);
     uint32_t moved = 0;  // this lane's coordinates whose step was nonzero
     hot_meta_load(a, md);
     int32_t fl_ix[NE];  // the buffer's current batch: cold entries' indices and values (0: none)
@@ -282,7 +282,7 @@ __device__ __forceinline__ void hot_producer(const HotArgs& h, const HotSched& s
         bool in[NE];
         float part[NE];  // cold part of the dot, summed over each aligned group of 8 lanes
         HotMeta nx;
-        nx.m = hot_coord(a, sc, b + NP, lane);
+        nx.m = hot_coord(h, sc, b + NP, lane);
         if (b < nb) {
             // Entries (entry 0 stands in for unused slots): key and value.
             const uint32_t len = md.m != kHotEmpty ? (uint32_t)(md.s1 - md.s0) : 0u;
@@ -409,13 +409,13 @@ __global__ __launch_bounds__(64 * kHotWaves) void k_epoch_hot(HotArgs h) {
     static_assert((kHotWaves - kHotMaxConsumers) % kHotMaxConsumers == 0, "a buffer's batches must share a consumer");
     U* const uu = static_cast<U*>(a.u);
     const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
-    // This epoch's window: fixed, or set by the previous epoch of the adaptive plan.
+    // This launch's window: fixed, or set by the previous launch of the adaptive plan.
     uint32_t W = h.W;
     if (h.adapt_in) {
         const uint32_t v = __hip_atomic_load(h.adapt_in, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
         if (v >= h.NC && v <= h.NC * (uint32_t)kHotMaxGroups) W = v;
     }
-    const HotSched sc = hot_sched(W, h.NC, h.cap, a.perm.n);
+    const HotSched sc = hot_sched(W, h.NC, h.cap, h.pos_n);
     for (uint32_t i = tid; i < h.n_hot + kHotZeroCells; i += blockDim.x) hot[i] = i < h.n_hot ? uu[h.hot_ids[i]] : U(0);
     if (tid < 2 * kHotMaxProducers + 2) ready[tid] = 0u;  // ready, freed, abort and moved are contiguous
     __syncthreads();
@@ -426,12 +426,12 @@ __global__ __launch_bounds__(64 * kHotWaves) void k_epoch_hot(HotArgs h) {
     }
     __syncthreads();
     for (uint32_t i = tid; i < h.n_hot; i += blockDim.x) uu[h.hot_ids[i]] = hot[i];
-    // Next epoch's window: (W - 1) f kappa <= budget with a fraction f of the coordinates moving,
-    // i.e. W = 1 + (w_rule - 1) / f, at most what the consumers hold.  An epoch that gave up keeps
-    // the window.
+    // Next launch's window: (W - 1) f kappa <= budget with a fraction f of this launch's coordinates
+    // moving, i.e. W = 1 + (w_rule - 1) / f, at most what the consumers hold.  A launch that gave up
+    // keeps the window.
     if (h.adapt_out && tid == 0 && *abort_flag == 0u) {
         const uint64_t mv = *moved, wmax = (uint64_t)h.NC * kHotMaxGroups;
-        uint64_t w = mv ? 1 + (uint64_t)(h.w_rule - 1) * a.perm.n / mv : wmax;
+        uint64_t w = mv ? 1 + (uint64_t)(h.w_rule - 1) * h.pos_n / mv : wmax;
         w = w < h.w_rule ? h.w_rule : w > wmax ? wmax : w;
         __hip_atomic_store(h.adapt_out, (uint32_t)w, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     }
@@ -548,7 +548,7 @@ __device__ void staged_stager(const HotArgs& h, const HotSched& sc, uint32_t* ld
         if (b >= kHotRing && !flag_wait(fr, (kHotRing + s) * 4u, b - kHotRing + 1u, h.spin_limit, h.err)) break;
         const uint32_t B = hot_batch_size(sc, b), NB = B * Smax;
         HotMeta md;
-        md.m = hot_coord(a, sc, b, lane);
+        md.m = hot_coord(h, sc, b, lane);
         hot_meta_load(a, md);
         const uint32_t len = md.m != kHotEmpty ? (uint32_t)(md.s1 - md.s0) : 0u;
         int32_t ky[NE];
@@ -771,7 +771,7 @@ __global__ __launch_bounds__(64 * kHotWaves) void k_epoch_staged(HotArgs h) {
         const uint32_t v = __hip_atomic_load(h.adapt_in, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
         if (v >= h.NC && v <= h.NC * (uint32_t)kHotMaxGroups) W = v;
     }
-    const HotSched sc = hot_sched(W, h.NC, h.cap, a.perm.n);
+    const HotSched sc = hot_sched(W, h.NC, h.cap, h.pos_n);
     if (blockIdx.x > 0) {
         if (blockIdx.x % kHotXcds == 0 && blockIdx.x / kHotXcds <= h.stagers)
             staged_stager<FORM, U>(h, sc, reinterpret_cast<uint32_t*>(hot_lds));
@@ -803,7 +803,7 @@ __global__ __launch_bounds__(64 * kHotWaves) void k_epoch_staged(HotArgs h) {
     for (uint32_t i = tid; i < h.n_hot; i += blockDim.x) uu[h.hot_ids[i]] = hot[i];
     if (h.adapt_out && tid == 0 && *abort_flag == 0u) {
         const uint64_t mv = *moved, wmax = (uint64_t)h.NC * kHotMaxGroups;
-        uint64_t w = mv ? 1 + (uint64_t)(h.w_rule - 1) * a.perm.n / mv : wmax;
+        uint64_t w = mv ? 1 + (uint64_t)(h.w_rule - 1) * h.pos_n / mv : wmax;
         w = w < h.w_rule ? h.w_rule : w > wmax ? wmax : w;
         __hip_atomic_store(h.adapt_out, (uint32_t)w, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     }

@@ -117,6 +117,8 @@ constexpr int kHotScratchBytes = kHotMaxConsumers * 64 * 8;  // write targets of
 constexpr int kHotZeroCells = 64;         // hot-array cells after the hot set, one per consumer lane
 constexpr int kHotMaxGroups = 8;          // coordinates per consumer step (groups of 8 lanes)
 constexpr int kHotMaxWindow = kHotMaxConsumers * kHotMaxGroups;
+// The first adaptive epoch runs its first 1/kHotOpening of the positions at the coupling rule's window.
+constexpr uint32_t kHotOpening = 16;
 constexpr int kHotMaxSegment = 64;
 
 constexpr uint16_t kHotCold = 0xFFFF;    // slot_of value of an entry that is not hot
@@ -162,6 +164,8 @@ struct HotArgs {
     uint32_t spin_limit;      // bounded waits: after this many sleeps a wave gives up and sets *err
     uint32_t w_rule;          // adaptive window: coordinates in flight the coupling rule allows
                               // when every coordinate moves
+    uint32_t pos0, pos_n;     // permutation positions [pos0, pos0 + pos_n) of the epoch that this
+                              // launch runs: the whole epoch, or one of its segments
     // Staged variant only (null otherwise):
     uint32_t* ring;            // [kHotRing][staged_rec_words(cap, Smax)]
     uint32_t* flags;           // [kHotFlagWords], zero at launch
@@ -169,9 +173,9 @@ struct HotArgs {
     uint32_t* prog;            // [4]: launch tag and XCD of workgroup 0, for the stagers
     uint32_t tag;              // this launch's tag (nonzero, new for every staged launch of the handle)
     uint32_t stagers;          // stager workgroups
-    const uint32_t* adapt_in;  // adaptive window (null: W): coordinates in flight for this epoch,
-                               // written by the previous epoch
-    uint32_t* adapt_out;       // adaptive window (null: none): receives the next epoch's window, set
+    const uint32_t* adapt_in;  // adaptive window (null: W): coordinates in flight for this launch,
+                               // written by the previous one
+    uint32_t* adapt_out;       // adaptive window (null: none): receives the next launch's window, set
                                // from the coordinates whose step was nonzero in this one
     int* err;
 };
