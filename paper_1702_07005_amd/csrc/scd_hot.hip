@@ -652,12 +652,38 @@ __device__ void staged_stager(const HotArgs& h, const HotSched& sc, uint32_t* ld
 
 constexpr uint32_t kStagedImageVecs = (hot_buf_words(64, kHotEntriesPerLane) / 4 + 63) / 64;  // uint4 per lane, at most
 
+// A loader's loads of one ring record (at byte offset rbase): the LDS image (IW words) and the cold
+// (index, value) pairs of its n_slots entry slots.  An agent-scope acquire comes first, so that no line
+// cached from the slot's previous batch is read; the caller has seen the record's tag.  Lanes past the
+// record read at an out-of-range offset (0, no access).  The loads are only issued here.
+template <int NE, int IV>
+__device__ __forceinline__ void staged_record_load(__amdgpu_buffer_rsrc_t gr, uint32_t rbase, uint32_t IW,
+                                                   uint32_t n_slots, int lane, xcd_v4 (&img)[IV], int32_t (&ix)[NE],
+                                                   float (&vx)[NE]) {
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
+#pragma unroll
+    for (int v = 0; v < IV; ++v) {
+        const uint32_t i = (uint32_t)lane + 64u * (uint32_t)v;
+        img[v] = __builtin_amdgcn_raw_buffer_load_b128(gr, (int)(i < IW / 4u ? rbase + 16u * i : 0x7FFFFFF0u), 0,
+                                                       kXcdLoad);
+    }
+#pragma unroll
+    for (int t = 0; t < NE; ++t) {
+        const uint32_t e = (uint32_t)t * 64u + (uint32_t)lane;
+        const xcd_v2 p = __builtin_amdgcn_raw_buffer_load_b64(
+            gr, (int)(e < n_slots ? rbase + 4u * IW + 8u * e : 0x7FFFFFF0u), 0, kXcdLoad);
+        ix[t] = p[0];
+        vx[t] = __int_as_float(p[1]);
+    }
+}
+
 // Loader wave q of workgroup 0 (buffer q, batches q, q + NP, ...).  Per batch: once the consumer has
 // finished the buffer's previous batch, publish that batch's results (model value and coefficient of
-// each coordinate, as 64-bit words tagged with the batch) for its stager; then wait for the new batch's
-// record, load it, free the record, gather the cold values and sum each coordinate's cold part, and
-// hand the buffer to the consumer.  The loader issues no atomic on the shared vector, so none of its
-// waits for loads also waits for a scatter.
+// each coordinate, as 64-bit words tagged with the batch) for its stager; then take the new batch's
+// record (usually loaded ahead, see below; else wait for its tag and load it now), gather the cold
+// values and sum each coordinate's cold part, write the buffer, free the record and hand the buffer to
+// the consumer.  The loader issues no atomic on the shared vector, so none of its waits for loads also
+// waits for a scatter.
 template <int FORM, typename U>
 __device__ __forceinline__ void staged_loader(const HotArgs& h, const HotSched& sc, uint32_t* ready, uint32_t* freed,
                                               uint32_t* abort_flag, uint32_t* bufs, uint32_t* moved_total, int q,
@@ -676,6 +702,21 @@ __device__ __forceinline__ void staged_loader(const HotArgs& h, const HotSched& 
     const uint32_t c0 = (uint32_t)lane / Smax, k0 = (uint32_t)lane - c0 * Smax;
     const uint32_t dc = 64u / Smax, dk = 64u - dc * Smax;
     uint32_t moved = 0;
+    // Flag words are read ahead so that their round trips overlap the consumer's steps: when batch b
+    // has been handed over, the loader reads whether the result slot of the batch it hands over next
+    // is free, and the record tag of its batch after next.  If the tag of its next batch (read one
+    // batch earlier) is already set, it also issues that batch's record loads into registers then;
+    // only the cold gathers, which must see recent updates, wait until the batch's turn.  A flag word
+    // that was read ahead and not yet set is read again when needed.  A flag, once set, stays set for
+    // the launch.
+    uint32_t tag_seen = 0, tag_ahead = 0, res_seen = 0;
+    bool pre = false;  // img, ix and vx hold batch b's record, loaded ahead
+    xcd_v4 img[IV];
+    int32_t ix[NE];
+    float vx[NE];
+    if ((uint32_t)q + NP < nb)
+        tag_ahead = (uint32_t)__builtin_amdgcn_raw_buffer_load_b32(fr, (int)((((uint32_t)q + NP) % kHotRing) * 4u), 0,
+                                                                   kXcdPoll);
     for (uint32_t b = (uint32_t)q; b < nb + NP; b += NP) {
         const uint32_t n = b / NP;
         if (n > 0 || b < nb) {
@@ -684,7 +725,8 @@ __device__ __forceinline__ void staged_loader(const HotArgs& h, const HotSched& 
         if (n > 0) {
             // Results of the buffer's previous batch, for the stager that assembled it.
             const uint32_t c = b - NP, s = c % kHotRing;
-            if (c >= kHotRing && !flag_wait(fr, (2 * kHotRing + s) * 4u, c - kHotRing + 1u, h.spin_limit, h.err)) {
+            if (c >= kHotRing && res_seen != c - kHotRing + 1u &&
+                !flag_wait(fr, (2 * kHotRing + s) * 4u, c - kHotRing + 1u, h.spin_limit, h.err)) {
                 __hip_atomic_store(abort_flag, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
                 break;
             }
@@ -702,30 +744,12 @@ __device__ __forceinline__ void staged_loader(const HotArgs& h, const HotSched& 
         }
         if (b >= nb) break;
         const uint32_t s = b % kHotRing;
-        if (!flag_wait(fr, s * 4u, b + 1u, h.spin_limit, h.err)) {
-            __hip_atomic_store(abort_flag, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
-            break;
-        }
-        // Agent-scope acquire: no line cached from the slot's previous batch is read below.  Lanes
-        // past the record read at an out-of-range offset (0, no access).
-        __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
-        const uint32_t rbase = s * RW * 4u;
-        xcd_v4 img[IV];
-#pragma unroll
-        for (int v = 0; v < IV; ++v) {
-            const uint32_t i = (uint32_t)lane + 64u * (uint32_t)v;
-            img[v] = __builtin_amdgcn_raw_buffer_load_b128(gr, (int)(i < IW / 4u ? rbase + 16u * i : 0x7FFFFFF0u), 0,
-                                                           kXcdLoad);
-        }
-        int32_t ix[NE];
-        float vx[NE];
-#pragma unroll
-        for (int t = 0; t < NE; ++t) {
-            const uint32_t e = (uint32_t)t * 64u + (uint32_t)lane;
-            const xcd_v2 p = __builtin_amdgcn_raw_buffer_load_b64(
-                gr, (int)(e < cap * Smax ? rbase + 4u * IW + 8u * e : 0x7FFFFFF0u), 0, kXcdLoad);
-            ix[t] = p[0];
-            vx[t] = __int_as_float(p[1]);
+        if (!pre) {
+            if (tag_seen != b + 1u && !flag_wait(fr, s * 4u, b + 1u, h.spin_limit, h.err)) {
+                __hip_atomic_store(abort_flag, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+                break;
+            }
+            staged_record_load<NE, IV>(gr, s * RW * 4u, IW, cap * Smax, lane, img, ix, vx);
         }
         U cv[NE];
 #pragma unroll
@@ -733,11 +757,10 @@ __device__ __forceinline__ void staged_loader(const HotArgs& h, const HotSched& 
         float part[NE];
 #pragma unroll
         for (int t = 0; t < NE; ++t) part[t] = group_sum<8>(vx[t] * (float)cv[t]);
-        // The record has been read (the sums above waited for every load): free it for batch b + R.
+        // The record has been read (the sums above waited for every load).
         __atomic_signal_fence(__ATOMIC_SEQ_CST);
         __builtin_amdgcn_s_waitcnt(0x0F70);  // vmcnt(0)
         __atomic_signal_fence(__ATOMIC_SEQ_CST);
-        if (lane == 0) flag_set(fr, (kHotRing + s) * 4u, b + 1u);
         xcd_v4* const dst = reinterpret_cast<xcd_v4*>(hb.rec);
 #pragma unroll
         for (int v = 0; v < IV; ++v) {
@@ -756,7 +779,23 @@ __device__ __forceinline__ void staged_loader(const HotArgs& h, const HotSched& 
                 ++c;
             }
         }
+        // The loads of the next batch's record go out here, while no other load or store of this
+        // wave is in flight (the acquire before them waits for all of them).  Then free this batch's
+        // record for batch b + R and hand the buffer over.
+        const uint32_t b2 = b + NP, b3 = b2 + NP;
+        pre = b2 < nb && tag_ahead == b2 + 1u;
+        if (pre) staged_record_load<NE, IV>(gr, (b2 % kHotRing) * RW * 4u, IW, cap * Smax, lane, img, ix, vx);
+        if (lane == 0) flag_set(fr, (kHotRing + s) * 4u, b + 1u);
         __hip_atomic_store(ready + q, n + 1, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_WORKGROUP);
+        tag_seen = b2 < nb && !pre
+                       ? (uint32_t)__builtin_amdgcn_raw_buffer_load_b32(fr, (int)((b2 % kHotRing) * 4u), 0, kXcdPoll)
+                       : 0u;
+        tag_ahead = b3 < nb
+                        ? (uint32_t)__builtin_amdgcn_raw_buffer_load_b32(fr, (int)((b3 % kHotRing) * 4u), 0, kXcdPoll)
+                        : 0u;
+        res_seen = b >= kHotRing
+                       ? (uint32_t)__builtin_amdgcn_raw_buffer_load_b32(fr, (int)((2 * kHotRing + s) * 4u), 0, kXcdPoll)
+                       : 0u;
     }
     for (int o = 32; o > 0; o >>= 1) moved += __shfl_xor(moved, o, 64);
     if (lane == 0) atomicAdd(moved_total, moved);
