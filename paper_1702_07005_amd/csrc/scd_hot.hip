@@ -41,12 +41,17 @@ size_t hot_lds_bytes(uint32_t hot_bytes, uint32_t cap, uint32_t Smax) {
            (size_t)kHotMaxProducers * hot_buf_words(cap, Smax) * sizeof(uint32_t);
 }
 
+// A value that is the same in every lane of the wave (a wave's index, a word that every lane read
+// from one address), marked so: the compiler then keeps it in a scalar register and branches on it
+// with scalar branches instead of execution masks.
+__device__ __forceinline__ uint32_t wave_uniform(uint32_t v) { return (uint32_t)__builtin_amdgcn_readfirstlane((int)v); }
+
 __device__ __forceinline__ bool hot_wait(uint32_t* flag, uint32_t want, uint32_t* abort_flag, uint32_t limit,
                                          int* err) {
     uint32_t spins = 0;
     for (;;) {
-        if (__hip_atomic_load(flag, __ATOMIC_ACQUIRE, __HIP_MEMORY_SCOPE_WORKGROUP) == want) return true;
-        if (__hip_atomic_load(abort_flag, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP)) return false;
+        if (wave_uniform(__hip_atomic_load(flag, __ATOMIC_ACQUIRE, __HIP_MEMORY_SCOPE_WORKGROUP)) == want) return true;
+        if (wave_uniform(__hip_atomic_load(abort_flag, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP))) return false;
         if (++spins > limit) {
             __hip_atomic_store(abort_flag, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
             __hip_atomic_fetch_or(err, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
@@ -408,7 +413,7 @@ __global__ __launch_bounds__(64 * kHotWaves) void k_epoch_hot(HotArgs h) {
     static_assert((2 * kHotMaxProducers + 2) * sizeof(uint32_t) <= kHotFlagBytes, "handover words exceed their area");
     static_assert((kHotWaves - kHotMaxConsumers) % kHotMaxConsumers == 0, "a buffer's batches must share a consumer");
     U* const uu = static_cast<U*>(a.u);
-    const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+    const int tid = threadIdx.x, wave = (int)wave_uniform((uint32_t)tid >> 6), lane = tid & 63;
     // This launch's window: fixed, or set by the previous launch of the adaptive plan.
     uint32_t W = h.W;
     if (h.adapt_in) {
@@ -491,7 +496,7 @@ __device__ __forceinline__ __amdgpu_buffer_rsrc_t xcd_rsrc(const void* p, uint32
 __device__ __forceinline__ bool flag_wait(__amdgpu_buffer_rsrc_t r, uint32_t off, uint32_t want, uint32_t limit,
                                           int* err) {
     for (uint32_t spins = 0;; ++spins) {
-        if ((uint32_t)__builtin_amdgcn_raw_buffer_load_b32(r, (int)off, 0, kXcdPoll) == want) return true;
+        if (wave_uniform((uint32_t)__builtin_amdgcn_raw_buffer_load_b32(r, (int)off, 0, kXcdPoll)) == want) return true;
         if (spins >= limit) {
             __hip_atomic_fetch_or(err, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
             return false;
@@ -507,7 +512,7 @@ __device__ __forceinline__ void flag_set(__amdgpu_buffer_rsrc_t r, uint32_t off,
 template <int FORM, typename U>
 __device__ void staged_stager(const HotArgs& h, const HotSched& sc, uint32_t* lds) {
     const EpochArgs& a = h.e;
-    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const int lane = threadIdx.x & 63, wave = (int)wave_uniform(threadIdx.x >> 6);
     {
         uint32_t* const same_xcd_word = lds + (uint32_t)kHotWaves * hot_buf_words(h.cap, h.Smax);
         uint32_t& same_xcd = *same_xcd_word;
@@ -541,7 +546,7 @@ __device__ void staged_stager(const HotArgs& h, const HotSched& sc, uint32_t* ld
     for (;;) {
         uint32_t b = 0;
         if (lane == 0) b = __hip_atomic_fetch_add(claim, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-        b = (uint32_t)__shfl((int)b, 0);
+        b = wave_uniform(b);  // lane 0's claim
         if (b >= sc.nb) break;
         const uint32_t s = b % kHotRing;
         // The record's previous batch (b - kHotRing) must have been loaded.
@@ -652,26 +657,22 @@ __device__ void staged_stager(const HotArgs& h, const HotSched& sc, uint32_t* ld
 
 constexpr uint32_t kStagedImageVecs = (hot_buf_words(64, kHotEntriesPerLane) / 4 + 63) / 64;  // uint4 per lane, at most
 
-// A loader's loads of one ring record (at byte offset rbase): the LDS image (IW words) and the cold
-// (index, value) pairs of its n_slots entry slots.  An agent-scope acquire comes first, so that no line
-// cached from the slot's previous batch is read; the caller has seen the record's tag.  Lanes past the
-// record read at an out-of-range offset (0, no access).  The loads are only issued here.
+// A loader's loads of one ring record (at byte offset rbase): the LDS image and the cold (index,
+// value) pairs of its entry slots.  ioff and eoff are the lane's offsets within a record (computed
+// once per launch; lanes past the record carry an out-of-range offset, so they read 0 and touch no
+// memory), and the record's base goes in the scalar offset.  An agent-scope acquire comes first, so
+// that no line cached from the slot's previous batch is read; the caller has seen the record's tag.
+// The loads are only issued here.
 template <int NE, int IV>
-__device__ __forceinline__ void staged_record_load(__amdgpu_buffer_rsrc_t gr, uint32_t rbase, uint32_t IW,
-                                                   uint32_t n_slots, int lane, xcd_v4 (&img)[IV], int32_t (&ix)[NE],
+__device__ __forceinline__ void staged_record_load(__amdgpu_buffer_rsrc_t gr, uint32_t rbase, const uint32_t (&ioff)[IV],
+                                                   const uint32_t (&eoff)[NE], xcd_v4 (&img)[IV], int32_t (&ix)[NE],
                                                    float (&vx)[NE]) {
     __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
 #pragma unroll
-    for (int v = 0; v < IV; ++v) {
-        const uint32_t i = (uint32_t)lane + 64u * (uint32_t)v;
-        img[v] = __builtin_amdgcn_raw_buffer_load_b128(gr, (int)(i < IW / 4u ? rbase + 16u * i : 0x7FFFFFF0u), 0,
-                                                       kXcdLoad);
-    }
+    for (int v = 0; v < IV; ++v) img[v] = __builtin_amdgcn_raw_buffer_load_b128(gr, (int)ioff[v], (int)rbase, kXcdLoad);
 #pragma unroll
     for (int t = 0; t < NE; ++t) {
-        const uint32_t e = (uint32_t)t * 64u + (uint32_t)lane;
-        const xcd_v2 p = __builtin_amdgcn_raw_buffer_load_b64(
-            gr, (int)(e < n_slots ? rbase + 4u * IW + 8u * e : 0x7FFFFFF0u), 0, kXcdLoad);
+        const xcd_v2 p = __builtin_amdgcn_raw_buffer_load_b64(gr, (int)eoff[t], (int)rbase, kXcdLoad);
         ix[t] = p[0];
         vx[t] = __int_as_float(p[1]);
     }
@@ -714,9 +715,22 @@ __device__ __forceinline__ void staged_loader(const HotArgs& h, const HotSched& 
     xcd_v4 img[IV];
     int32_t ix[NE];
     float vx[NE];
+    // Offsets within a record; out-of-range ones stay out of range once the record's base (below
+    // 2^20) is added.
+    uint32_t ioff[IV], eoff[NE];
+#pragma unroll
+    for (int v = 0; v < IV; ++v) {
+        const uint32_t i = (uint32_t)lane + 64u * (uint32_t)v;
+        ioff[v] = i < IW / 4u ? 16u * i : 0x7FF00000u;
+    }
+#pragma unroll
+    for (int t = 0; t < NE; ++t) {
+        const uint32_t e = (uint32_t)t * 64u + (uint32_t)lane;
+        eoff[t] = e < cap * Smax ? 4u * IW + 8u * e : 0x7FF00000u;
+    }
     if ((uint32_t)q + NP < nb)
-        tag_ahead = (uint32_t)__builtin_amdgcn_raw_buffer_load_b32(fr, (int)((((uint32_t)q + NP) % kHotRing) * 4u), 0,
-                                                                   kXcdPoll);
+        tag_ahead = wave_uniform((uint32_t)__builtin_amdgcn_raw_buffer_load_b32(
+            fr, (int)((((uint32_t)q + NP) % kHotRing) * 4u), 0, kXcdPoll));
     for (uint32_t b = (uint32_t)q; b < nb + NP; b += NP) {
         const uint32_t n = b / NP;
         if (n > 0 || b < nb) {
@@ -749,7 +763,7 @@ __device__ __forceinline__ void staged_loader(const HotArgs& h, const HotSched& 
                 __hip_atomic_store(abort_flag, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
                 break;
             }
-            staged_record_load<NE, IV>(gr, s * RW * 4u, IW, cap * Smax, lane, img, ix, vx);
+            staged_record_load<NE, IV>(gr, s * RW * 4u, ioff, eoff, img, ix, vx);
         }
         U cv[NE];
 #pragma unroll
@@ -765,7 +779,7 @@ __device__ __forceinline__ void staged_loader(const HotArgs& h, const HotSched& 
 #pragma unroll
         for (int v = 0; v < IV; ++v) {
             const uint32_t i = (uint32_t)lane + 64u * (uint32_t)v;
-            if (i < IW / 4u) dst[i] = img[v];
+            if (64u * (uint32_t)(v + 1) <= IW / 4u || i < IW / 4u) dst[i] = img[v];  // the first test is uniform
         }
         uint32_t c = c0, k = k0;
 #pragma unroll
@@ -784,18 +798,18 @@ __device__ __forceinline__ void staged_loader(const HotArgs& h, const HotSched& 
         // record for batch b + R and hand the buffer over.
         const uint32_t b2 = b + NP, b3 = b2 + NP;
         pre = b2 < nb && tag_ahead == b2 + 1u;
-        if (pre) staged_record_load<NE, IV>(gr, (b2 % kHotRing) * RW * 4u, IW, cap * Smax, lane, img, ix, vx);
+        if (pre) staged_record_load<NE, IV>(gr, (b2 % kHotRing) * RW * 4u, ioff, eoff, img, ix, vx);
         if (lane == 0) flag_set(fr, (kHotRing + s) * 4u, b + 1u);
         __hip_atomic_store(ready + q, n + 1, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_WORKGROUP);
-        tag_seen = b2 < nb && !pre
-                       ? (uint32_t)__builtin_amdgcn_raw_buffer_load_b32(fr, (int)((b2 % kHotRing) * 4u), 0, kXcdPoll)
-                       : 0u;
-        tag_ahead = b3 < nb
-                        ? (uint32_t)__builtin_amdgcn_raw_buffer_load_b32(fr, (int)((b3 % kHotRing) * 4u), 0, kXcdPoll)
-                        : 0u;
-        res_seen = b >= kHotRing
-                       ? (uint32_t)__builtin_amdgcn_raw_buffer_load_b32(fr, (int)((2 * kHotRing + s) * 4u), 0, kXcdPoll)
-                       : 0u;
+        tag_seen = b2 < nb && !pre ? wave_uniform((uint32_t)__builtin_amdgcn_raw_buffer_load_b32(
+                                         fr, (int)((b2 % kHotRing) * 4u), 0, kXcdPoll))
+                                   : 0u;
+        tag_ahead = b3 < nb ? wave_uniform((uint32_t)__builtin_amdgcn_raw_buffer_load_b32(
+                                  fr, (int)((b3 % kHotRing) * 4u), 0, kXcdPoll))
+                            : 0u;
+        res_seen = b >= kHotRing ? wave_uniform((uint32_t)__builtin_amdgcn_raw_buffer_load_b32(
+                                       fr, (int)((2 * kHotRing + s) * 4u), 0, kXcdPoll))
+                                 : 0u;
     }
     for (int o = 32; o > 0; o >>= 1) moved += __shfl_xor(moved, o, 64);
     if (lane == 0) atomicAdd(moved_total, moved);
@@ -824,7 +838,7 @@ __global__ __launch_bounds__(64 * kHotWaves) void k_epoch_staged(HotArgs h) {
     float* const scr = reinterpret_cast<float*>(hot_lds + h.hot_bytes + kHotFlagBytes);
     uint32_t* const bufs = reinterpret_cast<uint32_t*>(hot_lds + h.hot_bytes + kHotFlagBytes + kHotScratchBytes);
     U* const uu = static_cast<U*>(a.u);
-    const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+    const int tid = threadIdx.x, wave = (int)wave_uniform((uint32_t)tid >> 6), lane = tid & 63;
     if (tid == 0) {
         // Workgroup 0's XCD and this launch, for the stagers.
         __hip_atomic_store(h.prog + 1, hot_xcc_id(), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
