@@ -374,10 +374,11 @@ int plan_epoch(const scd_solver* h, LaunchPlan* lp, uint32_t* n_groups) {
     }
     HotGeom hg;
     if (hot_plan(h, window, &hg)) {
-        lp->kind = staged_plan(h) ? PLAN_HOT_STAGED : PLAN_HOT;
+        const bool staged = staged_plan(h) && staged_lds_bytes(hg.hot_bytes, hg.cap, hg.Smax) <= h->max_lds;
+        lp->kind = staged ? PLAN_HOT_STAGED : PLAN_HOT;
         lp->group = 8;
         lp->blocks = 1;
-        lp->lds_bytes = hg.lds;
+        lp->lds_bytes = staged ? staged_lds_bytes(hg.hot_bytes, hg.cap, hg.Smax) : hg.lds;
         // Coordinates in flight at most: what the consumers hold when the window adapts.
         *n_groups = hg.adaptive ? hg.NC * kHotMaxGroups : hg.W;
         return SCD_OK;
@@ -1033,6 +1034,7 @@ int scd_epochs(scd_handle_t h, uint64_t seed, int32_t n_epochs, void* stream) {
     HotGeom hg{};
     if (lp.kind == PLAN_HOT || lp.kind == PLAN_HOT_STAGED) {
         hot_plan(h, h->window ? h->window : h->auto_window, &hg);
+        hg.lds = lp.lds_bytes;  // the staged launch's workgroups all get the larger of the two needs
         if (lp.kind == PLAN_HOT)
             HIP_TRY(hot_prepare(h->form, h->wide != 0, hg.Smax, hg.lds));
         else

@@ -41,6 +41,12 @@ size_t hot_lds_bytes(uint32_t hot_bytes, uint32_t cap, uint32_t Smax) {
            (size_t)kHotMaxProducers * hot_buf_words(cap, Smax) * sizeof(uint32_t);
 }
 
+size_t staged_lds_bytes(uint32_t hot_bytes, uint32_t cap, uint32_t Smax) {
+    const size_t stager = (size_t)kHotWaves * hot_buf_words(cap, Smax) * sizeof(uint32_t) + 16;
+    const size_t hot = hot_lds_bytes(hot_bytes, cap, Smax);
+    return hot > stager ? hot : stager;
+}
+
 // A value that is the same in every lane of the wave (a wave's index, a word that every lane read
 // from one address), marked so: the compiler then keeps it in a scalar register and branches on it
 // with scalar branches instead of execution masks.
@@ -935,7 +941,7 @@ hipError_t launch_epoch_staged(int form, bool wide, const HotArgs& h, size_t lds
     const void* f = staged_kernel(form, wide, h.Smax);
     if (!f || !h.ring || !h.flags || !h.results || !h.prog || h.stagers < 1 || h.cap > 64) return hipErrorInvalidValue;
     // A stager keeps one batch image per wave in the dynamic LDS every workgroup of the launch receives.
-    if ((size_t)kHotWaves * hot_buf_words(h.cap, h.Smax) * 4 + 16 > lds_bytes) return hipErrorInvalidValue;
+    if (staged_lds_bytes(h.hot_bytes, h.cap, h.Smax) > lds_bytes) return hipErrorInvalidValue;
     hipError_t e = launch_fill_zero(reinterpret_cast<uint64_t*>(h.flags), kHotFlagWords / 2, s);
     if (e == hipSuccess) e = launch_fill_zero(h.results, kHotResultWords, s);
     if (e != hipSuccess) return e;

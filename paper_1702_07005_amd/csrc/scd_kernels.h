@@ -221,6 +221,9 @@ __host__ __device__ inline uint32_t hot_batch_size(const HotSched& s, uint32_t b
 }
 
 size_t hot_lds_bytes(uint32_t hot_bytes, uint32_t B, uint32_t Smax);
+// Dynamic LDS of a staged launch: every workgroup gets the same size, and a stager keeps one batch
+// image per wave, which exceeds the hot workgroup's need when the hot set is small.
+size_t staged_lds_bytes(uint32_t hot_bytes, uint32_t cap, uint32_t Smax);
 hipError_t hot_prepare(int form, bool wide, uint32_t Smax, size_t lds_bytes);
 hipError_t launch_epoch_hot(int form, bool wide, const HotArgs& h, size_t lds_bytes, hipStream_t s);
 // The staged variant (h.ring, h.flags, h.prog set): zeroes the flags, then launches 1 + kHotXcds *
