@@ -420,12 +420,14 @@ __global__ __launch_bounds__(64 * kHotWaves) void k_epoch_hot(HotArgs h) {
     static_assert((kHotWaves - kHotMaxConsumers) % kHotMaxConsumers == 0, "a buffer's batches must share a consumer");
     U* const uu = static_cast<U*>(a.u);
     const int tid = threadIdx.x, wave = (int)wave_uniform((uint32_t)tid >> 6), lane = tid & 63;
-    // This launch's window: fixed, or set by the previous launch of the adaptive plan.
+    // This launch's window: fixed, or set by the previous launch of the adaptive plan (and then split
+    // evenly between the consumers where that is faster).
     uint32_t W = h.W;
     if (h.adapt_in) {
         const uint32_t v = __hip_atomic_load(h.adapt_in, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
         if (v >= h.NC && v <= h.NC * (uint32_t)kHotMaxGroups) W = v;
     }
+    if (h.adapt_out) W = hot_balanced_window(W, h.NC, h.cap);
     const HotSched sc = hot_sched(W, h.NC, h.cap, h.pos_n);
     for (uint32_t i = tid; i < h.n_hot + kHotZeroCells; i += blockDim.x) hot[i] = i < h.n_hot ? uu[h.hot_ids[i]] : U(0);
     if (tid < 2 * kHotMaxProducers + 2) ready[tid] = 0u;  // ready, freed, abort and moved are contiguous
@@ -830,6 +832,7 @@ __global__ __launch_bounds__(64 * kHotWaves) void k_epoch_staged(HotArgs h) {
         const uint32_t v = __hip_atomic_load(h.adapt_in, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
         if (v >= h.NC && v <= h.NC * (uint32_t)kHotMaxGroups) W = v;
     }
+    if (h.adapt_out) W = hot_balanced_window(W, h.NC, h.cap);
     const HotSched sc = hot_sched(W, h.NC, h.cap, h.pos_n);
     if (blockIdx.x > 0) {
         if (blockIdx.x % kHotXcds == 0 && blockIdx.x / kHotXcds <= h.stagers)

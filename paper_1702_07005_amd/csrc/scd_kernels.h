@@ -207,6 +207,21 @@ __host__ __device__ inline HotSched hot_sched(uint32_t W, uint32_t NC, uint32_t 
     return s;
 }
 
+// An adaptive window that two consumers would split unevenly (odd W: w0 = w1 + 1) can leave the
+// consumer with the smaller share more steps per batch than the other (W = 11: batches of 12 rows
+// in 2 steps and of 15 rows in 3), and that consumer then sets the pace.  Such a window runs one
+// coordinate narrower when the even split moves more rows per step of the slower consumer (W = 11:
+// 10 as 5 + 5, batches of 15 rows in 3 steps each; likewise 9 -> 8 and 5 -> 4; 7, 13 and 15 stay).
+// A narrower window is within the coupling budget by construction.
+__host__ __device__ inline uint32_t hot_balanced_window(uint32_t W, uint32_t NC, uint32_t cap) {
+    if (NC != 2 || (W & 1u) == 0 || W < 5) return W;
+    const HotSched a = hot_sched(W, NC, cap, 0), b = hot_sched(W - 1, NC, cap, 0);
+    const uint32_t a0 = a.B0 / a.w0, a1 = a.B1 / a.w1, b0 = b.B0 / b.w0, b1 = b.B1 / b.w1;
+    const uint32_t sa = a0 > a1 ? a0 : a1, sb = b0 > b1 ? b0 : b1;  // steps per batch of the slower consumer
+    // rows per step of the slower consumer: (B0 + B1) / max steps, compared without division
+    return (uint64_t)(b.B0 + b.B1) * sa > (uint64_t)(a.B0 + a.B1) * sb ? W - 1 : W;
+}
+
 __host__ __device__ inline uint32_t hot_consumer_of(const HotSched& s, uint32_t b) { return s.NC == 1 ? 0u : (b & 1u); }
 __host__ __device__ inline uint32_t hot_groups(const HotSched& s, uint32_t c) { return c ? s.w1 : s.w0; }
 __host__ __device__ inline uint32_t hot_batch(const HotSched& s, uint32_t c) { return c ? s.B1 : s.B0; }
