@@ -260,8 +260,9 @@ int scd_set_state(scd_handle_t h, const float *model_dev, const float *shared_de
  *   "staged"      1 (default) = when the hot-set kernel runs the epoch and the matrix's entries take more
  *                 than 256 MB (beyond the GPU's Infinity Cache), the batches it runs are assembled by
  *                 stager workgroups on the hot-set workgroup's XCD (coordinate metadata, entry keys and
- *                 values) and passed through a ring of 64 records in device memory, so that the one
- *                 workgroup only loads records, gathers the cold entries and runs the steps; 2 =
+ *                 values, and the cold entries' shared-vector values) and passed through a ring of 32
+ *                 records in device memory, so that the one workgroup only copies records and runs
+ *                 the steps; 2 =
  *                 whenever the hot-set kernel runs; 0 = never.  The stagers need the GPU's CUs beside
  *                 the hot-set workgroup: a kernel of another stream that holds them delays the epoch,
  *                 and its bounded waits then report SCD_ERR_HIP.

@@ -29,10 +29,11 @@ namespace scd {
 // coordinates that moved and sets the next epoch's window so that the expected number of moving
 // coordinates in flight stays at what the coupling rule allows: W = 1 + (w_rule - 1) / f, f the
 // fraction that moved (in the hinge SVM dual most coordinates sit at a bound of the box and do not
-// move).  The first epoch runs at w_rule; the window lives in device memory, so the epochs of one
-// call need no synchronisation with the host.
-// Cold values are therefore read up to a few batches before their coordinate runs; cold
-// entries are by construction rarely updated, so such a read seldom misses an update.
+// move).  The first epoch after the state or the options changed opens with a launch over its
+// first 1/kHotOpening of the positions at w_rule and runs the rest at the window that opening gives;
+// the window lives in device memory, so the epochs of one call need no synchronisation with the host.
+// The producers read cold values up to a few batches before their coordinate runs; cold entries are
+// by construction rarely updated, so such a read seldom misses an update.
 // Producer and consumer hand buffers over through LDS sequence numbers; every wait is bounded
 // (spin_limit sleeps), after which the wave sets *err and all waves leave.
 // ----------------------------------------------------------------------------------------
@@ -458,15 +459,17 @@ __global__ __launch_bounds__(64 * kHotWaves) void k_epoch_hot(HotArgs h) {
 //
 //   stager waves (workgroups kHotXcds, 2 kHotXcds, ...): claim the next batch from a counter, wait
 //     until its ring record is free, read the coordinates' metadata and entry keys and values,
-//     assemble the batch's LDS image in their own LDS (records, hot keys and values, zero-cell keys
-//     for cold slots) and copy it into the record, followed by the cold (index, value) pairs; then
-//     wait until those stores have completed and publish the record's tag (batch + 1).  Last they
-//     load the batch's cold shared-vector entries (values unused), so the loader finds them in L2.
+//     gather the cold entries' shared-vector values, assemble the batch's LDS image in their own LDS
+//     (records with each coordinate's cold part of the dot, hot keys and values, zero-cell keys for
+//     cold slots) and copy it into the record; then wait until those stores have completed and
+//     publish the record's tag (batch + 1).  A batch runs at most kHotRing + NP batches after its
+//     stager read the cold values; cold entries are by construction rarely updated (an earlier
+//     version gathered them in the loader, about NP batches ahead, at the same per-epoch gap
+//     ratios and 6% more epoch time).
 //   loader waves (workgroup 0, in place of the producers): once the consumer has finished the
 //     buffer's previous batch, publish its results (each coordinate's new model value and scatter
-//     coefficient) in a result ring; then wait for the record of the next batch, load it, free
-//     the record, gather the cold values (as fresh as the producers' are), sum each coordinate's
-//     cold part and hand the buffer over.
+//     coefficient) in a result ring; then take the record of the next batch (read ahead when its
+//     tag was already set), copy it into the buffer, free the record and hand the buffer over.
 //   The stager of a batch waits for its results and writes the model values and the cold entries'
 //     updates out, so the hot-set workgroup never waits behind a device-scope atomic.
 //
@@ -550,7 +553,6 @@ __device__ void staged_stager(const HotArgs& h, const HotSched& sc, uint32_t* ld
     constexpr int NE = kHotEntriesPerLane;
     const uint32_t c0 = (uint32_t)lane / Smax, k0 = (uint32_t)lane - c0 * Smax;
     const uint32_t dc = 64u / Smax, dk = 64u - dc * Smax;
-    float touch = 0.0f;
     for (;;) {
         uint32_t b = 0;
         if (lane == 0) b = __hip_atomic_fetch_add(claim, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
@@ -584,24 +586,42 @@ __device__ void staged_stager(const HotArgs& h, const HotSched& sc, uint32_t* ld
                 ++c;
             }
         }
-        // The LDS image, as a producer writes it (the cold part of each record stays 0: the loader adds it).
+        // The cold entries' shared-vector values, read now: a batch runs at most kHotRing + NP batches
+        // after it is staged, and cold entries are by construction rarely updated.
+        U cv[NE];
+#pragma unroll
+        for (int t = 0; t < NE; ++t) cv[t] = hot_load_u<U>(ub, (uint32_t)ky[t], in[t] && ky[t] >= 0);
+        // The LDS image, as a producer writes it; each record's cold part of the dot is added below.
         if ((uint32_t)lane < B) {
             hb.mid[lane] = md.m;
             hb.rec[lane] = make_float4(md.m_old, hot_step_scale<FORM>(md.sn, a.k), md.ylab, 0.0f);
         }
-        uint32_t* const rec = h.ring + (size_t)s * RW;
-        int2* const pairs = reinterpret_cast<int2*>(rec + IW);
         c = c0;
         k = k0;
 #pragma unroll
         for (int t = 0; t < NE; ++t) {
             const uint32_t e = (uint32_t)t * 64u + (uint32_t)lane;
-            const bool hot = in[t] && ky[t] < 0, cold = in[t] && ky[t] >= 0;
+            const bool hot = in[t] && ky[t] < 0;
             if (e < NB) {
                 const uint32_t zlane = ((c & 7u) << 3) | (k & 7u);
                 hb.kv[e] = make_int2(hot ? -1 - ky[t] : (int32_t)(h.n_hot + zlane), __float_as_int(hot ? vv[t] : 0.0f));
             }
-            if (e < cap * Smax) pairs[e] = make_int2(cold ? ky[t] : 0, __float_as_int(cold ? vv[t] : 0.0f));
+            c += dc;
+            k += dk;
+            if (k >= Smax) {
+                k -= Smax;
+                ++c;
+            }
+        }
+        // Cold part: each aligned group of 8 slots belongs to one coordinate (Smax is a multiple of 8).
+        c = c0;
+        k = k0;
+#pragma unroll
+        for (int t = 0; t < NE; ++t) {
+            const uint32_t e = (uint32_t)t * 64u + (uint32_t)lane;
+            const bool cold = in[t] && ky[t] >= 0;
+            const float part = group_sum<8>(cold ? vv[t] * (float)cv[t] : 0.0f);
+            if (e < NB && (lane & 7) == 0 && part != 0.0f) atomicAdd(&hb.rec[c].w, part);
             c += dc;
             k += dk;
             if (k >= Smax) {
@@ -610,6 +630,7 @@ __device__ void staged_stager(const HotArgs& h, const HotSched& sc, uint32_t* ld
             }
         }
         // Copy the image into the record (the wave's LDS operations complete in order).
+        uint32_t* const rec = h.ring + (size_t)s * RW;
         const uint4* src = reinterpret_cast<const uint4*>(hb.rec);
         uint4* dst = reinterpret_cast<uint4*>(rec);
         for (uint32_t i = (uint32_t)lane; i < IW / 4u; i += 64u) dst[i] = src[i];
@@ -618,9 +639,6 @@ __device__ void staged_stager(const HotArgs& h, const HotSched& sc, uint32_t* ld
         __builtin_amdgcn_s_waitcnt(0x0F70);  // vmcnt(0)
         __atomic_signal_fence(__ATOMIC_SEQ_CST);
         if (lane == 0) flag_set(fr, s * 4u, b + 1u);
-        // Bring the cold entries into L2 for the loader's gathers.
-#pragma unroll
-        for (int t = 0; t < NE; ++t) touch += (float)hot_load_u<U>(ub, (uint32_t)ky[t], in[t] && ky[t] >= 0);
         // Wait for the batch's results (lane c: coordinate c's model value and coefficient, tagged b + 1),
         // then write the model values and the cold entries' updates out.
         const uint32_t roff = (s * 64u + (uint32_t)lane) * 16u;
@@ -660,81 +678,59 @@ __device__ void staged_stager(const HotArgs& h, const HotSched& sc, uint32_t* ld
             }
         }
     }
-    if (touch == 1.2345678e-38f) h.prog[3] = 1u;  // keeps the loads (prog[3] is read by nothing)
 }
 
 constexpr uint32_t kStagedImageVecs = (hot_buf_words(64, kHotEntriesPerLane) / 4 + 63) / 64;  // uint4 per lane, at most
 
-// A loader's loads of one ring record (at byte offset rbase): the LDS image and the cold (index,
-// value) pairs of its entry slots.  ioff and eoff are the lane's offsets within a record (computed
-// once per launch; lanes past the record carry an out-of-range offset, so they read 0 and touch no
-// memory), and the record's base goes in the scalar offset.  An agent-scope acquire comes first, so
-// that no line cached from the slot's previous batch is read; the caller has seen the record's tag.
-// The loads are only issued here.
-template <int NE, int IV>
+// A loader's loads of one ring record (at byte offset rbase): the LDS image of its batch.  ioff holds
+// the lane's offsets within a record (computed once per launch; lanes past the record carry an
+// out-of-range offset, so they read 0 and touch no memory), and the record's base goes in the scalar
+// offset.  An agent-scope acquire comes first, so that no line cached from the slot's previous batch
+// is read; the caller has seen the record's tag.  The loads are only issued here.
+template <int IV>
 __device__ __forceinline__ void staged_record_load(__amdgpu_buffer_rsrc_t gr, uint32_t rbase, const uint32_t (&ioff)[IV],
-                                                   const uint32_t (&eoff)[NE], xcd_v4 (&img)[IV], int32_t (&ix)[NE],
-                                                   float (&vx)[NE]) {
+                                                   xcd_v4 (&img)[IV]) {
     __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
 #pragma unroll
     for (int v = 0; v < IV; ++v) img[v] = __builtin_amdgcn_raw_buffer_load_b128(gr, (int)ioff[v], (int)rbase, kXcdLoad);
-#pragma unroll
-    for (int t = 0; t < NE; ++t) {
-        const xcd_v2 p = __builtin_amdgcn_raw_buffer_load_b64(gr, (int)eoff[t], (int)rbase, kXcdLoad);
-        ix[t] = p[0];
-        vx[t] = __int_as_float(p[1]);
-    }
 }
 
 // Loader wave q of workgroup 0 (buffer q, batches q, q + NP, ...).  Per batch: once the consumer has
 // finished the buffer's previous batch, publish that batch's results (model value and coefficient of
 // each coordinate, as 64-bit words tagged with the batch) for its stager; then take the new batch's
-// record (usually loaded ahead, see below; else wait for its tag and load it now), gather the cold
-// values and sum each coordinate's cold part, write the buffer, free the record and hand the buffer to
-// the consumer.  The loader issues no atomic on the shared vector, so none of its waits for loads also
-// waits for a scatter.
+// record (usually loaded ahead, see below; else wait for its tag and load it now), write it into the
+// buffer, free the record and hand the buffer to the consumer.  The stager has already added each
+// coordinate's cold part of the dot, so the loader gathers nothing, and it issues no atomic on the
+// shared vector.
 template <int FORM, typename U>
 __device__ __forceinline__ void staged_loader(const HotArgs& h, const HotSched& sc, uint32_t* ready, uint32_t* freed,
                                               uint32_t* abort_flag, uint32_t* bufs, uint32_t* moved_total, int q,
                                               int lane) {
-    const EpochArgs& a = h.e;
-    const SharedBuf<U> ub = shared_buf<U>(a.u, a.u_bytes, nullptr, a.u_shift);
     const uint32_t Smax = h.Smax, nb = sc.nb, NP = sc.NP, cap = h.cap;
     const uint32_t IW = hot_buf_words(cap, Smax), RW = staged_rec_words(cap, Smax);
-    const uint32_t B = hot_batch(sc, hot_consumer_of(sc, (uint32_t)q)), NB = B * Smax;
+    const uint32_t B = hot_batch(sc, hot_consumer_of(sc, (uint32_t)q));
     const HotBuf hb = hot_buf(bufs + q * IW, cap, Smax);
     const __amdgpu_buffer_rsrc_t fr = xcd_rsrc(h.flags, kHotFlagWords * 4u);
     const __amdgpu_buffer_rsrc_t rr = xcd_rsrc(h.results, kHotResultWords * 8u);
     const __amdgpu_buffer_rsrc_t gr = xcd_rsrc(h.ring, kHotRing * RW * 4u);
-    constexpr int NE = kHotEntriesPerLane;
     constexpr int IV = (int)kStagedImageVecs;
-    const uint32_t c0 = (uint32_t)lane / Smax, k0 = (uint32_t)lane - c0 * Smax;
-    const uint32_t dc = 64u / Smax, dk = 64u - dc * Smax;
     uint32_t moved = 0;
     // Flag words are read ahead so that their round trips overlap the consumer's steps: when batch b
     // has been handed over, the loader reads whether the result slot of the batch it hands over next
     // is free, and the record tag of its batch after next.  If the tag of its next batch (read one
-    // batch earlier) is already set, it also issues that batch's record loads into registers then;
-    // only the cold gathers, which must see recent updates, wait until the batch's turn.  A flag word
-    // that was read ahead and not yet set is read again when needed.  A flag, once set, stays set for
-    // the launch.
+    // batch earlier) is already set, it also issues that batch's record loads into registers then.
+    // A flag word that was read ahead and not yet set is read again when needed.  A flag, once set,
+    // stays set for the launch.
     uint32_t tag_seen = 0, tag_ahead = 0, res_seen = 0;
-    bool pre = false;  // img, ix and vx hold batch b's record, loaded ahead
+    bool pre = false;  // img holds batch b's record, loaded ahead
     xcd_v4 img[IV];
-    int32_t ix[NE];
-    float vx[NE];
     // Offsets within a record; out-of-range ones stay out of range once the record's base (below
     // 2^20) is added.
-    uint32_t ioff[IV], eoff[NE];
+    uint32_t ioff[IV];
 #pragma unroll
     for (int v = 0; v < IV; ++v) {
         const uint32_t i = (uint32_t)lane + 64u * (uint32_t)v;
         ioff[v] = i < IW / 4u ? 16u * i : 0x7FF00000u;
-    }
-#pragma unroll
-    for (int t = 0; t < NE; ++t) {
-        const uint32_t e = (uint32_t)t * 64u + (uint32_t)lane;
-        eoff[t] = e < cap * Smax ? 4u * IW + 8u * e : 0x7FF00000u;
     }
     if ((uint32_t)q + NP < nb)
         tag_ahead = wave_uniform((uint32_t)__builtin_amdgcn_raw_buffer_load_b32(
@@ -771,15 +767,9 @@ __device__ __forceinline__ void staged_loader(const HotArgs& h, const HotSched& 
                 __hip_atomic_store(abort_flag, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
                 break;
             }
-            staged_record_load<NE, IV>(gr, s * RW * 4u, ioff, eoff, img, ix, vx);
+            staged_record_load<IV>(gr, s * RW * 4u, ioff, img);
         }
-        U cv[NE];
-#pragma unroll
-        for (int t = 0; t < NE; ++t) cv[t] = hot_load_u<U>(ub, (uint32_t)ix[t], vx[t] != 0.0f);
-        float part[NE];
-#pragma unroll
-        for (int t = 0; t < NE; ++t) part[t] = group_sum<8>(vx[t] * (float)cv[t]);
-        // The record has been read (the sums above waited for every load).
+        // Wait for the record's loads (so its slot may be freed below), then write it into the buffer.
         __atomic_signal_fence(__ATOMIC_SEQ_CST);
         __builtin_amdgcn_s_waitcnt(0x0F70);  // vmcnt(0)
         __atomic_signal_fence(__ATOMIC_SEQ_CST);
@@ -789,24 +779,12 @@ __device__ __forceinline__ void staged_loader(const HotArgs& h, const HotSched& 
             const uint32_t i = (uint32_t)lane + 64u * (uint32_t)v;
             if (64u * (uint32_t)(v + 1) <= IW / 4u || i < IW / 4u) dst[i] = img[v];  // the first test is uniform
         }
-        uint32_t c = c0, k = k0;
-#pragma unroll
-        for (int t = 0; t < NE; ++t) {
-            const uint32_t e = (uint32_t)t * 64u + (uint32_t)lane;
-            if (e < NB && (lane & 7) == 0 && part[t] != 0.0f) atomicAdd(&hb.rec[c].w, part[t]);
-            c += dc;
-            k += dk;
-            if (k >= Smax) {
-                k -= Smax;
-                ++c;
-            }
-        }
         // The loads of the next batch's record go out here, while no other load or store of this
         // wave is in flight (the acquire before them waits for all of them).  Then free this batch's
         // record for batch b + R and hand the buffer over.
         const uint32_t b2 = b + NP, b3 = b2 + NP;
         pre = b2 < nb && tag_ahead == b2 + 1u;
-        if (pre) staged_record_load<NE, IV>(gr, (b2 % kHotRing) * RW * 4u, ioff, eoff, img, ix, vx);
+        if (pre) staged_record_load<IV>(gr, (b2 % kHotRing) * RW * 4u, ioff, img);
         if (lane == 0) flag_set(fr, (kHotRing + s) * 4u, b + 1u);
         __hip_atomic_store(ready + q, n + 1, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_WORKGROUP);
         tag_seen = b2 < nb && !pre ? wave_uniform((uint32_t)__builtin_amdgcn_raw_buffer_load_b32(

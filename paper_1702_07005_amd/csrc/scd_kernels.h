@@ -131,16 +131,16 @@ __host__ __device__ constexpr uint32_t hot_buf_words(uint32_t B, uint32_t Smax) 
 }
 
 // Staged variant of the hot-set epoch: stager workgroups (on the XCD of workgroup 0: workgroups
-// kHotXcds, 2 kHotXcds, ...) claim batches, read their metadata and entries, and write each batch's
-// LDS image and its cold (index, value) pairs into a ring of kHotRing records in device memory;
-// workgroup 0's loader waves copy records into LDS, gather the cold values and write the results out.
+// kHotXcds, 2 kHotXcds, ...) claim batches, read their metadata and entries, gather the cold entries'
+// shared-vector values, and write each batch's LDS image (with every coordinate's cold part of the
+// dot) into a ring of kHotRing records in device memory; workgroup 0's loader waves copy records
+// into LDS and hand the results back; the stagers write them out.
 constexpr int kHotXcds = 8;
 constexpr int kHotStagers = 16;
-constexpr uint32_t kHotRing = 64;
-// 32-bit words of one ring record: the LDS image of a batch buffer, then cap * Smax (index, value)
-// pairs, rounded to 16 bytes.
+constexpr uint32_t kHotRing = 32;
+// 32-bit words of one ring record: the LDS image of a batch buffer.
 __host__ __device__ constexpr uint32_t staged_rec_words(uint32_t cap, uint32_t Smax) {
-    return hot_buf_words(cap, Smax) + ((2u * cap * Smax + 3u) & ~3u);
+    return hot_buf_words(cap, Smax);
 }
 // Words of the ring's flags: tag[R] (batch + 1 staged), slot_free[R] (batch + 1 loaded), res_free[R]
 // (batch + 1 whose results its stager has read), the claim counter, padded; zeroed before every launch.
