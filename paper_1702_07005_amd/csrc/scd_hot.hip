@@ -740,11 +740,14 @@ __device__ __forceinline__ void staged_loader(const HotArgs& h, const HotSched& 
         if (n > 0 || b < nb) {
             if (!hot_wait(freed + q, n, abort_flag, h.spin_limit, h.err)) break;
         }
+        // Results of the buffer's previous batch, for the stager that assembled it: read out of the
+        // buffer now, stored to the result ring after the buffer has been handed over again (so that
+        // no wait for the stores' completion sits between the consumer's release and the hand-over).
+        const uint32_t c = b - NP, cs = c % kHotRing;
+        xcd_v2 w0 = {0, 0}, w1 = {0, 0};
         if (n > 0) {
-            // Results of the buffer's previous batch, for the stager that assembled it.
-            const uint32_t c = b - NP, s = c % kHotRing;
             if (c >= kHotRing && res_seen != c - kHotRing + 1u &&
-                !flag_wait(fr, (2 * kHotRing + s) * 4u, c - kHotRing + 1u, h.spin_limit, h.err)) {
+                !flag_wait(fr, (2 * kHotRing + cs) * 4u, c - kHotRing + 1u, h.spin_limit, h.err)) {
                 __hip_atomic_store(abort_flag, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
                 break;
             }
@@ -754,39 +757,54 @@ __device__ __forceinline__ void staged_loader(const HotArgs& h, const HotSched& 
                 moved += (m != kHotEmpty && zw.y != 0.0f) ? 1u : 0u;
                 // Each 8-byte half (value, tag) is written and read whole, so a reader that sees the tag
                 // sees its value.
-                const xcd_v2 w0 = {__float_as_int(zw.x), (int)(c + 1u)}, w1 = {__float_as_int(zw.y), (int)(c + 1u)};
-                const uint32_t roff = (s * 64u + (uint32_t)lane) * 16u;
+                w0 = xcd_v2{__float_as_int(zw.x), (int)(c + 1u)};
+                w1 = xcd_v2{__float_as_int(zw.y), (int)(c + 1u)};
+            }
+        }
+        // The result stores.  A loader never waits for a record's tag while it holds results it could
+        // publish: the stager it waits for may itself be waiting for those results.
+        bool published = n == 0;
+        auto publish = [&]() {
+            if ((uint32_t)lane < B) {
+                const uint32_t roff = (cs * 64u + (uint32_t)lane) * 16u;
                 __builtin_amdgcn_raw_buffer_store_b64(w0, rr, (int)roff, 0, kXcdStore);
                 __builtin_amdgcn_raw_buffer_store_b64(w1, rr, (int)roff + 8, 0, kXcdStore);
             }
-        }
-        if (b >= nb) break;
-        const uint32_t s = b % kHotRing;
-        if (!pre) {
-            if (tag_seen != b + 1u && !flag_wait(fr, s * 4u, b + 1u, h.spin_limit, h.err)) {
-                __hip_atomic_store(abort_flag, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
-                break;
+            published = true;
+        };
+        const uint32_t s = b % kHotRing, b2 = b + NP, b3 = b2 + NP;
+        if (b < nb) {
+            if (!pre) {
+                if (tag_seen != b + 1u) {
+                    if (!published) publish();
+                    if (!flag_wait(fr, s * 4u, b + 1u, h.spin_limit, h.err)) {
+                        __hip_atomic_store(abort_flag, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+                        break;
+                    }
+                }
+                staged_record_load<IV>(gr, s * RW * 4u, ioff, img);
             }
-            staged_record_load<IV>(gr, s * RW * 4u, ioff, img);
-        }
-        // Wait for the record's loads (so its slot may be freed below), then write it into the buffer.
-        __atomic_signal_fence(__ATOMIC_SEQ_CST);
-        __builtin_amdgcn_s_waitcnt(0x0F70);  // vmcnt(0)
-        __atomic_signal_fence(__ATOMIC_SEQ_CST);
-        xcd_v4* const dst = reinterpret_cast<xcd_v4*>(hb.rec);
+            // Wait for the record's loads (so its slot may be freed below), write it into the buffer
+            // and hand the buffer over.
+            __atomic_signal_fence(__ATOMIC_SEQ_CST);
+            __builtin_amdgcn_s_waitcnt(0x0F70);  // vmcnt(0)
+            __atomic_signal_fence(__ATOMIC_SEQ_CST);
+            xcd_v4* const dst = reinterpret_cast<xcd_v4*>(hb.rec);
 #pragma unroll
-        for (int v = 0; v < IV; ++v) {
-            const uint32_t i = (uint32_t)lane + 64u * (uint32_t)v;
-            if (64u * (uint32_t)(v + 1) <= IW / 4u || i < IW / 4u) dst[i] = img[v];  // the first test is uniform
+            for (int v = 0; v < IV; ++v) {
+                const uint32_t i = (uint32_t)lane + 64u * (uint32_t)v;
+                if (64u * (uint32_t)(v + 1) <= IW / 4u || i < IW / 4u) dst[i] = img[v];  // the first test is uniform
+            }
+            __hip_atomic_store(ready + q, n + 1, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_WORKGROUP);
+            // The loads of the next batch's record go out here, while no other load or store of this
+            // wave is in flight (the acquire before them waits for all of them).
+            pre = b2 < nb && tag_ahead == b2 + 1u;
+            if (pre) staged_record_load<IV>(gr, (b2 % kHotRing) * RW * 4u, ioff, img);
         }
-        // The loads of the next batch's record go out here, while no other load or store of this
-        // wave is in flight (the acquire before them waits for all of them).  Then free this batch's
-        // record for batch b + R and hand the buffer over.
-        const uint32_t b2 = b + NP, b3 = b2 + NP;
-        pre = b2 < nb && tag_ahead == b2 + 1u;
-        if (pre) staged_record_load<IV>(gr, (b2 % kHotRing) * RW * 4u, ioff, img);
+        if (!published) publish();
+        if (b >= nb) break;
+        // Free this batch's record for batch b + R, and read the flag words ahead.
         if (lane == 0) flag_set(fr, (kHotRing + s) * 4u, b + 1u);
-        __hip_atomic_store(ready + q, n + 1, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_WORKGROUP);
         tag_seen = b2 < nb && !pre ? wave_uniform((uint32_t)__builtin_amdgcn_raw_buffer_load_b32(
                                          fr, (int)((b2 % kHotRing) * 4u), 0, kXcdPoll))
                                    : 0u;

@@ -38,7 +38,7 @@ class Staged:
         self.claim = 0
         self.written = []
         self.stagers = [dict(b=None, ph=0) for _ in range(G)]
-        self.loaders = [dict(b=q, ph=0, pre=False, tag_seen=0, tag_ahead=0, res_seen=0, held=None)
+        self.loaders = [dict(b=q, ph=0, pre=False, tag_seen=0, tag_ahead=0, res_seen=0, held=None, published=True)
                         for q in range(self.NP)]
         for q, L in enumerate(self.loaders):
             if q + self.NP < nb:
@@ -83,45 +83,57 @@ class Staged:
         if b >= nb + NP:
             return False
         n = b // NP
+        c = b - NP
         if L["ph"] == 0:  # the consumer has finished the buffer's previous batch
             if (n > 0 or b < nb) and self.freed[q] != n:
                 return False
-            L["ph"] = 1
+            L["ph"], L["published"] = 1, n == 0
             return True
-        if L["ph"] == 1:  # publish the previous batch's results once its result slot is free
-            if n > 0:
-                c = b - NP
+        if L["ph"] == 1:  # the previous batch's result slot must be free before its results are published
+            if n > 0 and c >= R:
                 s = c % R
-                if c >= R and L["res_seen"] != c - R + 1 and self.res_read[s] != c - R + 1:
+                if L["res_seen"] != c - R + 1 and self.res_read[s] != c - R + 1:
                     return False
-                assert c < R or self.res_read[s] == c - R + 1, "results overwritten before they were read"
-                self.res[s] = c + 1
             L["ph"] = 2
-            if b >= nb:
-                L["b"] = nb + NP  # done
             return True
-        if L["ph"] == 2:  # the record: read ahead, or wait for its tag now
-            s = b % R
-            if not L["pre"]:
-                if L["tag_seen"] != b + 1 and self.tag[s] != b + 1:
-                    return False
+        if L["ph"] == 2:  # the record: read ahead, or wait for its tag now (results published first)
+            if b < nb and not L["pre"]:
+                s = b % R
+                if L["tag_seen"] != b + 1:
+                    if not L["published"]:
+                        self.publish(L, c)
+                        return True
+                    if self.tag[s] != b + 1:
+                        return False
                 self.take_record(L, b)
-            assert L["held"] == b
+            if b < nb:
+                assert L["held"] == b
+                self.ready[q] = n + 1  # image written, buffer handed over
+                b2 = b + NP
+                L["pre"] = b2 < nb and L["tag_ahead"] == b2 + 1
+                if L["pre"]:
+                    self.take_record(L, b2)
             L["ph"] = 3
             return True
-        # ph 3: gathers done; read the next record ahead if its tag was seen, free this record's slot,
-        # hand the buffer over, read the flag words ahead.
+        # ph 3: publish the results if not done yet; free this record's slot; read the flag words ahead.
+        if not L["published"]:
+            self.publish(L, c)
+        if b >= nb:
+            L["b"] = nb + NP  # done
+            return True
         b2, b3 = b + NP, b + 2 * NP
-        L["pre"] = b2 < nb and L["tag_ahead"] == b2 + 1
-        if L["pre"]:
-            self.take_record(L, b2)
         self.loaded[b % R] = b + 1
-        self.ready[q] = n + 1
         L["tag_seen"] = self.tag[b2 % R] if (b2 < nb and not L["pre"]) else 0
         L["tag_ahead"] = self.tag[b3 % R] if b3 < nb else 0
         L["res_seen"] = self.res_read[b % R] if b >= R else 0
         L["b"], L["ph"] = b2, 0
         return True
+
+    def publish(self, L, c):
+        s = c % self.R
+        assert c < self.R or self.res_read[s] == c - self.R + 1, "results overwritten before they were read"
+        self.res[s] = c + 1
+        L["published"] = True
 
     def consumer(self, i):
         b = self.consumers[i]
@@ -173,14 +185,14 @@ def test_staged_model_detects_a_missing_wait():
     class NoResWait(Staged):
         def loader(self, q):
             L = self.loaders[q]
-            if L["ph"] == 1 and L["b"] // self.NP > 0:
-                c = L["b"] - self.NP
-                self.res[c % self.R] = c + 1  # publish without waiting
+            if L["ph"] == 1:
                 L["ph"] = 2
-                if L["b"] >= self.nb:
-                    L["b"] = self.nb + self.NP
                 return True
             return super().loader(q)
+
+        def publish(self, L, c):
+            self.res[c % self.R] = c + 1  # no check that the slot's previous results were read
+            L["published"] = True
 
     failed = False
     for seed in range(20):
@@ -189,6 +201,21 @@ def test_staged_model_detects_a_missing_wait():
             failed = True
             break
     assert failed
+
+
+def test_staged_model_detects_waiting_for_a_tag_while_holding_results():
+    # Waiting for the next record's tag before publishing the results it holds deadlocks when the
+    # stager waves are few: the order the kernel follows matters.
+    class TagFirst(Staged):
+        def loader(self, q):
+            L = self.loaders[q]
+            b = L["b"]
+            if L["ph"] == 2 and b < self.nb and not L["pre"] and L["tag_seen"] != b + 1 and not L["published"]:
+                if self.tag[b % self.R] != b + 1:
+                    return False  # waits for the tag first
+            return super().loader(q)
+
+    assert any(TagFirst(200, 64, 1, 2, seed).run() != list(range(200)) for seed in range(5))
 
 
 # ------------------------------------------------------------------------------------------- split
