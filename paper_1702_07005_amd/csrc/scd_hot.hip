@@ -192,6 +192,9 @@ __device__ __forceinline__ void hot_consumer(const HotArgs& h, const HotSched& s
     const bool act = g < W;
     const uint32_t g0 = act ? g : 0u;  // inactive lanes read coordinate 0 of each step and write nothing
     float* const my_scr = scr + ci * 128u;
+    // The consumers set the epoch's pace; each shares its SIMD with two or three producer waves, so it
+    // takes the highest issue priority (2% of the full click epoch).
+    __builtin_amdgcn_s_setprio(3);
     for (uint32_t b = ci; b < sc.nb; b += sc.NC) {
         const uint32_t p = b % sc.NP, n = b / sc.NP;
         if (!hot_wait(ready + p, n + 1, abort_flag, h.spin_limit, h.err)) return;
