@@ -380,7 +380,7 @@ int plan_epoch(const scd_solver* h, LaunchPlan* lp, uint32_t* n_groups) {
         lp->blocks = 1;
         lp->lds_bytes = staged ? staged_lds_bytes(hg.hot_bytes, hg.cap, hg.Smax) : hg.lds;
         // Coordinates in flight at most: what the consumers hold when the window adapts.
-        *n_groups = hg.adaptive ? hg.NC * kHotMaxGroups : hg.W;
+        *n_groups = hg.adaptive ? (uint32_t)kHotMaxWindow : hg.W;
         return SCD_OK;
     }
     if (G == kBlockThreads) {

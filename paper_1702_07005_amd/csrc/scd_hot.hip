@@ -15,9 +15,9 @@ namespace scd {
 // back at the end), so their gathers and atomic adds stay inside the CU and are seen at once
 // by the other in-flight coordinates, which all run in the same workgroup.
 //
-// Waves 0..NC-1 (the consumers, NC = 1 or 2) run the in-flight coordinates, 8 lanes each and at
+// Waves 0..NC-1 (the consumers, NC = 1 to 4) run the in-flight coordinates, 8 lanes each and at
 // most kHotMaxGroups per wave, and read nothing but LDS; batch b goes to consumer b mod NC, and
-// each consumer steps through its batches independently of the other (their hot-entry updates
+// each consumer steps through its batches independently of the others (their hot-entry updates
 // meet in LDS atomics).  The other NP = kHotWaves - NC waves (producers) fill per-producer LDS
 // buffers with the next batches of permutation positions: each coordinate's metadata and, per
 // stored entry, its value and either its hot slot or (cold entry) its index and current
@@ -421,18 +421,19 @@ __global__ __launch_bounds__(64 * kHotWaves) void k_epoch_hot(HotArgs h) {
     float* const scr = reinterpret_cast<float*>(hot_lds + h.hot_bytes + kHotFlagBytes);
     uint32_t* const bufs = reinterpret_cast<uint32_t*>(hot_lds + h.hot_bytes + kHotFlagBytes + kHotScratchBytes);
     static_assert((2 * kHotMaxProducers + 2) * sizeof(uint32_t) <= kHotFlagBytes, "handover words exceed their area");
-    static_assert((kHotWaves - kHotMaxConsumers) % kHotMaxConsumers == 0, "a buffer's batches must share a consumer");
+    static_assert((kHotWaves - 3) % 3 == 0 && (kHotWaves - 4) % 4 == 0 && (kHotWaves - 2) % 2 == 0,
+                  "a buffer's batches must share a consumer");
     U* const uu = static_cast<U*>(a.u);
     const int tid = threadIdx.x, wave = (int)wave_uniform((uint32_t)tid >> 6), lane = tid & 63;
-    // This launch's window: fixed, or set by the previous launch of the adaptive plan (and then split
-    // evenly between the consumers where that is faster).
-    uint32_t W = h.W;
+    // This launch's window: fixed, or set by the previous launch of the adaptive plan (and then run by
+    // the consumer count and equal shares that hold the most of it per unit of step time).
+    uint32_t W = h.W, NC = h.NC;
     if (h.adapt_in) {
         const uint32_t v = __hip_atomic_load(h.adapt_in, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-        if (v >= h.NC && v <= h.NC * (uint32_t)kHotMaxGroups) W = v;
+        if (v >= 2 && v <= (uint32_t)kHotMaxWindow) W = v;
     }
-    if (h.adapt_out) W = hot_balanced_window(W, h.NC, h.cap);
-    const HotSched sc = hot_sched(W, h.NC, h.cap, h.pos_n);
+    if (h.adapt_out) W = hot_adaptive_share(W, &NC) * NC;
+    const HotSched sc = hot_sched(W, NC, h.cap, h.pos_n);
     for (uint32_t i = tid; i < h.n_hot + kHotZeroCells; i += blockDim.x) hot[i] = i < h.n_hot ? uu[h.hot_ids[i]] : U(0);
     if (tid < 2 * kHotMaxProducers + 2) ready[tid] = 0u;  // ready, freed, abort and moved are contiguous
     __syncthreads();
@@ -447,7 +448,7 @@ __global__ __launch_bounds__(64 * kHotWaves) void k_epoch_hot(HotArgs h) {
     // moving, i.e. W = 1 + (w_rule - 1) / f, at most what the consumers hold.  A launch that gave up
     // keeps the window.
     if (h.adapt_out && tid == 0 && *abort_flag == 0u) {
-        const uint64_t mv = *moved, wmax = (uint64_t)h.NC * kHotMaxGroups;
+        const uint64_t mv = *moved, wmax = kHotMaxWindow;
         uint64_t w = mv ? 1 + (uint64_t)(h.w_rule - 1) * h.pos_n / mv : wmax;
         w = w < h.w_rule ? h.w_rule : w > wmax ? wmax : w;
         __hip_atomic_store(h.adapt_out, (uint32_t)w, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
@@ -826,13 +827,13 @@ template <int FORM, typename U, int SL>
 __global__ __launch_bounds__(64 * kHotWaves) void k_epoch_staged(HotArgs h) {
     extern __shared__ __align__(16) unsigned char hot_lds[];
     const EpochArgs& a = h.e;
-    uint32_t W = h.W;
+    uint32_t W = h.W, NC = h.NC;
     if (h.adapt_in) {
         const uint32_t v = __hip_atomic_load(h.adapt_in, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-        if (v >= h.NC && v <= h.NC * (uint32_t)kHotMaxGroups) W = v;
+        if (v >= 2 && v <= (uint32_t)kHotMaxWindow) W = v;
     }
-    if (h.adapt_out) W = hot_balanced_window(W, h.NC, h.cap);
-    const HotSched sc = hot_sched(W, h.NC, h.cap, h.pos_n);
+    if (h.adapt_out) W = hot_adaptive_share(W, &NC) * NC;
+    const HotSched sc = hot_sched(W, NC, h.cap, h.pos_n);
     if (blockIdx.x > 0) {
         if (blockIdx.x % kHotXcds == 0 && blockIdx.x / kHotXcds <= h.stagers)
             staged_stager<FORM, U>(h, sc, reinterpret_cast<uint32_t*>(hot_lds));
@@ -863,7 +864,7 @@ __global__ __launch_bounds__(64 * kHotWaves) void k_epoch_staged(HotArgs h) {
     __syncthreads();
     for (uint32_t i = tid; i < h.n_hot; i += blockDim.x) uu[h.hot_ids[i]] = hot[i];
     if (h.adapt_out && tid == 0 && *abort_flag == 0u) {
-        const uint64_t mv = *moved, wmax = (uint64_t)h.NC * kHotMaxGroups;
+        const uint64_t mv = *moved, wmax = kHotMaxWindow;
         uint64_t w = mv ? 1 + (uint64_t)(h.w_rule - 1) * h.pos_n / mv : wmax;
         w = w < h.w_rule ? h.w_rule : w > wmax ? wmax : w;
         __hip_atomic_store(h.adapt_out, (uint32_t)w, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);

@@ -105,18 +105,20 @@ struct ObjArgs {
 };
 
 // Hot-set epoch (one workgroup of kHotWaves waves): the n_hot most-updated shared-vector entries live
-// in LDS for the epoch; one or two consumer waves run the in-flight coordinates from LDS only (each
+// in LDS for the epoch; one to four consumer waves run the in-flight coordinates from LDS only (each
 // up to kHotMaxGroups of them, 8 lanes each), and the other waves stream the next batches (segment,
-// hot slot or cold value) into LDS buffers, one buffer per producer.
+// hot slot or cold value) into LDS buffers, one buffer per producer.  kHotWaves - NC is a multiple
+// of NC for every consumer count NC used (11, 10, 9, 8 for NC = 1..4), so the batches of one buffer
+// all go to one consumer.
 constexpr int kHotWaves = 12;
-constexpr int kHotMaxConsumers = 2;
+constexpr int kHotMaxConsumers = 4;
 constexpr int kHotMaxProducers = kHotWaves - 1;  // with one consumer
 constexpr int kHotEntriesPerLane = 10;  // producer lanes x this >= batch entries (64 x 10 = 640)
 constexpr int kHotFlagBytes = 128;      // LDS words: ready[producer], freed[producer], abort, moved count
 constexpr int kHotScratchBytes = kHotMaxConsumers * 64 * 8;  // write targets of inactive consumer lanes
 constexpr int kHotZeroCells = 64;         // hot-array cells after the hot set, one per consumer lane
 constexpr int kHotMaxGroups = 8;          // coordinates per consumer step (groups of 8 lanes)
-constexpr int kHotMaxWindow = kHotMaxConsumers * kHotMaxGroups;
+constexpr int kHotMaxWindow = 2 * kHotMaxGroups;  // coordinates in flight at most
 // The first adaptive epoch runs its first 1/kHotOpening of the positions at the coupling rule's window.
 constexpr uint32_t kHotOpening = 16;
 constexpr int kHotMaxSegment = 64;
@@ -195,7 +197,7 @@ __host__ __device__ inline HotSched hot_sched(uint32_t W, uint32_t NC, uint32_t 
     s.NC = NC;
     s.NP = (uint32_t)kHotWaves - NC;
     s.w0 = (W + NC - 1) / NC;
-    s.w1 = NC > 1 ? W - s.w0 : s.w0;
+    s.w1 = NC > 2 ? s.w0 : NC > 1 ? W - s.w0 : s.w0;  // three or four consumers: equal shares (W = NC w0)
     s.B0 = cap / s.w0 * s.w0;
     s.B1 = cap / s.w1 * s.w1;
     if (NC == 1) {
@@ -207,22 +209,30 @@ __host__ __device__ inline HotSched hot_sched(uint32_t W, uint32_t NC, uint32_t 
     return s;
 }
 
-// An adaptive window that two consumers would split unevenly (odd W: w0 = w1 + 1) can leave the
-// consumer with the smaller share more steps per batch than the other (W = 11: batches of 12 rows
-// in 2 steps and of 15 rows in 3), and that consumer then sets the pace.  Such a window runs one
-// coordinate narrower when the even split moves more rows per step of the slower consumer (W = 11:
-// 10 as 5 + 5, batches of 15 rows in 3 steps each; likewise 9 -> 8 and 5 -> 4; 7, 13 and 15 stay).
-// A narrower window is within the coupling budget by construction.
-__host__ __device__ inline uint32_t hot_balanced_window(uint32_t W, uint32_t NC, uint32_t cap) {
-    if (NC != 2 || (W & 1u) == 0 || W < 5) return W;
-    const HotSched a = hot_sched(W, NC, cap, 0), b = hot_sched(W - 1, NC, cap, 0);
-    const uint32_t a0 = a.B0 / a.w0, a1 = a.B1 / a.w1, b0 = b.B0 / b.w0, b1 = b.B1 / b.w1;
-    const uint32_t sa = a0 > a1 ? a0 : a1, sb = b0 > b1 ? b0 : b1;  // steps per batch of the slower consumer
-    // rows per step of the slower consumer: (B0 + B1) / max steps, compared without division
-    return (uint64_t)(b.B0 + b.B1) * sa > (uint64_t)(a.B0 + a.B1) * sb ? W - 1 : W;
+// The consumer waves (up to kHotMaxConsumers) and the equal number w of coordinates each runs per
+// step for an adaptive window of W: the split with at most W in flight that moves the most
+// coordinates per unit of step time.  A step's time grows with the coordinates it holds (its LDS
+// gathers and atomics meet more bank and address conflicts): about 9 + w units, fitted to full-size
+// click epochs at fixed windows (4 consumers of 4 coordinates: 0.83 s, 2 of 8: 0.95 s; 4 of 3:
+// 0.99 s, 2 of 6: 1.25 s; 3 of 3: 1.29 s, 2 of 5: 1.30 s).  Shares below 2 are not used.  The
+// resulting splits: W = 16 as 4 x 4, 15 as 3 x 5, 12-14 as 4 x 3, 9-11 as 3 x 3, 8 as 4 x 2, 6-7 as
+// 3 x 2, 4-5 as 2 x 2.  A narrower window is within the coupling budget by construction.
+__host__ __device__ inline uint32_t hot_adaptive_share(uint32_t W, uint32_t* NC) {
+    uint32_t best_n = 1, best_w = W < (uint32_t)kHotMaxGroups ? W : (uint32_t)kHotMaxGroups;
+    for (uint32_t n = 2; n <= (uint32_t)kHotMaxConsumers; ++n) {
+        uint32_t w = W / n;
+        if (w > (uint32_t)kHotMaxGroups) w = kHotMaxGroups;
+        if (w < 2) break;
+        if ((uint64_t)n * w * (9 + best_w) > (uint64_t)best_n * best_w * (9 + w)) {
+            best_n = n;
+            best_w = w;
+        }
+    }
+    *NC = best_n;
+    return best_w;
 }
 
-__host__ __device__ inline uint32_t hot_consumer_of(const HotSched& s, uint32_t b) { return s.NC == 1 ? 0u : (b & 1u); }
+__host__ __device__ inline uint32_t hot_consumer_of(const HotSched& s, uint32_t b) { return b % s.NC; }
 __host__ __device__ inline uint32_t hot_groups(const HotSched& s, uint32_t c) { return c ? s.w1 : s.w0; }
 __host__ __device__ inline uint32_t hot_batch(const HotSched& s, uint32_t c) { return c ? s.B1 : s.B0; }
 
