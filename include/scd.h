@@ -268,9 +268,8 @@ int scd_set_state(scd_handle_t h, const float *model_dev, const float *shared_de
  *                 and its bounded waits then report SCD_ERR_HIP.
  *   "adapt"       1 (default) = when the window is automatic and the hot-set kernel runs the epoch,
  *                 each epoch's window follows the fraction f of coordinates whose step was nonzero
- *                 in the previous epoch: W = 1 + (auto_window - 1) / f, at most 16, run by 2 to 4
- *                 consumer waves with equal shares (16 as 4 x 4, 15 as 3 x 5, 12-14 as 4 x 3, 9-11
- *                 as 3 x 3, 8 as 4 x 2, 6-7 as 3 x 2, 4-5 as 2 x 2).  A coordinate
+ *                 in the previous epoch: W = 1 + (auto_window - 1) / f, at most 16, run by
+ *                 min(4, W / 2) consumer waves whose shares differ by at most one.  A coordinate
  *                 whose step is zero (in the hinge SVM dual, one whose alpha stays at a bound of
  *                 the box) changes nothing that others read, so the coupling rule's budget holds
  *                 for the coordinates in flight that move.  The window is kept in device memory,

@@ -426,13 +426,13 @@ __global__ __launch_bounds__(64 * kHotWaves) void k_epoch_hot(HotArgs h) {
     U* const uu = static_cast<U*>(a.u);
     const int tid = threadIdx.x, wave = (int)wave_uniform((uint32_t)tid >> 6), lane = tid & 63;
     // This launch's window: fixed, or set by the previous launch of the adaptive plan (and then run by
-    // the consumer count and equal shares that hold the most of it per unit of step time).
+    // as many consumers as keep two coordinates each per step, up to four).
     uint32_t W = h.W, NC = h.NC;
     if (h.adapt_in) {
         const uint32_t v = __hip_atomic_load(h.adapt_in, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
         if (v >= 2 && v <= (uint32_t)kHotMaxWindow) W = v;
     }
-    if (h.adapt_out) W = hot_adaptive_share(W, &NC) * NC;
+    if (h.adapt_out) NC = hot_adaptive_consumers(W);
     const HotSched sc = hot_sched(W, NC, h.cap, h.pos_n);
     for (uint32_t i = tid; i < h.n_hot + kHotZeroCells; i += blockDim.x) hot[i] = i < h.n_hot ? uu[h.hot_ids[i]] : U(0);
     if (tid < 2 * kHotMaxProducers + 2) ready[tid] = 0u;  // ready, freed, abort and moved are contiguous
@@ -832,7 +832,7 @@ __global__ __launch_bounds__(64 * kHotWaves) void k_epoch_staged(HotArgs h) {
         const uint32_t v = __hip_atomic_load(h.adapt_in, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
         if (v >= 2 && v <= (uint32_t)kHotMaxWindow) W = v;
     }
-    if (h.adapt_out) W = hot_adaptive_share(W, &NC) * NC;
+    if (h.adapt_out) NC = hot_adaptive_consumers(W);
     const HotSched sc = hot_sched(W, NC, h.cap, h.pos_n);
     if (blockIdx.x > 0) {
         if (blockIdx.x % kHotXcds == 0 && blockIdx.x / kHotXcds <= h.stagers)

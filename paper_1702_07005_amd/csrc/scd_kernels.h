@@ -182,67 +182,63 @@ struct HotArgs {
     int* err;
 };
 
-// Coordinates per batch and consumer steps of a hot-set epoch with W coordinates in flight: consumer
-// c runs w_c coordinates per step (w0 = ceil(W / NC), w1 = the rest), on every NC-th batch (batch b
-// goes to consumer b mod NC), batches of B_c = cap / w_c * w_c coordinates.  Scalar fields only: the
-// kernels select between them, which keeps the struct in registers.
+// Coordinates per batch and consumer steps of a hot-set epoch with W coordinates in flight on NC
+// consumer waves: consumer c runs w_c coordinates per step, the first n_hi consumers w_hi =
+// ceil(W / NC) and the rest w_lo = floor(W / NC), so that the shares sum to W; batch b goes to
+// consumer b mod NC and holds S w_c coordinates, S = cap / w_hi steps for every consumer.  Equal step
+// counts keep the consumers in step with one another (the batches go round them in turn), so the
+// epoch runs W coordinates per step time.  Scalar fields only: the kernels select between them,
+// which keeps the struct in registers.
 struct HotSched {
-    uint32_t NC, NP;  // consumer and producer waves
-    uint32_t w0, w1, B0, B1;
-    uint32_t nb;      // batches in the epoch
+    uint32_t NC, NP;   // consumer and producer waves
+    uint32_t W;        // coordinates in flight
+    uint32_t w_hi, w_lo, n_hi;
+    uint32_t S;        // steps per batch
+    uint32_t nb;       // batches in the launch
 };
+
+__host__ __device__ inline uint32_t hot_groups(const HotSched& s, uint32_t c) { return c < s.n_hi ? s.w_hi : s.w_lo; }
+__host__ __device__ inline uint32_t hot_batch(const HotSched& s, uint32_t c) { return s.S * hot_groups(s, c); }
+__host__ __device__ inline uint32_t hot_consumer_of(const HotSched& s, uint32_t b) { return b % s.NC; }
 
 __host__ __device__ inline HotSched hot_sched(uint32_t W, uint32_t NC, uint32_t cap, uint32_t n) {
     HotSched s{};
     s.NC = NC;
     s.NP = (uint32_t)kHotWaves - NC;
-    s.w0 = (W + NC - 1) / NC;
-    s.w1 = NC > 2 ? s.w0 : NC > 1 ? W - s.w0 : s.w0;  // three or four consumers: equal shares (W = NC w0)
-    s.B0 = cap / s.w0 * s.w0;
-    s.B1 = cap / s.w1 * s.w1;
-    if (NC == 1) {
-        s.nb = (n + s.B0 - 1) / s.B0;
-    } else {
-        const uint32_t pair = s.B0 + s.B1, q = n / pair, rem = n - q * pair;
-        s.nb = 2 * q + (rem == 0 ? 0 : rem > s.B0 ? 2 : 1);
+    s.W = W;
+    s.w_lo = W / NC;
+    s.n_hi = W - s.w_lo * NC;
+    s.w_hi = s.w_lo + (s.n_hi ? 1u : 0u);
+    s.S = cap / s.w_hi;
+    const uint32_t round = s.S * W, q = n / round;  // a round: one batch for each consumer
+    uint32_t rem = n - q * round, nb = q * NC;
+    for (uint32_t c = 0; c < NC && rem > 0; ++c) {
+        const uint32_t B = hot_batch(s, c);
+        rem = rem > B ? rem - B : 0u;
+        ++nb;
     }
+    s.nb = nb;
     return s;
 }
 
-// The consumer waves (up to kHotMaxConsumers) and the equal number w of coordinates each runs per
-// step for an adaptive window of W: the split with at most W in flight that moves the most
-// coordinates per unit of step time.  A step's time grows with the coordinates it holds (its LDS
-// gathers and atomics meet more bank and address conflicts): about 9 + w units, fitted to full-size
-// click epochs at fixed windows (4 consumers of 4 coordinates: 0.83 s, 2 of 8: 0.95 s; 4 of 3:
-// 0.99 s, 2 of 6: 1.25 s; 3 of 3: 1.29 s, 2 of 5: 1.30 s).  Shares below 2 are not used.  The
-// resulting splits: W = 16 as 4 x 4, 15 as 3 x 5, 12-14 as 4 x 3, 9-11 as 3 x 3, 8 as 4 x 2, 6-7 as
-// 3 x 2, 4-5 as 2 x 2.  A narrower window is within the coupling budget by construction.
-__host__ __device__ inline uint32_t hot_adaptive_share(uint32_t W, uint32_t* NC) {
-    uint32_t best_n = 1, best_w = W < (uint32_t)kHotMaxGroups ? W : (uint32_t)kHotMaxGroups;
-    for (uint32_t n = 2; n <= (uint32_t)kHotMaxConsumers; ++n) {
-        uint32_t w = W / n;
-        if (w > (uint32_t)kHotMaxGroups) w = kHotMaxGroups;
-        if (w < 2) break;
-        if ((uint64_t)n * w * (9 + best_w) > (uint64_t)best_n * best_w * (9 + w)) {
-            best_n = n;
-            best_w = w;
-        }
-    }
-    *NC = best_n;
-    return best_w;
-}
-
-__host__ __device__ inline uint32_t hot_consumer_of(const HotSched& s, uint32_t b) { return b % s.NC; }
-__host__ __device__ inline uint32_t hot_groups(const HotSched& s, uint32_t c) { return c ? s.w1 : s.w0; }
-__host__ __device__ inline uint32_t hot_batch(const HotSched& s, uint32_t c) { return c ? s.B1 : s.B0; }
-
-// First permutation position of batch b, and its size.
+// First permutation position of batch b (within the launch's range), and its size.
 __host__ __device__ inline uint32_t hot_batch_start(const HotSched& s, uint32_t b) {
-    if (s.NC == 1) return b * s.B0;
-    return (b >> 1) * (s.B0 + s.B1) + ((b & 1u) ? s.B0 : 0u);
+    const uint32_t r = b % s.NC;
+    return (b / s.NC) * s.S * s.W + s.S * (r * s.w_lo + (r < s.n_hi ? r : s.n_hi));
 }
 __host__ __device__ inline uint32_t hot_batch_size(const HotSched& s, uint32_t b) {
     return hot_batch(s, hot_consumer_of(s, b));
+}
+
+// The consumer waves for an adaptive window of W: as many as keep at least two coordinates per
+// consumer step, up to kHotMaxConsumers.  A step takes about the same time whatever it holds (about
+// 600 cycles for 3 to 4 coordinates at full click size, its two LDS round trips and dependent
+// instructions dominating; 730 for 8), so the epoch's rate is the window over the step time, and
+// more, narrower consumers shorten the step: full-size click epochs at 16 in flight took 0.83 s on
+// four consumers of 4 and 0.95 s on two of 8.
+__host__ __device__ inline uint32_t hot_adaptive_consumers(uint32_t W) {
+    const uint32_t n = W / 2;
+    return n < 1 ? 1u : n > (uint32_t)kHotMaxConsumers ? (uint32_t)kHotMaxConsumers : n;
 }
 
 size_t hot_lds_bytes(uint32_t hot_bytes, uint32_t B, uint32_t Smax);
