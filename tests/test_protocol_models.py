@@ -5,7 +5,7 @@ interleavings of their waves (host only; no GPU).
   write each batch's results out; loader waves of the hot workgroup publish results, take records
   (read ahead when the tag was already seen) and hand buffers to the consumer waves.  The model
   follows the kernel's order of waits and flag writes and reads flag words ahead the way the loader
-  does.  Checked: no interleaving deadlocks (for 1 to 192 stager waves, one or two consumers, rings
+  does.  Checked: no interleaving deadlocks (for 1 to 192 stager waves, one to four consumers, rings
   of 2 to 64 records), every record a loader takes is its batch's, every result a stager reads is its
   batch's, and every batch is written out exactly once.
 * The split epoch: workgroups claim chunks of units in order and process them in order; a SCATTER
@@ -166,7 +166,7 @@ class Staged:
         return sorted(self.written)
 
 
-@pytest.mark.parametrize("NC", [1, 2])
+@pytest.mark.parametrize("NC", [1, 2, 3, 4])
 @pytest.mark.parametrize("R", [2, 5, 10, 64])
 @pytest.mark.parametrize("G", [1, 3, 192])
 def test_staged_protocol_completes_without_stale_records(NC, R, G):
