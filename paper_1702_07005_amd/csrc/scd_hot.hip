@@ -216,6 +216,84 @@ __device__ __forceinline__ void hot_consumer(const HotArgs& h, const HotSched& s
     }
 }
 
+// The same consumer with 16 lanes per coordinate, for consumers of at most 4 coordinates per step
+// (the adaptive plans with three or four consumers): 4 coordinates fill the wave, each lane holds
+// SL2 = ceil(Smax / 16) entry slots (slot sub + 16 r of its coordinate), so a step issues fewer LDS
+// gathers and atomics per lane and sums over 16 lanes.  The batch image is the one the 8-lane
+// consumer reads; a lane's slots past Smax read its own zero cell (hot array slot n_hot + lane).
+// Only the first lane of a coordinate writes its record back (the others write into `scr`).
+template <int SL2>
+__device__ __forceinline__ void hot_load_step16(HotStep<SL2>& t, const HotBuf& hb, uint32_t c, uint32_t Smax,
+                                                uint32_t sub, int32_t zkey) {
+    t.r = hb.rec[c];
+#pragma unroll
+    for (int r = 0; r < SL2; ++r) {
+        const uint32_t k = sub + 16u * (uint32_t)r;
+        const bool in = k < Smax;
+        const int2 p = hb.kv[c * Smax + (in ? k : 0u)];
+        t.kk[r] = in ? p.x : zkey;
+        t.vv[r] = in ? __int_as_float(p.y) : 0.0f;
+    }
+}
+
+template <int FORM, typename U, int SL2>
+__device__ __forceinline__ void hot_step16(const StepConsts& k, U* hot, const HotBuf& hb, float* scr, uint32_t Smax,
+                                           uint32_t cn, bool act, uint32_t sub, int lane, int32_t zkey,
+                                           const HotStep<SL2>& cur, uint32_t c, HotStep<SL2>& nxt) {
+    U hv[SL2];
+#pragma unroll
+    for (int r = 0; r < SL2; ++r) hv[r] = hot[cur.kk[r]];
+    __builtin_amdgcn_sched_barrier(0);
+    hot_load_step16<SL2>(nxt, hb, cn, Smax, sub, zkey);
+    __builtin_amdgcn_sched_barrier(0);
+    float acc = 0.0f;
+#pragma unroll
+    for (int r = 0; r < SL2; ++r) acc = fmaf(cur.vv[r], (float)hv[r], acc);
+    const float gsum = group_sum<16>(acc) + cur.r.w;
+    float coef;
+    const float m_new = hot_coord_step<FORM>(gsum, cur.r.x, cur.r.y, cur.r.z, k, &coef);
+    if (!act) coef = 0.0f;
+    *reinterpret_cast<float2*>(act && sub == 0 ? &hb.rec[c].z : scr + 2 * lane) = make_float2(m_new, coef);
+    if (coef != 0.0f) {
+#pragma unroll
+        for (int r = 0; r < SL2; ++r) atomicAdd(hot + cur.kk[r], (U)(coef * cur.vv[r]));
+    }
+}
+
+template <int FORM, typename U, int SL2>
+__device__ __forceinline__ void hot_consumer16(const HotArgs& h, const HotSched& sc, uint32_t ci, U* hot,
+                                               uint32_t* ready, uint32_t* freed, uint32_t* abort_flag, uint32_t* bufs,
+                                               float* scr, int lane) {
+    const StepConsts k = h.e.k;
+    const uint32_t Smax = h.Smax, W = hot_groups(sc, ci), B = hot_batch(sc, ci), bw = hot_buf_words(h.cap, Smax);
+    const uint32_t S = B / W;
+    const uint32_t g = (uint32_t)lane >> 4, sub = (uint32_t)lane & 15u;
+    const bool act = g < W;
+    const uint32_t g0 = act ? g : 0u;  // inactive lanes read coordinate 0 of each step and write nothing
+    const int32_t zkey = (int32_t)(h.n_hot + (uint32_t)lane);
+    float* const my_scr = scr + ci * 128u;
+    __builtin_amdgcn_s_setprio(3);  // as in hot_consumer
+    for (uint32_t b = ci; b < sc.nb; b += sc.NC) {
+        const uint32_t p = b % sc.NP, n = b / sc.NP;
+        if (!hot_wait(ready + p, n + 1, abort_flag, h.spin_limit, h.err)) return;
+        const HotBuf hb = hot_buf(bufs + p * bw, h.cap, Smax);
+        HotStep<SL2> sa, sb;
+        hot_load_step16<SL2>(sa, hb, g0, Smax, sub, zkey);
+        uint32_t st = 0;
+        for (; st + 1 < S; st += 2) {
+            const uint32_t c0 = st * W + g0, c1 = c0 + W;
+            const uint32_t c2 = st + 2 < S ? c1 + W : c1;
+            hot_step16<FORM, U, SL2>(k, hot, hb, my_scr, Smax, c1, act, sub, lane, zkey, sa, c0, sb);
+            hot_step16<FORM, U, SL2>(k, hot, hb, my_scr, Smax, c2, act, sub, lane, zkey, sb, c1, sa);
+        }
+        if (st < S) {
+            const uint32_t c0 = st * W + g0;
+            hot_step16<FORM, U, SL2>(k, hot, hb, my_scr, Smax, c0, act, sub, lane, zkey, sa, c0, sb);
+        }
+        __hip_atomic_store(freed + p, n + 1, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_WORKGROUP);
+    }
+}
+
 // A producer's view of one batch: lane c < B loads coordinate c's metadata.  The coordinate index
 // is computed first (arithmetic only) and the loads are issued later, so that they can be issued
 // behind the previous batch's entry loads.
@@ -438,7 +516,10 @@ __global__ __launch_bounds__(64 * kHotWaves) void k_epoch_hot(HotArgs h) {
     if (tid < 2 * kHotMaxProducers + 2) ready[tid] = 0u;  // ready, freed, abort and moved are contiguous
     __syncthreads();
     if ((uint32_t)wave < sc.NC) {
-        hot_consumer<FORM, U, SL>(h, sc, (uint32_t)wave, hot, ready, freed, abort_flag, bufs, scr, lane);
+        if (sc.w_hi <= 4)
+            hot_consumer16<FORM, U, (SL + 1) / 2>(h, sc, (uint32_t)wave, hot, ready, freed, abort_flag, bufs, scr, lane);
+        else
+            hot_consumer<FORM, U, SL>(h, sc, (uint32_t)wave, hot, ready, freed, abort_flag, bufs, scr, lane);
     } else {
         hot_producer<FORM, U>(h, sc, ready, freed, abort_flag, bufs, moved, wave - (int)sc.NC, lane);
     }
@@ -857,9 +938,12 @@ __global__ __launch_bounds__(64 * kHotWaves) void k_epoch_staged(HotArgs h) {
     for (uint32_t i = tid; i < h.n_hot + kHotZeroCells; i += blockDim.x) hot[i] = i < h.n_hot ? uu[h.hot_ids[i]] : U(0);
     if (tid < 2 * kHotMaxProducers + 2) ready[tid] = 0u;
     __syncthreads();
-    if ((uint32_t)wave < sc.NC)
-        hot_consumer<FORM, U, SL>(h, sc, (uint32_t)wave, hot, ready, freed, abort_flag, bufs, scr, lane);
-    else
+    if ((uint32_t)wave < sc.NC) {
+        if (sc.w_hi <= 4)
+            hot_consumer16<FORM, U, (SL + 1) / 2>(h, sc, (uint32_t)wave, hot, ready, freed, abort_flag, bufs, scr, lane);
+        else
+            hot_consumer<FORM, U, SL>(h, sc, (uint32_t)wave, hot, ready, freed, abort_flag, bufs, scr, lane);
+    } else
         staged_loader<FORM, U>(h, sc, ready, freed, abort_flag, bufs, moved, wave - (int)sc.NC, lane);
     __syncthreads();
     for (uint32_t i = tid; i < h.n_hot; i += blockDim.x) uu[h.hot_ids[i]] = hot[i];
