@@ -805,8 +805,11 @@ __device__ __forceinline__ void staged_loader(const HotArgs& h, const HotSched& 
     // is free, and the record tag of its batch after next.  If the tag of its next batch (read one
     // batch earlier) is already set, it also issues that batch's record loads into registers then.
     // A flag word that was read ahead and not yet set is read again when needed.  A flag, once set,
-    // stays set for the launch.
+    // stays set for the launch.  The words read ahead stay in vector registers until the consumer has
+    // released the buffer (`*_v`), so that the wait for their loads, which also waits for the record
+    // loads and result stores issued before them, falls after that release and not before it.
     uint32_t tag_seen = 0, tag_ahead = 0, res_seen = 0;
+    uint32_t tag_seen_v = 0, tag_ahead_v = 0, res_seen_v = 0;
     bool pre = false;  // img holds batch b's record, loaded ahead
     xcd_v4 img[IV];
     // Offsets within a record; out-of-range ones stay out of range once the record's base (below
@@ -818,13 +821,16 @@ __device__ __forceinline__ void staged_loader(const HotArgs& h, const HotSched& 
         ioff[v] = i < IW / 4u ? 16u * i : 0x7FF00000u;
     }
     if ((uint32_t)q + NP < nb)
-        tag_ahead = wave_uniform((uint32_t)__builtin_amdgcn_raw_buffer_load_b32(
-            fr, (int)((((uint32_t)q + NP) % kHotRing) * 4u), 0, kXcdPoll));
+        tag_ahead_v = (uint32_t)__builtin_amdgcn_raw_buffer_load_b32(
+            fr, (int)((((uint32_t)q + NP) % kHotRing) * 4u), 0, kXcdPoll);
     for (uint32_t b = (uint32_t)q; b < nb + NP; b += NP) {
         const uint32_t n = b / NP;
         if (n > 0 || b < nb) {
             if (!hot_wait(freed + q, n, abort_flag, h.spin_limit, h.err)) break;
         }
+        tag_seen = wave_uniform(tag_seen_v);
+        tag_ahead = wave_uniform(tag_ahead_v);
+        res_seen = wave_uniform(res_seen_v);
         // Results of the buffer's previous batch, for the stager that assembled it: read out of the
         // buffer now, stored to the result ring after the buffer has been handed over again (so that
         // no wait for the stores' completion sits between the consumer's release and the hand-over).
@@ -890,15 +896,15 @@ __device__ __forceinline__ void staged_loader(const HotArgs& h, const HotSched& 
         if (b >= nb) break;
         // Free this batch's record for batch b + R, and read the flag words ahead.
         if (lane == 0) flag_set(fr, (kHotRing + s) * 4u, b + 1u);
-        tag_seen = b2 < nb && !pre ? wave_uniform((uint32_t)__builtin_amdgcn_raw_buffer_load_b32(
-                                         fr, (int)((b2 % kHotRing) * 4u), 0, kXcdPoll))
+        tag_seen_v = b2 < nb && !pre ? (uint32_t)__builtin_amdgcn_raw_buffer_load_b32(
+                                           fr, (int)((b2 % kHotRing) * 4u), 0, kXcdPoll)
+                                     : 0u;
+        tag_ahead_v = b3 < nb ? (uint32_t)__builtin_amdgcn_raw_buffer_load_b32(
+                                    fr, (int)((b3 % kHotRing) * 4u), 0, kXcdPoll)
+                              : 0u;
+        res_seen_v = b >= kHotRing ? (uint32_t)__builtin_amdgcn_raw_buffer_load_b32(
+                                         fr, (int)((2 * kHotRing + s) * 4u), 0, kXcdPoll)
                                    : 0u;
-        tag_ahead = b3 < nb ? wave_uniform((uint32_t)__builtin_amdgcn_raw_buffer_load_b32(
-                                  fr, (int)((b3 % kHotRing) * 4u), 0, kXcdPoll))
-                            : 0u;
-        res_seen = b >= kHotRing ? wave_uniform((uint32_t)__builtin_amdgcn_raw_buffer_load_b32(
-                                       fr, (int)((2 * kHotRing + s) * 4u), 0, kXcdPoll))
-                                 : 0u;
     }
     for (int o = 32; o > 0; o >>= 1) moved += __shfl_xor(moved, o, 64);
     if (lane == 0) atomicAdd(moved_total, moved);
