@@ -159,7 +159,7 @@ __device__ __forceinline__ void hot_step(const StepConsts& k, U* hot, const HotB
 #pragma unroll
     for (int r = 0; r < SL; ++r) hv[r] = hot[cur.kk[r]];
     __builtin_amdgcn_sched_barrier(0);
-    hot_load_step<SL>(nxt, hb, cn, cn * Smax + sub);
+    hot_load_step<SL>(nxt, hb, cn, __umul24(cn, Smax) + sub);
     __builtin_amdgcn_sched_barrier(0);
     float acc = 0.0f;
 #pragma unroll
@@ -186,7 +186,10 @@ __device__ __forceinline__ void hot_consumer(const HotArgs& h, const HotSched& s
                                              uint32_t* ready, uint32_t* freed, uint32_t* abort_flag, uint32_t* bufs,
                                              float* scr, int lane) {
     const StepConsts k = h.e.k;
-    const uint32_t Smax = h.Smax, W = hot_groups(sc, ci), B = hot_batch(sc, ci), bw = hot_buf_words(h.cap, Smax);
+    // The instance for rows of Smax entries has SL = Smax / 8 (the host picks it so): Smax is a
+    // compile-time constant, so the slot range tests fold and the slot offsets need no 32-bit multiply.
+    constexpr uint32_t Smax = 8u * SL;
+    const uint32_t W = hot_groups(sc, ci), B = hot_batch(sc, ci), bw = hot_buf_words(h.cap, Smax);
     const uint32_t S = B / W;
     const uint32_t g = (uint32_t)lane >> 3, sub = (uint32_t)lane & 7u;
     const bool act = g < W;
@@ -230,7 +233,7 @@ __device__ __forceinline__ void hot_load_step16(HotStep<SL2>& t, const HotBuf& h
     for (int r = 0; r < SL2; ++r) {
         const uint32_t k = sub + 16u * (uint32_t)r;
         const bool in = k < Smax;
-        const int2 p = hb.kv[c * Smax + (in ? k : 0u)];
+        const int2 p = hb.kv[__umul24(c, Smax) + (in ? k : 0u)];
         t.kk[r] = in ? p.x : zkey;
         t.vv[r] = in ? __int_as_float(p.y) : 0.0f;
     }
@@ -260,12 +263,13 @@ __device__ __forceinline__ void hot_step16(const StepConsts& k, U* hot, const Ho
     }
 }
 
-template <int FORM, typename U, int SL2>
+template <int FORM, typename U, int SL2, int SL>
 __device__ __forceinline__ void hot_consumer16(const HotArgs& h, const HotSched& sc, uint32_t ci, U* hot,
                                                uint32_t* ready, uint32_t* freed, uint32_t* abort_flag, uint32_t* bufs,
                                                float* scr, int lane) {
     const StepConsts k = h.e.k;
-    const uint32_t Smax = h.Smax, W = hot_groups(sc, ci), B = hot_batch(sc, ci), bw = hot_buf_words(h.cap, Smax);
+    constexpr uint32_t Smax = 8u * SL;  // as in hot_consumer
+    const uint32_t W = hot_groups(sc, ci), B = hot_batch(sc, ci), bw = hot_buf_words(h.cap, Smax);
     const uint32_t S = B / W;
     const uint32_t g = (uint32_t)lane >> 4, sub = (uint32_t)lane & 15u;
     const bool act = g < W;
@@ -517,7 +521,7 @@ __global__ __launch_bounds__(64 * kHotWaves) void k_epoch_hot(HotArgs h) {
     __syncthreads();
     if ((uint32_t)wave < sc.NC) {
         if (sc.w_hi <= 4)
-            hot_consumer16<FORM, U, (SL + 1) / 2>(h, sc, (uint32_t)wave, hot, ready, freed, abort_flag, bufs, scr, lane);
+            hot_consumer16<FORM, U, (SL + 1) / 2, SL>(h, sc, (uint32_t)wave, hot, ready, freed, abort_flag, bufs, scr, lane);
         else
             hot_consumer<FORM, U, SL>(h, sc, (uint32_t)wave, hot, ready, freed, abort_flag, bufs, scr, lane);
     } else {
@@ -946,7 +950,7 @@ __global__ __launch_bounds__(64 * kHotWaves) void k_epoch_staged(HotArgs h) {
     __syncthreads();
     if ((uint32_t)wave < sc.NC) {
         if (sc.w_hi <= 4)
-            hot_consumer16<FORM, U, (SL + 1) / 2>(h, sc, (uint32_t)wave, hot, ready, freed, abort_flag, bufs, scr, lane);
+            hot_consumer16<FORM, U, (SL + 1) / 2, SL>(h, sc, (uint32_t)wave, hot, ready, freed, abort_flag, bufs, scr, lane);
         else
             hot_consumer<FORM, U, SL>(h, sc, (uint32_t)wave, hot, ready, freed, abort_flag, bufs, scr, lane);
     } else
@@ -978,6 +982,7 @@ static const void* hot_kernel_sl(uint32_t sl) {
 }
 
 static const void* hot_kernel(int form, bool wide, uint32_t Smax) {
+    if (Smax % 8 != 0) return nullptr;  // the consumers take Smax = 8 * SL
     const uint32_t sl = Smax / 8;
     switch (form) {
         case FORM_RIDGE_PRIMAL:
@@ -1012,6 +1017,7 @@ static const void* staged_kernel_sl(uint32_t sl) {
 }
 
 static const void* staged_kernel(int form, bool wide, uint32_t Smax) {
+    if (Smax % 8 != 0) return nullptr;  // as in hot_kernel
     const uint32_t sl = Smax / 8;
     switch (form) {
         case FORM_RIDGE_PRIMAL:
