@@ -215,7 +215,7 @@ bool hot_geometry(const scd_solver* h, int64_t W, HotGeom* g) {
     // A second consumer wave when the window may exceed what one consumer holds.
     g->NC = (g->adaptive || W > kHotMaxGroups) ? 2u : 1u;
     g->Smax = (uint32_t)std::max<int64_t>(8, (h->max_seg + 7) / 8 * 8);
-    g->cap = std::min<uint32_t>(64, 64u * kHotEntriesPerLane / g->Smax);
+    g->cap = hot_batch_cap(g->Smax, kHotEntriesPerLane);  // the staged plan's is larger (staged_cap)
     if (g->cap < (uint32_t)kHotMaxGroups) return false;
     g->hot_bytes = (uint32_t)(((size_t)(h->n_hot + kHotZeroCells) * (h->wide ? sizeof(double) : sizeof(float)) + 15) /
                               16 * 16);
@@ -223,10 +223,11 @@ bool hot_geometry(const scd_solver* h, int64_t W, HotGeom* g) {
     return true;
 }
 
-// Largest hot set that fits LDS next to the largest batch buffers (64 x kHotEntriesPerLane slots) as
+// Largest hot set that fits LDS next to the largest batch buffers (64 x kStagedEntriesPerLane slots, the
+// staged plan's, which exceed the single-workgroup plan's) as
 // fp64 entries, so that it stays valid at both widths of the shared vector.
 uint32_t hot_capacity(const scd_solver* h) {
-    const size_t worst = hot_lds_bytes(0, 64, kHotEntriesPerLane);
+    const size_t worst = hot_lds_bytes(0, 64, kStagedEntriesPerLane);
     if (h->max_lds <= worst + 16) return 0;
     const size_t cells = (h->max_lds - worst - 16) / sizeof(double);
     if (cells <= (size_t)kHotZeroCells) return 0;
@@ -256,6 +257,16 @@ int64_t pipe_groups(const scd_solver* h, int64_t window, int64_t groups) {
 bool staged_plan(const scd_solver* h) {
     if (h->staged == 0 || !h->ring || h->cus < 1 + kHotXcds * kHotStagers) return false;
     return h->staged == 2 || h->nnz * 8 > kStagedMinBytes;
+}
+
+// The staged plan's batches: kStagedEntriesPerLane slots per stager lane.  False if its LDS (the hot
+// workgroup's buffers, or the stagers' images) would not fit; the hot set is sized so that it does.
+bool staged_geometry(const scd_solver* h, HotGeom* g) {
+    const uint32_t cap = hot_batch_cap(g->Smax, kStagedEntriesPerLane);
+    if (cap < (uint32_t)kHotMaxGroups || staged_lds_bytes(g->hot_bytes, cap, g->Smax) > h->max_lds) return false;
+    g->cap = cap;
+    g->lds = hot_lds_bytes(g->hot_bytes, cap, g->Smax);
+    return true;
 }
 
 bool hot_plan(const scd_solver* h, int64_t window, HotGeom* g) {
@@ -374,11 +385,11 @@ int plan_epoch(const scd_solver* h, LaunchPlan* lp, uint32_t* n_groups) {
     }
     HotGeom hg;
     if (hot_plan(h, window, &hg)) {
-        const bool staged = staged_plan(h) && staged_lds_bytes(hg.hot_bytes, hg.cap, hg.Smax) <= h->max_lds;
+        const bool staged = staged_plan(h) && staged_geometry(h, &hg);
         lp->kind = staged ? PLAN_HOT_STAGED : PLAN_HOT;
         lp->group = 8;
         lp->blocks = 1;
-        lp->lds_bytes = staged ? staged_lds_bytes(hg.hot_bytes, hg.cap, hg.Smax) : hg.lds;
+        lp->lds_bytes = staged ? staged_lds_bytes(hg.hot_bytes, hg.cap, hg.Smax) : hg.lds;  // hg: staged_geometry's
         // Coordinates in flight at most: what the consumers hold when the window adapts.
         *n_groups = hg.adaptive ? (uint32_t)kHotMaxWindow : hg.W;
         return SCD_OK;
@@ -543,7 +554,7 @@ int build_hot_tables(scd_solver* h, hipStream_t s) {
             h->hot_cover = (double)sum / (double)h->nnz;
             // The staged variant's ring (a few hundred KB); without it only the single-workgroup kernel runs.
             const uint32_t Smax = (uint32_t)std::max<int64_t>(8, (h->max_seg + 7) / 8 * 8);
-            const uint32_t cap = std::min<uint32_t>(64, 64u * kHotEntriesPerLane / Smax);
+            const uint32_t cap = hot_batch_cap(Smax, kStagedEntriesPerLane);
             const size_t ring_bytes = sizeof(uint32_t) * (size_t)kHotRing * staged_rec_words(cap, Smax);
             if (hipMalloc(&h->ring, ring_bytes) != hipSuccess ||
                 hipMalloc(&h->ring_flags, sizeof(uint32_t) * kHotFlagWords) != hipSuccess ||
@@ -1034,6 +1045,7 @@ int scd_epochs(scd_handle_t h, uint64_t seed, int32_t n_epochs, void* stream) {
     HotGeom hg{};
     if (lp.kind == PLAN_HOT || lp.kind == PLAN_HOT_STAGED) {
         hot_plan(h, h->window ? h->window : h->auto_window, &hg);
+        if (lp.kind == PLAN_HOT_STAGED) staged_geometry(h, &hg);  // held when the plan was made
         hg.lds = lp.lds_bytes;  // the staged launch's workgroups all get the larger of the two needs
         if (lp.kind == PLAN_HOT)
             HIP_TRY(hot_prepare(h->form, h->wide != 0, hg.Smax, hg.lds));

@@ -639,7 +639,7 @@ __device__ void staged_stager(const HotArgs& h, const HotSched& sc, uint32_t* ld
     const __amdgpu_buffer_rsrc_t rr = xcd_rsrc(h.results, kHotResultWords * 8u);
     uint32_t* const claim = h.flags + 3 * kHotRing;
     U* const uu = static_cast<U*>(a.u);
-    constexpr int NE = kHotEntriesPerLane;
+    constexpr int NE = kStagedEntriesPerLane;
     const uint32_t c0 = (uint32_t)lane / Smax, k0 = (uint32_t)lane - c0 * Smax;
     const uint32_t dc = 64u / Smax, dk = 64u - dc * Smax;
     for (;;) {
@@ -769,7 +769,7 @@ __device__ void staged_stager(const HotArgs& h, const HotSched& sc, uint32_t* ld
     }
 }
 
-constexpr uint32_t kStagedImageVecs = (hot_buf_words(64, kHotEntriesPerLane) / 4 + 63) / 64;  // uint4 per lane, at most
+constexpr uint32_t kStagedImageVecs = (hot_buf_words(64, kStagedEntriesPerLane) / 4 + 63) / 64;  // uint4 per lane, at most
 
 // A loader's loads of one ring record (at byte offset rbase): the LDS image of its batch.  ioff holds
 // the lane's offsets within a record (computed once per launch; lanes past the record carry an

@@ -114,6 +114,10 @@ constexpr int kHotWaves = 12;
 constexpr int kHotMaxConsumers = 4;
 constexpr int kHotMaxProducers = kHotWaves - 1;  // with one consumer
 constexpr int kHotEntriesPerLane = 10;  // producer lanes x this >= batch entries (64 x 10 = 640)
+// Stager lanes x this >= a staged batch's entries (64 x 15 = 960).  Staged batches are larger, so
+// that the hot workgroup's per-batch hand-over (a loader's turn, the consumer's wait and first
+// read) is spread over more consumer steps; the hot set that fits beside such buffers is smaller.
+constexpr int kStagedEntriesPerLane = 15;
 constexpr int kHotFlagBytes = 128;      // LDS words: ready[producer], freed[producer], abort, moved count
 constexpr int kHotScratchBytes = kHotMaxConsumers * 64 * 8;  // write targets of inactive consumer lanes
 constexpr int kHotZeroCells = 64;         // hot-array cells after the hot set, one per consumer lane
@@ -130,6 +134,10 @@ constexpr uint16_t kHotCold = 0xFFFF;    // slot_of value of an entry that is no
 // and its records stay aligned.
 __host__ __device__ constexpr uint32_t hot_buf_words(uint32_t B, uint32_t Smax) {
     return (5u * B + 2u * B * Smax + 3u) & ~3u;
+}
+// Coordinates per batch for rows of Smax entry slots, with `per_lane` entries per producer lane.
+__host__ __device__ constexpr uint32_t hot_batch_cap(uint32_t Smax, uint32_t per_lane) {
+    return 64u * per_lane / Smax < 64u ? 64u * per_lane / Smax : 64u;
 }
 
 // Staged variant of the hot-set epoch: stager workgroups (on the XCD of workgroup 0: workgroups
